@@ -1,0 +1,68 @@
+"""The paper's storage formula and auto-tuner rules reproduce its printed numbers."""
+
+import pytest
+
+from oracle import paper_accounting as pa
+from conftest import read_golden_table
+
+RTX3090_SMS = 82
+MB = 1024 * 1024
+
+
+def printed():
+    return {name: float(value) for name, value, _ in read_golden_table("paper_printed_numbers.txt")}
+
+
+def test_gemv_split_count():
+    assert pa.gemv_ksplit(RTX3090_SMS, 1, 4096) == printed()["gemv_ksplit_rtx3090_4096"]
+
+
+def test_gemm_split_count_and_occupancy():
+    p = printed()
+    splits = pa.gemm_splits(RTX3090_SMS, 128)
+    assert splits == p["gemm_splits_rtx3090_L128"]
+    assert 128 * splits == p["gemm_blocks_rtx3090_L128"]
+    assert round(128 * splits / RTX3090_SMS, 1) == p["gemm_blocks_per_sm_L128"]
+    # split-K is switched off for long prompts (Sec. 4.2)
+    assert pa.gemm_splits(RTX3090_SMS, 512) == 1
+
+
+def test_index_table_sizes():
+    p = printed()
+    assert pa.index_table_bytes(4096 // 2, 4096) / MB == p["index_table_MB_sz2_4096"]
+    assert pa.index_table_bytes(4096 // 1, 4096) / MB == p["index_table_MB_sz1_4096"]
+    assert 4096 * 4096 * 2 / MB == p["fp16_weight_MB_4096"]
+
+
+def test_layer_footprint_formula():
+    # 4096 x 4096 at SZ=2, K_s=256: ids 8 MiB, per-subspace codebooks 2 MiB
+    bits = pa.layer_footprint_bits(256, 2048, 2, 4096)
+    assert bits == 16 * 256 * 4096 + 8 * 2048 * 4096
+    assert bits / 8 / MB == pytest.approx(10.0)
+
+
+def test_codebook_lut_sizes():
+    p = printed()
+    assert pa.subspace_codebook_bytes(256, 2) / 1024 == p["subspace_codebook_KB_ks256_sz2"]
+    assert round(100 * pa.lut_waste_fraction(256), 1) == p["lut_waste_percent_ks256"]
+    assert pa.double_buffered_lut_bytes(256) == 2056
+    assert round(pa.double_buffered_lut_bytes(256) / 1024) == p["lut_pair_KB_ks256"]
+
+
+def test_memory_savings_ratios():
+    p = printed()
+    # the paper prints two decimals; 15317 / 5482 = 2.794 is printed as 2.80
+    assert abs(15317 / 5975 - p["mem_savings_4bit"]) < 0.01
+    assert abs(15317 / 5482 - p["mem_savings_3bit"]) < 0.01
+
+
+@pytest.mark.parametrize("sz,ks,key", [(2, 1024, "effective_bits_2_1024"), (2, 512, "effective_bits_2_512"),
+                                       (2, 256, "effective_bits_2_256"), (2, 128, "effective_bits_2_128")])
+def test_effective_bits(sz, ks, key):
+    assert pa.effective_bits(ks, sz) == printed()[key]
+
+
+def test_effective_bits_of_the_built_workloads():
+    assert pa.effective_bits(256, 2) == 4.0     # d=2, C=256, 8-bit ids
+    assert 12 / 4 == 3.0                        # d=4, C=4096 in 12-bit ids
+    assert pa.effective_bits(65536, 4) == 4.0   # d=4, C=65536, 16-bit ids
