@@ -1,0 +1,134 @@
+/*
+ * fasq.h - product-quantized (PQ) weight matmul for AMD Instinct MI355X (gfx950).
+ *
+ * The operation (FASQ, Sec. 3.1.2, Eq. lut-accumulate; Sec. 2.2):
+ *
+ *   A weight matrix W_hat with N output features and K input features is never
+ *   stored densely.  Each output row n is cut along K into S = K / d
+ *   sub-vectors of length d, and sub-vector s is replaced by the id u(n, s) of
+ *   one of C fp16 codewords:
+ *
+ *       W_hat[n, s*d + i] = codebook[u(n, s) * d + i]        (0 <= i < d)
+ *       y[m, n]           = sum_s dot(x[m, s*d : s*d + d], codebook[u(n, s)])
+ *                         = (x . W_hat^T)[m, n]
+ *
+ *   One codebook is shared by every sub-vector of the matrix (the paper's
+ *   per-subspace tables with all tables equal).
+ *
+ * Layouts (all buffers are DEVICE memory, owned and allocated by the caller):
+ *   x        fp16 [M x K], row-major, contiguous.
+ *   y        fp16 [M x N], row-major, contiguous; every element is written
+ *            (no zeroing needed).  Accumulation is fp32; each output is rounded
+ *            to fp16 (round to nearest even) exactly once.
+ *   codebook fp16 [C x d], row-major.
+ *   idx      N rows of R = fasq_idx_row_bytes(K, d, idx_bits) bytes, back to
+ *            back (row n starts at byte n*R).  Within a row the ids form one
+ *            least-significant-bit-first bit stream: id s occupies stream bits
+ *            [idx_bits*s, idx_bits*s + idx_bits), and stream bit t is bit
+ *            (t mod 8) of byte (t div 8).  So idx_bits = 8 is one byte per id,
+ *            16 a little-endian byte pair, and 12 packs two ids in three bytes
+ *            (b0 = u0 & 0xFF, b1 = (u0 >> 8) | (u1 & 0xF) << 4, b2 = u1 >> 4).
+ *            The pad bits of an odd 12-bit row are ignored.
+ *
+ * Conventions:
+ *   - Every call is asynchronous on `stream` (0 = the null stream).  The
+ *     library keeps no pointer after returning, allocates no device memory,
+ *     and uses no workspace, so the calls may be captured in a hipGraph.
+ *   - Argument checks run before any HIP call.  A bad argument returns
+ *     FASQ_ERR_INVALID_ARG and launches nothing.  A failed launch returns
+ *     FASQ_ERR_HIP.  fasq_last_error() then describes the failure (per calling
+ *     thread).  A fault inside a kernel surfaces at the caller's next
+ *     synchronisation.
+ *   - Preconditions that are NOT checked: every id is < C (an id >= C reads
+ *     outside the codebook); x, y, idx and codebook do not overlap.
+ *   - Calls that share no output buffer may run concurrently from any thread.
+ *   - Results are deterministic: the same inputs give the same bits.
+ */
+#ifndef FASQ_H
+#define FASQ_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FASQ_ABI_VERSION 1
+
+typedef enum {
+  FASQ_OK = 0,
+  FASQ_ERR_INVALID_ARG = 1, /* a size, pointer or format argument is invalid */
+  FASQ_ERR_UNSUPPORTED = 2, /* valid, but no kernel handles this combination */
+  FASQ_ERR_HIP = 3          /* the HIP runtime reported an error */
+} fasq_status;
+
+/*
+ * Decode regime (FASQ Sec. 4.1, the batch-1 GEMV of the decode phase):
+ * y[M x N] = x[M x K] . W_hat^T.  Tuned for M <= 16 (M = 1 is token-by-token
+ * decode); any M >= 1 is accepted and computed correctly.
+ *
+ *   x, M, K     activations, fp16 [M x K]
+ *   N           output features (rows of the index table)
+ *   idx         packed ids, N rows of fasq_idx_row_bytes(K, d, idx_bits) bytes
+ *   idx_bits    8, 12 or 16
+ *   d           sub-vector length, d >= 1, K % d == 0
+ *   codebook, C fp16 [C x d], 1 <= C <= 2^idx_bits
+ *   y           output, fp16 [M x N]
+ *   stream      HIP stream the kernels are queued on
+ *
+ * Returns FASQ_OK, FASQ_ERR_INVALID_ARG (M, K, N < 1; d < 1; K % d != 0;
+ * idx_bits not in {8, 12, 16}; C outside [1, 2^idx_bits]; a NULL pointer) or
+ * FASQ_ERR_HIP.
+ */
+fasq_status fasq_pq_gemv(const void* x, int64_t M, int64_t K, int64_t N,
+                         const void* idx, int idx_bits, int d,
+                         const void* codebook, int64_t C,
+                         void* y, hipStream_t stream);
+
+/*
+ * Prefill regime (FASQ Sec. 4.2: many tokens share one weight matrix).  Same
+ * operation, arguments, layouts and errors as fasq_pq_gemv; built for M in the
+ * tens to thousands.  Weight tiles are decoded from the ids into on-chip
+ * memory and contracted with matrix-core (MFMA) instructions, fp16 inputs,
+ * fp32 accumulation.
+ */
+fasq_status fasq_pq_gemm(const void* x, int64_t M, int64_t K, int64_t N,
+                         const void* idx, int idx_bits, int d,
+                         const void* codebook, int64_t C,
+                         void* y, hipStream_t stream);
+
+/*
+ * Decode W_hat explicitly (the reconstruction the paper's reconstruction-free
+ * kernels avoid, Sec. 3.1.2).  Writes fp16 [N x K] to `w`; every element is a
+ * bit-for-bit copy of a codebook entry (signed zeros, subnormals, NaN
+ * payloads preserved).  Diagnostic only: it is how the decoder is tested.
+ * Errors as for fasq_pq_gemv.
+ */
+fasq_status fasq_pq_reconstruct(const void* idx, int64_t N, int64_t K, int idx_bits, int d,
+                                const void* codebook, int64_t C, void* w,
+                                hipStream_t stream);
+
+/*
+ * Bytes of one packed index row: ceil((K / d) * idx_bits / 8).  Returns -1
+ * when K < 1, d < 1, K % d != 0 or idx_bits is not 8, 12 or 16.  Host only.
+ */
+int64_t fasq_idx_row_bytes(int64_t K, int d, int idx_bits);
+
+/* Static, human-readable name of a status code. */
+const char* fasq_status_string(fasq_status s);
+
+/*
+ * Detail of the calling thread's most recent failed call ("" if none).  The
+ * string stays valid until the thread's next fasq_* call.
+ */
+const char* fasq_last_error(void);
+
+/* FASQ_ABI_VERSION of the built library. */
+int fasq_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FASQ_H */

@@ -1,0 +1,240 @@
+"""Python binding for libfasq, the MI355X product-quantized matmul library.
+
+The binding marshals arguments only: every computation runs in the HIP
+kernels of ``libfasq.so``.  Torch is used for device buffers and streams.
+If the library is not built, every call raises :class:`LibraryNotBuilt`;
+there is no fallback.
+
+Operation (FASQ, Sec. 3.1.2, Eq. lut-accumulate): ``y = x . W_hat^T`` where
+``W_hat[n, s*d + i] = codebook[u(n, s), i]`` and ``u(n, s)`` are packed ids
+(8, 12 or 16 bits, one least-significant-bit-first stream per output row).
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+from typing import Optional
+
+__all__ = [
+    "FasqError",
+    "LibraryNotBuilt",
+    "LIB_PATH",
+    "lib",
+    "library_loaded",
+    "abi_version",
+    "idx_row_bytes",
+    "status_string",
+    "last_error",
+    "pq_gemv",
+    "pq_gemm",
+    "pq_reconstruct",
+    "gemv_raw",
+    "gemm_raw",
+    "reconstruct_raw",
+    "FASQ_OK",
+    "FASQ_ERR_INVALID_ARG",
+    "FASQ_ERR_UNSUPPORTED",
+    "FASQ_ERR_HIP",
+    "EXPORTED_SYMBOLS",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfasq.so")
+
+FASQ_OK = 0
+FASQ_ERR_INVALID_ARG = 1
+FASQ_ERR_UNSUPPORTED = 2
+FASQ_ERR_HIP = 3
+
+EXPORTED_SYMBOLS = (
+    "fasq_pq_gemv",
+    "fasq_pq_gemm",
+    "fasq_pq_reconstruct",
+    "fasq_idx_row_bytes",
+    "fasq_status_string",
+    "fasq_last_error",
+    "fasq_abi_version",
+)
+
+
+class LibraryNotBuilt(ImportError):
+    pass
+
+
+class FasqError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{message} (status {status})")
+        self.status = status
+
+
+_lock = threading.Lock()
+_lib: Optional[ctypes.CDLL] = None
+
+_c_i64 = ctypes.c_int64
+_c_int = ctypes.c_int
+_c_vp = ctypes.c_void_p
+
+
+def lib() -> ctypes.CDLL:
+    """Load ``libfasq.so`` (once) and declare its signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(LIB_PATH):
+            raise LibraryNotBuilt(f"{LIB_PATH} is missing; build it with __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        mm = [_c_vp, _c_i64, _c_i64, _c_i64, _c_vp, _c_int, _c_int, _c_vp, _c_i64, _c_vp, _c_vp]
+        for name in ("fasq_pq_gemv", "fasq_pq_gemm"):
+            f = getattr(L, name)
+            f.argtypes = mm
+            f.restype = _c_int
+        L.fasq_pq_reconstruct.argtypes = [_c_vp, _c_i64, _c_i64, _c_int, _c_int, _c_vp, _c_i64, _c_vp, _c_vp]
+        L.fasq_pq_reconstruct.restype = _c_int
+        L.fasq_idx_row_bytes.argtypes = [_c_i64, _c_int, _c_int]
+        L.fasq_idx_row_bytes.restype = _c_i64
+        L.fasq_status_string.argtypes = [_c_int]
+        L.fasq_status_string.restype = ctypes.c_char_p
+        L.fasq_last_error.argtypes = []
+        L.fasq_last_error.restype = ctypes.c_char_p
+        L.fasq_abi_version.argtypes = []
+        L.fasq_abi_version.restype = _c_int
+        _lib = L
+        return L
+
+
+def library_loaded() -> bool:
+    return _lib is not None
+
+
+def abi_version() -> int:
+    return lib().fasq_abi_version()
+
+
+def idx_row_bytes(K: int, d: int, idx_bits: int) -> int:
+    return lib().fasq_idx_row_bytes(K, d, idx_bits)
+
+
+def status_string(status: int) -> str:
+    return lib().fasq_status_string(status).decode()
+
+
+def last_error() -> str:
+    return lib().fasq_last_error().decode()
+
+
+def _check(status: int) -> None:
+    if status != FASQ_OK:
+        raise FasqError(status, f"{status_string(status)}: {last_error()}")
+
+
+# ---------------------------------------------------------------------------
+# Raw-pointer entry points (integers are device addresses; stream 0 = null)
+# ---------------------------------------------------------------------------
+
+def gemv_raw(x, M, K, N, idx, idx_bits, d, codebook, C, y, stream=0) -> int:
+    return lib().fasq_pq_gemv(x, M, K, N, idx, idx_bits, d, codebook, C, y, stream)
+
+
+def gemm_raw(x, M, K, N, idx, idx_bits, d, codebook, C, y, stream=0) -> int:
+    return lib().fasq_pq_gemm(x, M, K, N, idx, idx_bits, d, codebook, C, y, stream)
+
+
+def reconstruct_raw(idx, N, K, idx_bits, d, codebook, C, w, stream=0) -> int:
+    return lib().fasq_pq_reconstruct(idx, N, K, idx_bits, d, codebook, C, w, stream)
+
+
+# ---------------------------------------------------------------------------
+# Torch-tensor entry points
+# ---------------------------------------------------------------------------
+
+def _torch():
+    import torch
+
+    return torch
+
+
+def _stream_handle(tensor) -> int:
+    torch = _torch()
+    return torch.cuda.current_stream(tensor.device).cuda_stream
+
+
+def _require(t, name, dtype, ndim):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.dim() != ndim:
+        raise ValueError(f"{name} must be {ndim}-D")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _matmul(fn, x, idx, idx_bits, d, codebook, out=None):
+    torch = _torch()
+    _require(x, "x", torch.float16, 2)
+    _require(idx, "idx", torch.uint8, 2)
+    _require(codebook, "codebook", torch.float16, 2)
+    M, K = x.shape
+    N, R = idx.shape
+    C, dd = codebook.shape
+    if dd != d:
+        raise ValueError(f"codebook is [C x {dd}] but d = {d}")
+    want = idx_row_bytes(K, d, idx_bits)
+    if want < 0:
+        raise ValueError("invalid (K, d, idx_bits)")
+    if R != want:
+        raise ValueError(f"idx rows are {R} bytes, expected {want}")
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float16, device=x.device)
+    else:
+        _require(out, "out", torch.float16, 2)
+        if tuple(out.shape) != (M, N):
+            raise ValueError("out must be [M x N]")
+    for t in (idx, codebook, out):
+        if t.device != x.device:
+            raise ValueError("all tensors must be on one device")
+    with torch.cuda.device(x.device):
+        _check(fn(x.data_ptr(), M, K, N, idx.data_ptr(), idx_bits, d, codebook.data_ptr(), C,
+                  out.data_ptr(), _stream_handle(x)))
+    return out
+
+
+def pq_gemv(x, idx, idx_bits: int, d: int, codebook, out=None):
+    """Decode-regime ``y = x . W_hat^T`` (fp16 [M x N]); see ``fasq_pq_gemv``."""
+    return _matmul(lib().fasq_pq_gemv, x, idx, idx_bits, d, codebook, out)
+
+
+def pq_gemm(x, idx, idx_bits: int, d: int, codebook, out=None):
+    """Prefill-regime ``y = x . W_hat^T`` (MFMA path); see ``fasq_pq_gemm``."""
+    return _matmul(lib().fasq_pq_gemm, x, idx, idx_bits, d, codebook, out)
+
+
+def pq_reconstruct(idx, K: int, idx_bits: int, d: int, codebook, out=None):
+    """Explicit ``W_hat`` (fp16 [N x K]), bit copies of codebook entries."""
+    torch = _torch()
+    _require(idx, "idx", torch.uint8, 2)
+    _require(codebook, "codebook", torch.float16, 2)
+    N, R = idx.shape
+    C, dd = codebook.shape
+    if dd != d:
+        raise ValueError(f"codebook is [C x {dd}] but d = {d}")
+    want = idx_row_bytes(K, d, idx_bits)
+    if want < 0 or R != want:
+        raise ValueError(f"idx rows are {R} bytes, expected {want}")
+    if out is None:
+        out = torch.empty((N, K), dtype=torch.float16, device=idx.device)
+    else:
+        _require(out, "out", torch.float16, 2)
+        if tuple(out.shape) != (N, K):
+            raise ValueError("out must be [N x K]")
+    with torch.cuda.device(idx.device):
+        _check(lib().fasq_pq_reconstruct(idx.data_ptr(), N, K, idx_bits, d, codebook.data_ptr(), C,
+                                         out.data_ptr(), _stream_handle(idx)))
+    return out

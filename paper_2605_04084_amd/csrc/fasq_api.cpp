@@ -1,0 +1,184 @@
+// libfasq C ABI: argument validation, kernel selection, error reporting.
+#include "../../include/fasq.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <string>
+
+#include "fasq_internal.h"
+
+namespace fasq {
+
+hipError_t launch_gemv_m1_u8(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
+hipError_t launch_gemv_m1_u12(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
+hipError_t launch_gemv_m1_u16(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
+
+hipError_t launch_gemv_m1(const Problem& p, const DeviceInfo& dev, hipStream_t stream) {
+  switch (p.idx_bits) {
+    case 8: return launch_gemv_m1_u8(p, dev, stream);
+    case 12: return launch_gemv_m1_u12(p, dev, stream);
+    default: return launch_gemv_m1_u16(p, dev, stream);
+  }
+}
+
+namespace {
+
+thread_local std::string t_last_error;
+
+constexpr int kMaxDevices = 64;
+std::mutex g_dev_mutex;
+DeviceInfo g_dev[kMaxDevices];
+
+fasq_status fail(fasq_status s, const std::string& msg) {
+  t_last_error = msg;
+  return s;
+}
+
+fasq_status hip_fail(const char* what, hipError_t e) {
+  std::string m = what;
+  m += ": ";
+  m += hipGetErrorString(e);
+  return fail(FASQ_ERR_HIP, m);
+}
+
+// Validation shared by the three compute entry points.  No HIP call is made.
+fasq_status validate(int64_t M, int64_t K, int64_t N, int idx_bits, int d, int64_t C, const void* x,
+                     const void* idx, const void* codebook, const void* y, bool need_x) {
+  if (M < 1 || K < 1 || N < 1) return fail(FASQ_ERR_INVALID_ARG, "M, K and N must be >= 1");
+  if (d < 1) return fail(FASQ_ERR_INVALID_ARG, "d must be >= 1");
+  if (K % d != 0) return fail(FASQ_ERR_INVALID_ARG, "K must be a multiple of d");
+  if (idx_bits != 8 && idx_bits != 12 && idx_bits != 16)
+    return fail(FASQ_ERR_INVALID_ARG, "idx_bits must be 8, 12 or 16");
+  if (C < 1 || C > (int64_t(1) << idx_bits))
+    return fail(FASQ_ERR_INVALID_ARG, "C must lie in [1, 2^idx_bits]");
+  if ((need_x && x == nullptr) || idx == nullptr || codebook == nullptr || y == nullptr)
+    return fail(FASQ_ERR_INVALID_ARG, "a buffer pointer is NULL");
+  // the largest flat index any kernel forms must fit in int64
+  if (M > (int64_t(1) << 40) / K || N > (int64_t(1) << 40) / K)
+    return fail(FASQ_ERR_INVALID_ARG, "problem too large");
+  return FASQ_OK;
+}
+
+Problem make_problem(const void* x, int64_t M, int64_t K, int64_t N, const void* idx, int idx_bits, int d,
+                     const void* codebook, int64_t C, void* y) {
+  Problem p;
+  p.x = x;
+  p.M = M;
+  p.K = K;
+  p.N = N;
+  p.idx = idx;
+  p.idx_bits = idx_bits;
+  p.d = d;
+  p.codebook = codebook;
+  p.C = C;
+  p.y = y;
+  p.S = K / d;
+  p.R = (p.S * idx_bits + 7) / 8;
+  return p;
+}
+
+enum class Regime { kGemv, kGemm };
+
+fasq_status run(const Problem& p, Regime regime, hipStream_t stream) {
+  DeviceInfo dev;
+  hipError_t e = device_info(&dev);
+  if (e != hipSuccess) return hip_fail("querying the current device", e);
+  e = hipErrorNotSupported;
+  if (!force_generic()) {
+    if (regime == Regime::kGemv && p.M == 1) e = launch_gemv_m1(p, dev, stream);
+    if (e == hipErrorNotSupported) e = launch_gemm_mfma(p, dev, stream);
+  }
+  if (e == hipErrorNotSupported) e = launch_generic(p, stream);
+  if (e != hipSuccess) return hip_fail("kernel launch", e);
+  t_last_error.clear();
+  return FASQ_OK;
+}
+
+}  // namespace
+
+hipError_t device_info(DeviceInfo* out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev >= 0 && dev < kMaxDevices) {
+    std::lock_guard<std::mutex> lock(g_dev_mutex);
+    if (g_dev[dev].device == dev) {
+      *out = g_dev[dev];
+      return hipSuccess;
+    }
+  }
+  DeviceInfo info;
+  info.device = dev;
+  e = hipDeviceGetAttribute(&info.num_cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  e = hipDeviceGetAttribute(&info.lds_per_block, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+  if (e != hipSuccess) return e;
+  if (dev >= 0 && dev < kMaxDevices) {
+    std::lock_guard<std::mutex> lock(g_dev_mutex);
+    g_dev[dev] = info;
+  }
+  *out = info;
+  return hipSuccess;
+}
+
+bool force_generic() {
+  const char* v = std::getenv("FASQ_FORCE_PATH");
+  return v != nullptr && std::strcmp(v, "generic") == 0;
+}
+
+}  // namespace fasq
+
+using fasq::Problem;
+
+extern "C" {
+
+fasq_status fasq_pq_gemv(const void* x, int64_t M, int64_t K, int64_t N, const void* idx, int idx_bits, int d,
+                         const void* codebook, int64_t C, void* y, hipStream_t stream) {
+  fasq_status s = fasq::validate(M, K, N, idx_bits, d, C, x, idx, codebook, y, true);
+  if (s != FASQ_OK) return s;
+  return fasq::run(fasq::make_problem(x, M, K, N, idx, idx_bits, d, codebook, C, y), fasq::Regime::kGemv, stream);
+}
+
+fasq_status fasq_pq_gemm(const void* x, int64_t M, int64_t K, int64_t N, const void* idx, int idx_bits, int d,
+                         const void* codebook, int64_t C, void* y, hipStream_t stream) {
+  fasq_status s = fasq::validate(M, K, N, idx_bits, d, C, x, idx, codebook, y, true);
+  if (s != FASQ_OK) return s;
+  return fasq::run(fasq::make_problem(x, M, K, N, idx, idx_bits, d, codebook, C, y), fasq::Regime::kGemm, stream);
+}
+
+fasq_status fasq_pq_reconstruct(const void* idx, int64_t N, int64_t K, int idx_bits, int d, const void* codebook,
+                                int64_t C, void* w, hipStream_t stream) {
+  fasq_status s = fasq::validate(1, K, N, idx_bits, d, C, nullptr, idx, codebook, w, false);
+  if (s != FASQ_OK) return s;
+  Problem p = fasq::make_problem(nullptr, 1, K, N, idx, idx_bits, d, codebook, C, nullptr);
+  hipError_t e = fasq::launch_reconstruct(p, w, stream);
+  if (e != hipSuccess) return fasq::hip_fail("kernel launch", e);
+  fasq::t_last_error.clear();
+  return FASQ_OK;
+}
+
+int64_t fasq_idx_row_bytes(int64_t K, int d, int idx_bits) {
+  if (K < 1 || d < 1 || K % d != 0) return -1;
+  if (idx_bits != 8 && idx_bits != 12 && idx_bits != 16) return -1;
+  return (K / d * idx_bits + 7) / 8;
+}
+
+const char* fasq_status_string(fasq_status s) {
+  switch (s) {
+    case FASQ_OK: return "FASQ_OK";
+    case FASQ_ERR_INVALID_ARG: return "FASQ_ERR_INVALID_ARG";
+    case FASQ_ERR_UNSUPPORTED: return "FASQ_ERR_UNSUPPORTED";
+    case FASQ_ERR_HIP: return "FASQ_ERR_HIP";
+  }
+  return "FASQ_UNKNOWN_STATUS";
+}
+
+const char* fasq_last_error(void) { return fasq::t_last_error.c_str(); }
+
+int fasq_abi_version(void) { return FASQ_ABI_VERSION; }
+
+}  // extern "C"

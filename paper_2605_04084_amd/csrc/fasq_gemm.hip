@@ -1,0 +1,89 @@
+// Prefill GEMM kernels: variant selection and launch.
+#include "fasq_gemm_mfma.h"
+#include "fasq_gemv_m1_launch.h"
+
+namespace fasq {
+
+namespace {
+
+template <int BITS, int D, int MODE, int BM, int BN>
+hipError_t launch_gemm_variant(const GemmArgs& a, int lds, hipStream_t stream) {
+  auto kern = k_gemm_mfma<BITS, D, MODE, BM, BN>;
+  hipError_t e = allow_lds(kern, lds);
+  if (e != hipSuccess) return e;
+  dim3 grid((unsigned)((a.N + BN - 1) / BN), (unsigned)((a.M + BM - 1) / BM));
+  hipLaunchKernelGGL(kern, grid, dim3(256), lds, stream, a);
+  return hipGetLastError();
+}
+
+template <int BITS, int D>
+hipError_t launch_gemm_mode(const GemmArgs& a, int mode, int lds, hipStream_t stream) {
+  switch (mode) {
+    case CB_REPL: return launch_gemm_variant<BITS, D, CB_REPL, 128, 128>(a, lds, stream);
+    case CB_LDS: return launch_gemm_variant<BITS, D, CB_LDS, 128, 128>(a, lds, stream);
+    default: return launch_gemm_variant<BITS, D, CB_GLOBAL, 128, 128>(a, lds, stream);
+  }
+}
+
+template <int BITS>
+hipError_t launch_gemm_bits(const GemmArgs& a, int d, int mode, int lds, hipStream_t stream) {
+  switch (d) {
+    case 1: return launch_gemm_mode<BITS, 1>(a, mode, lds, stream);
+    case 2: return launch_gemm_mode<BITS, 2>(a, mode, lds, stream);
+    case 4: return launch_gemm_mode<BITS, 4>(a, mode, lds, stream);
+    default:
+      if constexpr (BITS == 12) return hipErrorNotSupported;  // 4 ids = 6 bytes: not dword aligned
+      else return launch_gemm_mode<BITS, 8>(a, mode, lds, stream);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t stream) {
+  const int d = p.d;
+  if (!(d == 1 || d == 2 || d == 4 || d == 8)) return hipErrorNotSupported;
+  if (p.idx_bits == 12 && d == 8) return hipErrorNotSupported;
+  if (p.K % kGemmKC) return hipErrorNotSupported;
+  if (p.R * 8 != p.S * p.idx_bits) return hipErrorNotSupported;
+  if ((reinterpret_cast<uintptr_t>(p.x) & 15) || (reinterpret_cast<uintptr_t>(p.codebook) & 15) ||
+      (reinterpret_cast<uintptr_t>(p.idx) & 15) || (p.R & 3))
+    return hipErrorNotSupported;
+  // per-lane index runs are read as 16/8/4-byte words: they must be aligned so
+  const int hb = (32 / d) * p.idx_bits / 8;
+  const int align = (hb % 16 == 0) ? 16 : (hb % 8 == 0) ? 8 : 4;
+  if (p.R % align) return hipErrorNotSupported;
+
+  int mode, cb_bytes;
+  const int64_t repl = p.C * (int64_t)(d <= 2 ? 128 : 256);
+  if (repl <= kLdsCodebookBudget) {
+    mode = CB_REPL;
+    cb_bytes = (int)repl;
+  } else if (p.C * d * 2 <= kLdsCodebookBudget) {
+    mode = CB_LDS;
+    cb_bytes = (int)((p.C * d * 2 + 15) / 16 * 16);
+  } else {
+    mode = CB_GLOBAL;
+    cb_bytes = 0;
+  }
+  const int lds = cb_bytes + 2 * 128 * kXRowBytes;
+  if (lds > dev.lds_per_block) return hipErrorNotSupported;
+
+  GemmArgs a;
+  a.x = static_cast<const half_t*>(p.x);
+  a.M = p.M;
+  a.K = p.K;
+  a.N = p.N;
+  a.idx = static_cast<const uint8_t*>(p.idx);
+  a.R = p.R;
+  a.cb = static_cast<const half_t*>(p.codebook);
+  a.C = (int)p.C;
+  a.cb_lds_bytes = cb_bytes;
+  a.y = static_cast<half_t*>(p.y);
+  switch (p.idx_bits) {
+    case 8: return launch_gemm_bits<8>(a, d, mode, lds, stream);
+    case 12: return launch_gemm_bits<12>(a, d, mode, lds, stream);
+    default: return launch_gemm_bits<16>(a, d, mode, lds, stream);
+  }
+}
+
+}  // namespace fasq

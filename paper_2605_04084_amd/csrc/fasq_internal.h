@@ -1,0 +1,46 @@
+// Host-side declarations shared by the libfasq sources (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fasq {
+
+// One validated call: y[M x N] = x[M x K] . W_hat^T.
+struct Problem {
+  const void* x;
+  int64_t M, K, N;
+  const void* idx;
+  int idx_bits;
+  int d;
+  const void* codebook;
+  int64_t C;
+  void* y;
+  int64_t S;  // sub-vectors per row, K / d
+  int64_t R;  // bytes per packed index row
+};
+
+// Properties of the current device, read once per device and cached.
+struct DeviceInfo {
+  int device = -1;
+  int num_cus = 0;
+  int lds_per_block = 0;  // bytes of LDS one workgroup may use
+};
+hipError_t device_info(DeviceInfo* out);
+
+// Launchers.  Each returns hipSuccess or the launch error; none synchronizes.
+hipError_t launch_reconstruct(const Problem& p, void* w, hipStream_t stream);
+hipError_t launch_generic(const Problem& p, hipStream_t stream);
+
+// Tuned decode kernel for M == 1.  Returns hipErrorNotSupported (without
+// launching) when no tuned variant applies.
+hipError_t launch_gemv_m1(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
+
+// Tuned MFMA prefill kernel.  hipErrorNotSupported when no variant applies.
+hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
+
+// Environment overrides used by tests and ablations: FASQ_FORCE_PATH=generic
+// makes every call take the general kernel.
+bool force_generic();
+
+}  // namespace fasq

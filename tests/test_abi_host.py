@@ -1,0 +1,112 @@
+"""Host-side checks of the C ABI: the library loads, exports every declared
+symbol, and rejects bad arguments before touching the GPU."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2605_04084_amd as fasq
+from conftest import ROOT
+
+HEADER = os.path.join(ROOT, "include", "fasq.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(fasq.LIB_PATH):
+        from paper_2605_04084_amd import _build
+
+        _build.build()
+    return fasq.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fasq_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_binding_symbols():
+    assert declared_functions() == sorted(fasq.EXPORTED_SYMBOLS)
+
+
+def test_every_declared_symbol_is_exported(L):
+    for name in declared_functions():
+        assert hasattr(L, name), name
+        assert ctypes.cast(getattr(L, name), ctypes.c_void_p).value
+
+
+def test_abi_version(L):
+    assert fasq.abi_version() == 1
+
+
+def test_status_strings(L):
+    assert fasq.status_string(0) == "FASQ_OK"
+    assert fasq.status_string(1) == "FASQ_ERR_INVALID_ARG"
+    assert fasq.status_string(2) == "FASQ_ERR_UNSUPPORTED"
+    assert fasq.status_string(3) == "FASQ_ERR_HIP"
+    assert fasq.status_string(99) == "FASQ_UNKNOWN_STATUS"
+
+
+@pytest.mark.parametrize("K,d,bits,R", [(4096, 2, 8, 2048), (4096, 4, 12, 1536), (4096, 4, 16, 2048),
+                                        (14336, 2, 8, 7168), (12, 4, 12, 5), (256, 4, 8, 64), (7, 7, 8, 1),
+                                        (10, 3, 8, -1), (0, 1, 8, -1), (8, 0, 8, -1), (8, 2, 10, -1)])
+def test_idx_row_bytes(L, K, d, bits, R):
+    assert fasq.idx_row_bytes(K, d, bits) == R
+
+
+DUMMY = 0x1000  # never dereferenced: validation fails first
+
+
+@pytest.mark.parametrize("entry", ["gemv", "gemm"])
+@pytest.mark.parametrize("args,why", [
+    (dict(M=0), "M, K and N"),
+    (dict(K=0), "M, K and N"),
+    (dict(N=-1), "M, K and N"),
+    (dict(d=0), "d must"),
+    (dict(K=10, d=4), "multiple of d"),
+    (dict(idx_bits=10), "idx_bits"),
+    (dict(C=0), "C must"),
+    (dict(C=257), "C must"),
+    (dict(idx_bits=12, C=4097), "C must"),
+    (dict(x=0), "NULL"),
+    (dict(idx=0), "NULL"),
+    (dict(codebook=0), "NULL"),
+    (dict(y=0), "NULL"),
+])
+def test_invalid_arguments_rejected_without_launch(L, entry, args, why):
+    a = dict(x=DUMMY, M=1, K=16, N=4, idx=DUMMY, idx_bits=8, d=2, codebook=DUMMY, C=256, y=DUMMY)
+    a.update(args)
+    fn = fasq.gemv_raw if entry == "gemv" else fasq.gemm_raw
+    st = fn(a["x"], a["M"], a["K"], a["N"], a["idx"], a["idx_bits"], a["d"], a["codebook"], a["C"], a["y"], 0)
+    assert st == fasq.FASQ_ERR_INVALID_ARG
+    assert why in fasq.last_error()
+
+
+def test_reconstruct_validation(L):
+    st = fasq.reconstruct_raw(DUMMY, 4, 10, 8, 4, DUMMY, 16, DUMMY, 0)
+    assert st == fasq.FASQ_ERR_INVALID_ARG
+    st = fasq.reconstruct_raw(0, 4, 8, 8, 4, DUMMY, 16, DUMMY, 0)
+    assert st == fasq.FASQ_ERR_INVALID_ARG
+    st = fasq.reconstruct_raw(DUMMY, 4, 8, 16, 4, DUMMY, 70000, DUMMY, 0)
+    assert st == fasq.FASQ_ERR_INVALID_ARG
+
+
+def test_python_binding_rejects_host_tensors(L):
+    torch = pytest.importorskip("torch")
+    x = torch.zeros((1, 16), dtype=torch.float16)
+    idx = torch.zeros((4, 8), dtype=torch.uint8)
+    cb = torch.zeros((256, 2), dtype=torch.float16)
+    with pytest.raises(ValueError):
+        fasq.pq_gemv(x, idx, 8, 2, cb)
+
+
+def test_binding_has_no_cpu_compute_path():
+    """The binding module must not import or reference the oracle."""
+    src = open(os.path.join(ROOT, "paper_2605_04084_amd", "__init__.py")).read()
+    assert "oracle" not in src.replace("Oracle", "")
+    for f in os.listdir(os.path.join(ROOT, "paper_2605_04084_amd", "csrc")):
+        text = open(os.path.join(ROOT, "paper_2605_04084_amd", "csrc", f)).read()
+        assert "oracle" not in text.lower(), f

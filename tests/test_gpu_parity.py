@@ -1,0 +1,289 @@
+"""GPU parity: libfasq (through the C ABI) against the CPU oracle.
+
+Index decoding and reconstruction must match bit for bit; y must satisfy
+rel_L2 <= 1e-3 and max|err| <= 1e-2 * rms(y_ref); structured inputs whose
+exact result fits fp16 must match bit for bit.  Full-size workloads are
+checked on sampled output rows.
+"""
+
+import os
+
+import numpy as np
+import pytest
+
+import pq_inputs as pi
+from oracle import pq_oracle as orc
+from gpu_util import assert_close, sample_rows, to_dev, to_np
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+fasq = pytest.importorskip("paper_2605_04084_amd")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    fasq.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def run(entry, p, x=None):
+    fn = fasq.pq_gemv if entry == "gemv" else fasq.pq_gemm
+    x = p.x if x is None else x
+    y = fn(to_dev(x), to_dev(p.idx), p.idx_bits, p.d, to_dev(p.codebook))
+    return to_np(y).astype(np.float64)
+
+
+# ---------------------------------------------------------------------------
+# Reconstruction: bit-exact
+# ---------------------------------------------------------------------------
+
+RECON_CASES = [
+    # N, K, d, C, bits
+    (37, 64, 1, 256, 8),
+    (129, 256, 2, 256, 8),
+    (5, 12, 3, 7, 8),
+    (64, 96, 4, 4096, 12),
+    (33, 36, 4, 4096, 12),   # S = 9: odd 12-bit rows with a pad nibble
+    (70, 56, 8, 100, 12),
+    (17, 40, 4, 65536, 16),
+    (300, 128, 2, 3000, 16),
+]
+
+
+@pytest.mark.parametrize("case", RECON_CASES)
+def test_reconstruct_bit_exact(case):
+    N, K, d, C, bits = case
+    print(f"[case] reconstruct {case}", flush=True)
+    rng = np.random.default_rng(sum(case))
+    p = pi.draw_problem(rng, 1, K, N, d, C, bits)
+    w = fasq.pq_reconstruct(to_dev(p.idx), K, bits, d, to_dev(p.codebook))
+    ref = orc.reconstruct(p.idx, K, bits, d, p.codebook)
+    assert np.array_equal(to_np(w).view(np.uint16), ref.view(np.uint16))
+
+
+def test_reconstruct_preserves_special_values():
+    specials = np.array([0x0000, 0x8000, 0x0001, 0x8001, 0x03FF, 0x83FF, 0x7C00, 0xFC00,
+                         0x7E01, 0xFE55, 0x3C00, 0xBC00, 0x0200, 0x8200, 0x7BFF, 0xFBFF], dtype=np.uint16)
+    cb = specials.view(np.float16).reshape(4, 4)
+    rng = np.random.default_rng(5)
+    ids = rng.integers(0, 4, size=(50, 24))
+    for bits in (8, 12, 16):
+        idx = pi.pack_indices(ids, bits)
+        w = fasq.pq_reconstruct(to_dev(idx), 96, bits, 4, to_dev(cb))
+        ref = orc.reconstruct(idx, 96, bits, 4, cb)
+        assert np.array_equal(to_np(w).view(np.uint16), ref.view(np.uint16))
+
+
+@pytest.mark.parametrize("wl,mat", [("llama3_8b_4bit", 4), ("llama3_8b_3bit", 7), ("qwen3_8b_sweep", 6)])
+def test_reconstruct_full_size_sampled(wl, mat):
+    print(f"[case] reconstruct full {wl} matrix {mat}", flush=True)
+    p = pi.workload(wl).problem(mat)
+    w = fasq.pq_reconstruct(to_dev(p.idx), p.K, p.idx_bits, p.d, to_dev(p.codebook))
+    rows = sample_rows(p.N, 64)
+    got = to_np(w[torch.from_numpy(rows).to(w.device)]).view(np.uint16)
+    ref = orc.reconstruct(p.idx, p.K, p.idx_bits, p.d, p.codebook, rows=rows).view(np.uint16)
+    assert np.array_equal(got, ref)
+
+
+# ---------------------------------------------------------------------------
+# y on the named workloads (full size, sampled rows)
+# ---------------------------------------------------------------------------
+
+def test_gemv_tiny_workload():
+    p = pi.workload("tiny").problem(0)
+    y = run("gemv", p)
+    assert_close(y, orc.pq_linear(p.x, p.idx, 8, 4, p.codebook), "tiny")
+
+
+@pytest.mark.parametrize("mat", range(7))
+def test_gemv_llama3_8b_4bit(mat):
+    w = pi.workload("llama3_8b_4bit")
+    print(f"[case] gemv 4bit {w.matrices[mat]}", flush=True)
+    p = w.problem(mat)
+    y = run("gemv", p)
+    rows = sample_rows(p.N)
+    assert_close(y[:, rows], orc.pq_linear(p.x, p.idx, p.idx_bits, p.d, p.codebook, rows=rows),
+                 f"4bit {w.matrices[mat].name}")
+
+
+@pytest.mark.parametrize("mat", range(8))
+def test_gemv_llama3_8b_3bit(mat):
+    w = pi.workload("llama3_8b_3bit")
+    print(f"[case] gemv 3bit {w.matrices[mat]}", flush=True)
+    p = w.problem(mat)
+    y = run("gemv", p)
+    rows = sample_rows(p.N)
+    assert_close(y[:, rows], orc.pq_linear(p.x, p.idx, p.idx_bits, p.d, p.codebook, rows=rows),
+                 f"3bit {w.matrices[mat].name}")
+
+
+@pytest.mark.parametrize("M", [1, 4, 16])
+@pytest.mark.parametrize("mat", [0, 1, 4, 6])
+def test_gemv_qwen3_8b_sweep(M, mat):
+    w = pi.workload("qwen3_8b_sweep")
+    print(f"[case] gemv qwen M={M} {w.matrices[mat]}", flush=True)
+    p = w.problem(mat, M=M)
+    y = run("gemv", p)
+    rows = sample_rows(p.N)
+    assert_close(y[:, rows], orc.pq_linear(p.x, p.idx, p.idx_bits, p.d, p.codebook, rows=rows),
+                 f"qwen M={M} {w.matrices[mat].name}")
+
+
+@pytest.mark.parametrize("M", [128, 512, 2048])
+@pytest.mark.parametrize("mat", range(3))
+def test_gemm_prefill(M, mat):
+    w = pi.workload("prefill")
+    print(f"[case] gemm prefill M={M} {w.matrices[mat]}", flush=True)
+    p = w.problem(mat, M=M)
+    y = run("gemm", p)
+    rows = sample_rows(p.N, 128)
+    assert_close(y[:, rows], orc.pq_linear(p.x, p.idx, p.idx_bits, p.d, p.codebook, rows=rows),
+                 f"prefill M={M} {w.matrices[mat].name}")
+
+
+# ---------------------------------------------------------------------------
+# Ragged and small shapes, every id width and sub-vector length
+# ---------------------------------------------------------------------------
+
+RAGGED = [
+    # M, K, N, d, C, bits
+    (1, 256, 129, 2, 256, 8),
+    (1, 4096 + 512, 1000, 2, 256, 8),   # row not a multiple of the per-wave span
+    (1, 320, 77, 4, 256, 8),
+    (1, 1024, 33, 1, 256, 8),
+    (1, 2048, 50, 8, 256, 8),
+    (1, 128 * 12, 260, 4, 4096, 12),
+    (1, 4096, 31, 2, 4096, 12),
+    (1, 4096, 45, 4, 65536, 16),
+    (1, 512, 64, 2, 1000, 16),
+    (1, 36, 5, 4, 9, 12),               # odd 12-bit rows: general kernel
+    (1, 30, 7, 3, 11, 8),               # d = 3: general kernel
+    (1, 24, 9, 24, 40, 8),              # full vector quantization, d = K
+    (3, 256, 100, 4, 256, 8),
+    (5, 192, 70, 2, 256, 8),
+    (17, 640, 200, 4, 256, 8),
+    (37, 320, 130, 2, 300, 16),
+    (64, 128, 64, 8, 256, 8),
+    (130, 256, 257, 4, 4096, 12),
+    (33, 64, 50, 1, 256, 8),
+]
+
+
+@pytest.mark.parametrize("entry", ["gemv", "gemm"])
+@pytest.mark.parametrize("case", RAGGED)
+def test_ragged_shapes(entry, case):
+    M, K, N, d, C, bits = case
+    print(f"[case] {entry} ragged {case}", flush=True)
+    rng = np.random.default_rng(sum(case) + (entry == "gemm"))
+    p = pi.draw_problem(rng, M, K, N, d, C, bits)
+    y = run(entry, p)
+    assert_close(y, orc.pq_linear(p.x, p.idx, bits, d, p.codebook), f"{entry} {case}")
+
+
+# ---------------------------------------------------------------------------
+# Exact cases, determinism, path invariance, alignment, linearity
+# ---------------------------------------------------------------------------
+
+ONE_HOT = [
+    (1, 4096, 300, 2, 256, 8),
+    (1, 4096, 100, 4, 4096, 12),
+    (1, 2048, 64, 4, 65536, 16),
+    (1, 1024, 70, 1, 256, 8),
+    (1, 2048, 40, 8, 256, 8),
+    (16, 4096, 64, 4, 65536, 16),
+    (200, 1024, 150, 4, 256, 8),
+]
+
+
+@pytest.mark.parametrize("entry", ["gemv", "gemm"])
+@pytest.mark.parametrize("case", ONE_HOT)
+def test_signed_one_hot_is_bit_exact(entry, case):
+    """Codewords in {0, +-1} and x in {-1, 0, 1}: every partial sum is a small
+    integer, so the kernels must reproduce the oracle exactly."""
+    M, K, N, d, C, bits = case
+    rng = np.random.default_rng(77 + sum(case))
+    cb = pi.signed_one_hot_codebook(C, d, rng)
+    ids = rng.integers(0, C, size=(N, K // d))
+    x = pi.ternary_x(rng, M, K)
+    idx = pi.pack_indices(ids, bits)
+    ref = orc.pq_linear(x, idx, bits, d, cb)
+    assert np.abs(ref).max() <= 2048
+    fn = fasq.pq_gemv if entry == "gemv" else fasq.pq_gemm
+    y = to_np(fn(to_dev(x), to_dev(idx), bits, d, to_dev(cb))).astype(np.float64)
+    assert np.array_equal(y, ref)
+
+
+@pytest.mark.parametrize("entry", ["gemv", "gemm"])
+def test_repeated_launches_are_bitwise_identical(entry):
+    p = pi.workload("llama3_8b_4bit").problem(4) if entry == "gemv" else pi.workload("prefill").problem(0, M=128)
+    x, idx, cb = to_dev(p.x), to_dev(p.idx), to_dev(p.codebook)
+    fn = fasq.pq_gemv if entry == "gemv" else fasq.pq_gemm
+    a = fn(x, idx, p.idx_bits, p.d, cb)
+    b = fn(x, idx, p.idx_bits, p.d, cb)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+@pytest.mark.parametrize("case", [(1, 4096, 1024, 2, 256, 8), (1, 4096, 512, 4, 4096, 12),
+                                  (4, 4096, 300, 4, 65536, 16), (96, 512, 200, 4, 256, 8)])
+def test_tuned_kernels_match_general_kernel(case, monkeypatch):
+    M, K, N, d, C, bits = case
+    rng = np.random.default_rng(3 + sum(case))
+    p = pi.draw_problem(rng, M, K, N, d, C, bits)
+    fast = run("gemv", p)
+    monkeypatch.setenv("FASQ_FORCE_PATH", "generic")
+    slow = run("gemv", p)
+    ref = orc.pq_linear(p.x, p.idx, bits, d, p.codebook)
+    assert_close(fast, ref, "tuned")
+    assert_close(slow, ref, "general")
+
+
+@pytest.mark.parametrize("entry", ["gemv", "gemm"])
+def test_unaligned_buffers_take_a_correct_path(entry):
+    rng = np.random.default_rng(8)
+    M, K, N, d, C, bits = (1 if entry == "gemv" else 40), 1024, 96, 2, 256, 8
+    p = pi.draw_problem(rng, M, K, N, d, C, bits)
+    # offset every buffer by a few bytes inside a larger allocation
+    xb = torch.zeros(M * K + 1, dtype=torch.float16, device="cuda:0")
+    xb[1:].copy_(to_dev(p.x).view(-1))
+    ib = torch.zeros(p.idx.size + 3, dtype=torch.uint8, device="cuda:0")
+    ib[3:].copy_(to_dev(p.idx).view(-1))
+    cbb = torch.zeros(C * d + 1, dtype=torch.float16, device="cuda:0")
+    cbb[1:].copy_(to_dev(p.codebook).view(-1))
+    yb = torch.zeros(M * N + 1, dtype=torch.float16, device="cuda:0")
+    fn = fasq.gemv_raw if entry == "gemv" else fasq.gemm_raw
+    st = fn(xb.data_ptr() + 2, M, K, N, ib.data_ptr() + 3, bits, d, cbb.data_ptr() + 2, C,
+            yb.data_ptr() + 2, torch.cuda.current_stream().cuda_stream)
+    assert st == fasq.FASQ_OK
+    y = to_np(yb[1:]).astype(np.float64).reshape(M, N)
+    assert_close(y, orc.pq_linear(p.x, p.idx, bits, d, p.codebook), f"unaligned {entry}")
+
+
+def test_linearity_in_x_on_gpu():
+    rng = np.random.default_rng(9)
+    p = pi.draw_problem(rng, 1, 4096, 512, 2, 256, 8)
+    x1 = (rng.integers(-8, 9, size=(1, 4096)) / 8).astype(np.float16)
+    x2 = (rng.integers(-8, 9, size=(1, 4096)) / 8).astype(np.float16)
+    y1 = run("gemv", p, x1)
+    y2 = run("gemv", p, x2)
+    y12 = run("gemv", p, (x1.astype(np.float64) + x2).astype(np.float16))
+    ref = orc.pq_linear(x1.astype(np.float64) + x2, p.idx, 8, 2, p.codebook)
+    assert_close(y12, ref, "x1+x2")
+    assert_close(y1 + y2, ref, "y(x1)+y(x2)")
+
+
+def test_errors_surface_as_exceptions():
+    x = torch.zeros((1, 16), dtype=torch.float16, device="cuda:0")
+    idx = torch.zeros((4, 8), dtype=torch.uint8, device="cuda:0")
+    cb = torch.zeros((256, 2), dtype=torch.float16, device="cuda:0")
+    with pytest.raises(ValueError):
+        fasq.pq_gemv(x, idx[:, :4], 8, 2, cb)          # wrong row bytes
+    with pytest.raises(TypeError):
+        fasq.pq_gemv(x.float(), idx, 8, 2, cb)
+    with pytest.raises(ValueError):
+        fasq.pq_gemv(torch.zeros((16, 2), dtype=torch.float16, device="cuda:0").t(), idx, 8, 2, cb)
+    st = fasq.gemv_raw(x.data_ptr(), 1, 16, 4, idx.data_ptr(), 8, 2, cb.data_ptr(), 300, x.data_ptr(), 0)
+    assert st == fasq.FASQ_ERR_INVALID_ARG
