@@ -1,0 +1,391 @@
+#!/usr/bin/env python3
+"""Benchmark of the PQ matmul hot path on one MI355X.
+
+One step = one Llama-3-8B decoder layer of decode GEMVs at effective 4 bits
+(q, k, v, o, gate, up, down; M = 1, d = 2, C = 256, 8-bit ids), every matrix
+read cold from HBM: the inputs are rotated over enough distinct copies
+(>= 1 GiB) that the 256 MB Infinity Cache cannot serve them.
+
+The timed region replays one HIP graph per step (the seven launches of one
+layer, as deployed).  Separately, every launch is bracketed with HIP events
+on the launch stream (behind a spin kernel, so that host launch latency does
+not enter the measurement) to get per-kernel durations: these give the
+roofline figures and the kernel-sum microseconds per layer.
+
+Also reported: the effective 3-bit layer plus lm_head (d = 4, C = 4096,
+12-bit ids) and the prefill GEMM (M = 128 / 512 / 2048 tokens, d = 4,
+C = 256, 8-bit ids) in TFLOP/s.  --sweep adds the Qwen3-8B decode sweep
+(M = 1, 4, 16; C = 65536, 16-bit ids, codebook in L2).
+
+Algorithmic bytes of one GEMV: N*R (packed ids) + C*d*2 (codebook) +
+M*K*2 (x) + M*N*2 (y); flops of one GEMM: 2*M*N*K.
+
+Prints ONE JSON line on stdout; progress goes to stderr.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+FP16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 matrix peak
+METRIC = "PQ GEMV HBM GB/s (% of peak) + us per Llama-3-8B layer; prefill PQ GEMM TFLOP/s"
+ROTATION_BYTES = 1 << 30
+SPACER_CYCLES = 2_000_000      # spin kernel queued ahead of event-timed launches
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def gemv_bytes(M, K, N, d, C, bits):
+    R = (K // d * bits + 7) // 8
+    return N * R + C * d * 2 + M * K * 2 + M * N * 2
+
+
+# ---------------------------------------------------------------------------
+# A set of matrices with rotating device copies
+# ---------------------------------------------------------------------------
+
+class MatrixSet:
+    """Device copies of a list of PQ problems, rotated to defeat the MALL."""
+
+    def __init__(self, torch, fasq, problems, names, entry, min_copies=1, rotation_bytes=ROTATION_BYTES):
+        self.torch, self.fasq = torch, fasq
+        self.problems, self.names, self.entry = problems, names, entry
+        self.bytes_per_set = sum(gemv_bytes(p.M, p.K, p.N, p.d, p.C, p.idx_bits) for p in problems)
+        self.copies = max(min_copies, math.ceil(rotation_bytes / self.bytes_per_set) + 1)
+        dev = torch.device("cuda:0")
+        base = []
+        for p in problems:
+            base.append(dict(
+                x=torch.from_numpy(p.x).to(dev), idx=torch.from_numpy(p.idx).to(dev),
+                cb=torch.from_numpy(p.codebook).to(dev)))
+        self.sets = []
+        for c in range(self.copies):
+            s = []
+            for p, b in zip(problems, base):
+                t = dict(x=b["x"].clone(), idx=b["idx"].clone(), cb=b["cb"].clone(),
+                         y=torch.empty((p.M, p.N), dtype=torch.float16, device=dev))
+                s.append(t)
+            self.sets.append(s)
+        del base
+        torch.cuda.synchronize()
+
+    def launch(self, c, i, stream):
+        p, t = self.problems[i], self.sets[c][i]
+        fn = self.fasq.gemv_raw if self.entry == "gemv" else self.fasq.gemm_raw
+        st = fn(t["x"].data_ptr(), p.M, p.K, p.N, t["idx"].data_ptr(), p.idx_bits, p.d,
+                t["cb"].data_ptr(), p.C, t["y"].data_ptr(), stream)
+        if st != 0:
+            raise RuntimeError(f"launch failed: {self.fasq.status_string(st)}: {self.fasq.last_error()}")
+
+    def launch_all(self, c, stream):
+        for i in range(len(self.problems)):
+            self.launch(c, i, stream)
+
+    def capture_graphs(self):
+        torch = self.torch
+        s = torch.cuda.Stream()
+        # eager warm-up first: one-time host-side set-up happens outside capture
+        for c in range(self.copies):
+            self.launch_all(c, torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        graphs = []
+        for c in range(self.copies):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=s):
+                self.launch_all(c, torch.cuda.current_stream().cuda_stream)
+            graphs.append(g)
+        torch.cuda.synchronize()
+        return graphs
+
+    def time_kernels(self, steps):
+        """Per-launch durations (seconds) from HIP events around each launch.
+
+        A spin kernel is queued first so that the events and launches of one
+        step reach the GPU back to back, whatever the host launch latency.
+        """
+        torch = self.torch
+        n = len(self.problems)
+        per = [[] for _ in range(n)]
+        stream = torch.cuda.current_stream()
+        handle = stream.cuda_stream
+        for s in range(steps):
+            c = s % self.copies
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+            torch.cuda._sleep(SPACER_CYCLES)
+            ev[0].record(stream)
+            for i in range(n):
+                self.launch(c, i, handle)
+                ev[i + 1].record(stream)
+            ev[-1].synchronize()
+            for i in range(n):
+                per[i].append(ev[i].elapsed_time(ev[i + 1]) * 1e-3)
+        return per
+
+
+def source_hash():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2605_04084_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode())
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel_key):
+    """HBM traffic per launch from the committed rocprofv3 counter summary, if
+    it was taken on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        with open(path) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if data.get("source_hash") != source_hash():
+        return None
+    entry = data.get("kernels", {}).get(kernel_key)
+    return None if entry is None else entry.get("hbm_bytes_per_launch")
+
+
+# ---------------------------------------------------------------------------
+# Workload runners
+# ---------------------------------------------------------------------------
+
+def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None):
+    wl = pi.workload(wl_name)
+    mats = list(range(len(wl.matrices))) if include is None else include
+    log(f"[bench] {wl_name} M={M}: generating {len(mats)} matrices")
+    problems = [wl.problem(i, M=M) for i in mats]
+    names = [wl.matrices[i].name for i in mats]
+    ms = MatrixSet(torch, fasq, problems, names, "gemv")
+    log(f"[bench] {wl_name}: {ms.bytes_per_set / 1e6:.1f} MB per layer, {ms.copies} copies")
+    graphs = ms.capture_graphs()
+    for s in range(warmup):
+        graphs[s % ms.copies].replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(steps):
+        graphs[(warmup + s) % ms.copies].replay()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    del graphs
+    per = ms.time_kernels(max(steps, 10))
+    med = [float(np.median(v)) for v in per]
+    mean = [float(np.mean(v)) for v in per]
+    rows = []
+    for p, name, tm, ta in zip(problems, names, med, mean):
+        b = gemv_bytes(p.M, p.K, p.N, p.d, p.C, p.idx_bits)
+        rows.append(dict(name=name, N=p.N, K=p.K, bytes=b, us_median=tm * 1e6, us_mean=ta * 1e6,
+                         gbs=b / tm / 1e9, pct_hbm=100.0 * b / tm / 1e9 / HBM_PEAK_GBS))
+    res = dict(workload=wl_name, M=M, bytes_per_layer=ms.bytes_per_set, copies=ms.copies,
+               wall_s=wall, steps=steps, us_per_layer_graph=wall / steps * 1e6,
+               us_per_layer_kernel_sum=sum(med) * 1e6, matrices=rows)
+    res["gbs_graph"] = ms.bytes_per_set * steps / wall / 1e9
+    res["gbs_kernel_sum"] = ms.bytes_per_set / sum(med) / 1e9
+    del ms
+    torch.cuda.empty_cache()
+    return res
+
+
+def prefill(torch, fasq, pi, Ms, reps):
+    wl = pi.workload("prefill")
+    out = []
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    for i, spec in enumerate(wl.matrices):
+        base = wl.problem(i, M=max(Ms))
+        x_all = torch.from_numpy(base.x).to(dev)
+        idx = torch.from_numpy(base.idx).to(dev)
+        cb = torch.from_numpy(base.codebook).to(dev)
+        for M in Ms:
+            x = x_all[:M].contiguous()
+            y = torch.empty((M, spec.N), dtype=torch.float16, device=dev)
+            args = (x.data_ptr(), M, spec.K, spec.N, idx.data_ptr(), base.idx_bits, base.d, cb.data_ptr(),
+                    base.C, y.data_ptr(), stream.cuda_stream)
+            assert fasq.gemm_raw(*args) == 0, fasq.last_error()
+            times = []
+            for _ in range(reps):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                torch.cuda._sleep(SPACER_CYCLES)
+                e0.record(stream)
+                assert fasq.gemm_raw(*args) == 0
+                e1.record(stream)
+                e1.synchronize()
+                times.append(e0.elapsed_time(e1) * 1e-3)
+            t = float(np.median(times))
+            fl = 2.0 * M * spec.N * spec.K
+            out.append(dict(name=spec.name, M=M, N=spec.N, K=spec.K, us=t * 1e6, tflops=fl / t / 1e12,
+                            pct_mfma=100.0 * fl / t / 1e12 / FP16_MFMA_PEAK_TFLOPS))
+            log(f"[bench] prefill {spec.name} M={M}: {t * 1e6:.1f} us, {fl / t / 1e12:.1f} TFLOP/s")
+        del x_all, idx, cb
+    torch.cuda.empty_cache()
+    return out
+
+
+def cpu_baseline(pi, frac=1.0):
+    """The CPU oracle (fp64 NumPy) on a bounded sample of the decode layer:
+    the first `frac` of the output rows of each of the seven matrices."""
+    from oracle import pq_oracle as orc
+
+    try:
+        from threadpoolctl import threadpool_info
+
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # threadpoolctl missing or failing: report the affinity mask
+        blas = len(os.sched_getaffinity(0))
+    wl = pi.workload("llama3_8b_4bit")
+    total_bytes = 0
+    elapsed = 0.0
+    for i, spec in enumerate(wl.matrices):
+        p = wl.problem(i)
+        rows = np.arange(int(spec.N * frac))
+        t0 = time.perf_counter()
+        orc.pq_linear(p.x, p.idx, p.idx_bits, p.d, p.codebook, rows=rows)
+        elapsed += time.perf_counter() - t0
+        total_bytes += gemv_bytes(1, spec.K, rows.size, p.d, p.C, p.idx_bits)
+    return dict(value=total_bytes / elapsed / 1e9, unit="GB/s", cores=int(blas), kind="oracle",
+                seconds=elapsed,
+                sample=f"first {int(frac * 100)}% of the output rows of each of the 7 matrices of one "
+                       f"effective-4-bit Llama-3-8B layer (M=1), {total_bytes / 1e6:.1f} MB of algorithmic "
+                       f"bytes; id decoding and gather single-threaded NumPy, fp64 matmul on "
+                       f"{blas} BLAS threads; {len(os.sched_getaffinity(0))} cores in the affinity mask")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--sweep", action="store_true", help="add the Qwen3-8B M=1/4/16 decode sweep")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-extra", action="store_true", help="only the effective-4-bit decode layer")
+    ap.add_argument("--out", default=None, help="also write the JSON record to this file")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the library has no "
+              f"multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2605_04084_amd as fasq
+    import pq_inputs as pi
+
+    if not os.path.exists(fasq.LIB_PATH):
+        import __graft_entry__
+
+        __graft_entry__.build()
+    fasq.lib()
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+
+    main_res = decode_layer(torch, fasq, pi, "llama3_8b_4bit", args.steps, args.warmup)
+    for r in main_res["matrices"]:
+        log(f"[bench] 4bit {r['name']:10s} N={r['N']:6d} K={r['K']:6d}: {r['us_median']:7.2f} us "
+            f"{r['gbs']:7.1f} GB/s ({r['pct_hbm']:.1f}% of HBM peak)")
+    log(f"[bench] 4bit layer: graph {main_res['us_per_layer_graph']:.2f} us/layer "
+        f"({main_res['gbs_graph']:.1f} GB/s), kernel sum {main_res['us_per_layer_kernel_sum']:.2f} us "
+        f"({main_res['gbs_kernel_sum']:.1f} GB/s)")
+
+    # dominant kernel: the instantiation with the largest share of the layer's kernel time.
+    # Matrices with the same K share one kernel instantiation in this workload.
+    groups = {}
+    for r in main_res["matrices"]:
+        g = groups.setdefault(r["K"], dict(us=0.0, bytes=0, n=0, names=[]))
+        g["us"] += r["us_median"]
+        g["bytes"] += r["bytes"]
+        g["n"] += 1
+        g["names"].append(r["name"])
+    domK, dom = max(groups.items(), key=lambda kv: kv[1]["us"])
+    kernel_key = f"gemv_m1_u8_d2_K{domK}"
+    achieved = (dom["bytes"] / dom["n"]) / (dom["us"] / dom["n"] * 1e-6) / 1e9
+    roofline = dict(bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
+                    frac=achieved / HBM_PEAK_GBS, traffic=load_traffic(kernel_key),
+                    kernel=f"k_gemv_m1 (8-bit ids, d=2, replicated LDS codebook) on the K={domK} "
+                           f"matrices: {', '.join(dom['names'])}",
+                    bytes_per_launch=dom["bytes"] / dom["n"], us_per_launch=dom["us"] / dom["n"])
+
+    extra = {}
+    if not args.no_extra:
+        r3 = decode_layer(torch, fasq, pi, "llama3_8b_3bit", max(10, args.steps // 2), 3)
+        for r in r3["matrices"]:
+            log(f"[bench] 3bit {r['name']:10s} N={r['N']:6d} K={r['K']:6d}: {r['us_median']:7.2f} us "
+                f"{r['gbs']:7.1f} GB/s ({r['pct_hbm']:.1f}%)")
+        extra["llama3_8b_3bit"] = r3
+        extra["prefill"] = prefill(torch, fasq, pi, (128, 512, 2048), 10)
+    if args.sweep:
+        for M in (1, 4, 16):
+            r5 = decode_layer(torch, fasq, pi, "qwen3_8b_sweep", max(10, args.steps // 2), 3, M=M)
+            log(f"[bench] qwen M={M}: kernel sum {r5['us_per_layer_kernel_sum']:.2f} us/layer "
+                f"({r5['gbs_kernel_sum']:.1f} GB/s); x36 layers {36 * r5['us_per_layer_kernel_sum'] / 1e3:.3f} ms")
+            extra[f"qwen3_8b_M{M}"] = r5
+
+    cpu = None
+    if not args.no_cpu:
+        log("[bench] timing the CPU oracle")
+        cpu = cpu_baseline(pi)
+        log(f"[bench] oracle: {cpu['value'] * 1e3:.2f} MB/s over {cpu['seconds']:.1f} s")
+
+    ms_per_step = main_res["wall_s"] / args.steps * 1e3
+    value = main_res["gbs_graph"]
+    record = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {
+            "workload": "Llama-3-8B decoder layer, decode GEMV at effective 4 bits: q,k,v,o,gate,up,down; "
+                        "M=1, d=2, C=256, 8-bit ids, one fp16 codebook per matrix, uniform ids, seed 0",
+            "bytes_per_step": main_res["bytes_per_layer"],
+            "rotation_copies": main_res["copies"],
+            "timed_region": "HIP graph replay per layer (7 launches), inputs cold in HBM",
+        },
+        "pct_of_hbm_peak": 100.0 * value / HBM_PEAK_GBS,
+        "us_per_layer": main_res["us_per_layer_graph"],
+        "us_per_layer_kernel_sum": main_res["us_per_layer_kernel_sum"],
+        "gbs_kernel_sum": main_res["gbs_kernel_sum"],
+        "per_matrix": main_res["matrices"],
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "extra": extra,
+    }
+    if "prefill" in extra:
+        best = max(extra["prefill"], key=lambda r: r["tflops"])
+        record["prefill_tflops_best"] = best["tflops"]
+        record["prefill_best_config"] = f"{best['name']} M={best['M']}"
+    line = json.dumps(record)
+    print(line, flush=True)
+    if args.out:
+        with open(args.out, "w") as f:
+            f.write(line + "\n")
+
+
+if __name__ == "__main__":
+    main()

@@ -13,15 +13,26 @@
 
 namespace fasq {
 
-hipError_t launch_gemv_m1_u8(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
-hipError_t launch_gemv_m1_u12(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
-hipError_t launch_gemv_m1_u16(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
+hipError_t launch_gemv_u8_m1(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
+hipError_t launch_gemv_u12_m1(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
+hipError_t launch_gemv_u16_m1(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
+hipError_t launch_gemv_u8_m16(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
+hipError_t launch_gemv_u12_m16(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
+hipError_t launch_gemv_u16_m16(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
 
-hipError_t launch_gemv_m1(const Problem& p, const DeviceInfo& dev, hipStream_t stream) {
+hipError_t launch_gemv(const Problem& p, const DeviceInfo& dev, hipStream_t stream) {
+  if (p.M == 1) {
+    switch (p.idx_bits) {
+      case 8: return launch_gemv_u8_m1(p, dev, stream);
+      case 12: return launch_gemv_u12_m1(p, dev, stream);
+      default: return launch_gemv_u16_m1(p, dev, stream);
+    }
+  }
+  if (p.M > 16) return hipErrorNotSupported;
   switch (p.idx_bits) {
-    case 8: return launch_gemv_m1_u8(p, dev, stream);
-    case 12: return launch_gemv_m1_u12(p, dev, stream);
-    default: return launch_gemv_m1_u16(p, dev, stream);
+    case 8: return launch_gemv_u8_m16(p, dev, stream);
+    case 12: return launch_gemv_u12_m16(p, dev, stream);
+    default: return launch_gemv_u16_m16(p, dev, stream);
   }
 }
 
@@ -89,7 +100,7 @@ fasq_status run(const Problem& p, Regime regime, hipStream_t stream) {
   if (e != hipSuccess) return hip_fail("querying the current device", e);
   e = hipErrorNotSupported;
   if (!force_generic()) {
-    if (regime == Regime::kGemv && p.M == 1) e = launch_gemv_m1(p, dev, stream);
+    if (regime == Regime::kGemv) e = launch_gemv(p, dev, stream);
     if (e == hipErrorNotSupported) e = launch_gemm_mfma(p, dev, stream);
   }
   if (e == hipErrorNotSupported) e = launch_generic(p, stream);

@@ -1,6 +1,6 @@
 // Prefill GEMM kernels: variant selection and launch.
 #include "fasq_gemm_mfma.h"
-#include "fasq_gemv_m1_launch.h"
+#include "fasq_gemv_launch.h"
 
 namespace fasq {
 
@@ -53,18 +53,8 @@ hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t
   const int align = (hb % 16 == 0) ? 16 : (hb % 8 == 0) ? 8 : 4;
   if (p.R % align) return hipErrorNotSupported;
 
-  int mode, cb_bytes;
-  const int64_t repl = p.C * (int64_t)(d <= 2 ? 128 : 256);
-  if (repl <= kLdsCodebookBudget) {
-    mode = CB_REPL;
-    cb_bytes = (int)repl;
-  } else if (p.C * d * 2 <= kLdsCodebookBudget) {
-    mode = CB_LDS;
-    cb_bytes = (int)((p.C * d * 2 + 15) / 16 * 16);
-  } else {
-    mode = CB_GLOBAL;
-    cb_bytes = 0;
-  }
+  const int mode = choose_cb_mode(p.C, d);
+  const int cb_bytes = (int)cb_lds_bytes(mode, p.C, d);
   const int lds = cb_bytes + 2 * 128 * kXRowBytes;
   if (lds > dev.lds_per_block) return hipErrorNotSupported;
 

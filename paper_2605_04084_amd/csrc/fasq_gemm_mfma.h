@@ -18,21 +18,10 @@
 #pragma once
 
 #include "fasq_device.h"
-#include "fasq_gemv_m1.h"
+#include "fasq_codebook.h"
 #include "fasq_internal.h"
 
 namespace fasq {
-
-// Id i of an LSB-first stream held in dwords w[] (i is a compile-time constant
-// after unrolling).
-template <int BITS>
-__device__ __forceinline__ uint32_t stream_id(const uint32_t* w, int i) {
-  const int bit = i * BITS;
-  const int word = bit >> 5;
-  const int sh = bit & 31;
-  if (sh + BITS <= 32) return __builtin_amdgcn_ubfe(w[word], sh, BITS);
-  return __builtin_amdgcn_alignbit(w[word + 1], w[word], sh) & ((1u << BITS) - 1u);
-}
 
 constexpr int kGemmKC = 64;          // K per chunk
 constexpr int kXRowBytes = 144;      // padded LDS row of one X chunk (128 B of data)
@@ -87,14 +76,14 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(GemmArgs a) {
       if constexpr (HW % 4 == 0) {
 #pragma unroll
         for (int w = 0; w < HW; w += 4) {
-          const uint4 v = *reinterpret_cast<const uint4*>(p + w);
-          buf[fn][w] = v.x; buf[fn][w + 1] = v.y; buf[fn][w + 2] = v.z; buf[fn][w + 3] = v.w;
+          const u32x4 v = *reinterpret_cast<const u32x4*>(p + w);
+          buf[fn][w] = v[0]; buf[fn][w + 1] = v[1]; buf[fn][w + 2] = v[2]; buf[fn][w + 3] = v[3];
         }
       } else if constexpr (HW % 2 == 0) {
 #pragma unroll
         for (int w = 0; w < HW; w += 2) {
-          const uint2 v = *reinterpret_cast<const uint2*>(p + w);
-          buf[fn][w] = v.x; buf[fn][w + 1] = v.y;
+          const u32x2 v = *reinterpret_cast<const u32x2*>(p + w);
+          buf[fn][w] = v[0]; buf[fn][w + 1] = v[1];
         }
       } else {
 #pragma unroll
@@ -104,29 +93,36 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(GemmArgs a) {
   };
 
   // ---- X chunk loads: thread -> (row, 16-byte column)
-  uint4 xreg[XPASS];
+  // rows >= M read row M - 1: they are computed but never stored
+  const half_t* xrow[XPASS];
+#pragma unroll
+  for (int ps = 0; ps < XPASS; ++ps) {
+    const int64_t m = m0 + ps * 32 + tid / 8;
+    xrow[ps] = a.x + (m < a.M ? m : a.M - 1) * a.K + (tid % 8) * 8;
+  }
+  u32x4 xreg[XPASS];
   auto load_x = [&](int64_t c) {
 #pragma unroll
-    for (int ps = 0; ps < XPASS; ++ps) {
-      const int r = ps * 32 + tid / 8;
-      const int64_t m = m0 + r;
-      if (m < a.M) xreg[ps] = *reinterpret_cast<const uint4*>(a.x + m * a.K + c * kGemmKC + (tid % 8) * 8);
-      else xreg[ps] = make_uint4(0, 0, 0, 0);
-    }
+    for (int ps = 0; ps < XPASS; ++ps)
+      xreg[ps] = *reinterpret_cast<const u32x4*>(xrow[ps] + c * kGemmKC);
   };
   auto store_x = [&](int buf) {
     uint8_t* base = xs + buf * (BM * kXRowBytes);
 #pragma unroll
     for (int ps = 0; ps < XPASS; ++ps) {
       const int r = ps * 32 + tid / 8;
-      *reinterpret_cast<uint4*>(base + r * kXRowBytes + (tid % 8) * 16) = xreg[ps];
+      *reinterpret_cast<u32x4*>(base + r * kXRowBytes + (tid % 8) * 16) = xreg[ps];
     }
   };
 
+  // The codebook (L2-resident) is staged before the first index / X loads:
+  // the vector L1 returns loads in order, so it would otherwise wait for them.
+  CbStage cst;
+  cb_fetch<D, MODE>(a.cb, a.C, cst);
+  cb_store<D, MODE>(smem, a.cb, a.C, cst);
   uint32_t idsA[FN][HW], idsB[FN][HW];
   load_ids(idsA, 0);
   load_x(0);
-  if constexpr (MODE != CB_GLOBAL) stage_codebook<D, MODE>(smem, a.cb, a.C);
   store_x(0);
   __syncthreads();
 
@@ -138,7 +134,7 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(GemmArgs a) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[fm][fn][i] = 0.f;
 
-  const uint32_t lane_off = (uint32_t)(lane % Repl<D>::COPIES) * Repl<D>::ESZ;
+  const uint32_t lane_off = repl_lane_off<D>(lane);
 
   auto compute_chunk = [&](const uint32_t (&ids)[FN][HW], int buf) {
     const uint8_t* xb = xs + buf * (BM * kXRowBytes);
@@ -146,28 +142,7 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(GemmArgs a) {
     for (int t = 0; t < 4; ++t) {
       half8_t bop[FN];
 #pragma unroll
-      for (int fn = 0; fn < FN; ++fn) {
-        uint32_t w4[4];
-        if constexpr (D == 1) {
-#pragma unroll
-          for (int e = 0; e < 8; e += 2) {
-            uint32_t c0[1], c1[1];
-            gather<D, MODE>(smem, a.cb, lane_off, stream_id<BITS>(ids[fn], t * IPS + e), c0);
-            gather<D, MODE>(smem, a.cb, lane_off, stream_id<BITS>(ids[fn], t * IPS + e + 1), c1);
-            w4[e / 2] = (c0[0] & 0xFFFFu) | (c1[0] << 16);
-          }
-        } else {
-          constexpr int CW = D / 2;
-#pragma unroll
-          for (int e = 0; e < IPS; ++e) {
-            uint32_t c[CW];
-            gather<D, MODE>(smem, a.cb, lane_off, stream_id<BITS>(ids[fn], t * IPS + e), c);
-#pragma unroll
-            for (int w = 0; w < CW; ++w) w4[e * CW + w] = c[w];
-          }
-        }
-        bop[fn] = __builtin_bit_cast(half8_t, make_uint4(w4[0], w4[1], w4[2], w4[3]));
-      }
+      for (int fn = 0; fn < FN; ++fn) bop[fn] = gather8<BITS, D, MODE>(smem, a.cb, lane_off, ids[fn], t * IPS);
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm) {
         const int r = wm * WM + fm * 32 + l32;
@@ -179,21 +154,25 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(GemmArgs a) {
     }
   };
 
+  // Chunk c lives in one register set / LDS buffer while chunk c + 1 is
+  // loaded into the other.  The next-chunk loads are unconditional (the last
+  // chunk is re-read) so that the number of loads in flight is static.
   int64_t c = 0;
   int buf = 0;
   while (c < nchunks) {
-    // chunk c lives in idsA / LDS buffer `buf`
-    const bool more = (c + 1) < nchunks;
-    if (more) { load_ids(idsB, c + 1); load_x(c + 1); }
+    int64_t cn = (c + 1) < nchunks ? c + 1 : c;
+    load_ids(idsB, cn);
+    load_x(cn);
     compute_chunk(idsA, buf);
-    if (more) store_x(buf ^ 1);
+    store_x(buf ^ 1);
     __syncthreads();
     ++c; buf ^= 1;
     if (c >= nchunks) break;
-    const bool more2 = (c + 1) < nchunks;
-    if (more2) { load_ids(idsA, c + 1); load_x(c + 1); }
+    cn = (c + 1) < nchunks ? c + 1 : c;
+    load_ids(idsA, cn);
+    load_x(cn);
     compute_chunk(idsB, buf);
-    if (more2) store_x(buf ^ 1);
+    store_x(buf ^ 1);
     __syncthreads();
     ++c; buf ^= 1;
   }

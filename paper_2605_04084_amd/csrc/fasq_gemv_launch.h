@@ -1,0 +1,138 @@
+// Host-side variant selection and launch of the decode GEMV (M <= 16).
+#pragma once
+
+#include <atomic>
+
+#include "fasq_gemv.h"
+#include "fasq_internal.h"
+
+namespace fasq {
+
+constexpr int kLdsCodebookBudget = 64 * 1024;  // bytes of LDS a codebook may take
+
+// Raise a kernel's dynamic-LDS limit to the 160 KB a gfx950 CU offers, once
+// per device (one bit per device ordinal; ordinals >= 64 set it every time).
+template <typename K>
+hipError_t allow_lds(K kernel, int bytes) {
+  static std::atomic<uint64_t> done{0};
+  if (bytes <= 64 * 1024) return hipSuccess;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const uint64_t bit = dev < 64 ? (uint64_t(1) << dev) : 0;
+  if (bit && (done.load(std::memory_order_acquire) & bit)) return hipSuccess;
+  e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                          160 * 1024);
+  if (e == hipSuccess && bit) done.fetch_or(bit, std::memory_order_acq_rel);
+  return e;
+}
+
+// Codebook placement for a call: replicated in LDS when the replicated table
+// fits the budget, one copy in LDS when that fits, else global memory.
+inline int choose_cb_mode(int64_t C, int d) {
+  if ((C * d * 2) % 16 != 0) return CB_GLOBAL;
+  if (cb_lds_bytes(CB_REPL, C, d) <= kLdsCodebookBudget) return CB_REPL;
+  if (cb_lds_bytes(CB_LDS, C, d) <= kLdsCodebookBudget) return CB_LDS;
+  return CB_GLOBAL;
+}
+
+template <int BITS, int D, int T, int MODE, int MR>
+hipError_t launch_gemv_variant(const GemvArgs& a, int threads, int blocks, int lds, hipStream_t stream) {
+  auto kern = k_gemv<BITS, D, T, MODE, MR>;
+  hipError_t e = allow_lds(kern, lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3(blocks), dim3(threads), lds, stream, a);
+  return hipGetLastError();
+}
+
+template <int BITS, int MR, int D, int MODE>
+hipError_t launch_gemv_t(const GemvArgs& a, int T, int threads, int blocks, int lds, hipStream_t stream) {
+  switch (T) {
+    case 1: return launch_gemv_variant<BITS, D, 1, MODE, MR>(a, threads, blocks, lds, stream);
+    case 2: return launch_gemv_variant<BITS, D, 2, MODE, MR>(a, threads, blocks, lds, stream);
+    case 4: return launch_gemv_variant<BITS, D, 4, MODE, MR>(a, threads, blocks, lds, stream);
+    default: return launch_gemv_variant<BITS, D, 8, MODE, MR>(a, threads, blocks, lds, stream);
+  }
+}
+
+template <int BITS, int MR, int D>
+hipError_t launch_gemv_mode(const GemvArgs& a, int mode, int T, int threads, int blocks, int lds,
+                            hipStream_t stream) {
+  switch (mode) {
+    case CB_REPL: return launch_gemv_t<BITS, MR, D, CB_REPL>(a, T, threads, blocks, lds, stream);
+    case CB_LDS: return launch_gemv_t<BITS, MR, D, CB_LDS>(a, T, threads, blocks, lds, stream);
+    default: return launch_gemv_t<BITS, MR, D, CB_GLOBAL>(a, T, threads, blocks, lds, stream);
+  }
+}
+
+// Select (T, P, Q, codebook placement, rows per workgroup) and launch;
+// hipErrorNotSupported when another kernel has to take the call.
+template <int BITS, int MR>
+hipError_t launch_gemv_bits(const Problem& p, const DeviceInfo& dev, hipStream_t stream) {
+  constexpr int G = Chunk<BITS>::G;
+  constexpr int CBY = Chunk<BITS>::DW * 4;
+  const int d = p.d;
+  if (MR == 1 ? p.M != 1 : (p.M < 2 || p.M > 16)) return hipErrorNotSupported;
+  if (!(d == 1 || d == 2 || d == 4 || d == 8)) return hipErrorNotSupported;
+  if (p.S % G || p.K % 8) return hipErrorNotSupported;
+  const int64_t CH = p.S / G;
+  if (CH * CBY != p.R) return hipErrorNotSupported;
+  const uintptr_t ia = reinterpret_cast<uintptr_t>(p.idx);
+  if ((ia & (CBY == 16 ? 15 : 3)) || (reinterpret_cast<uintptr_t>(p.x) & 15) ||
+      (reinterpret_cast<uintptr_t>(p.codebook) & 15))
+    return hipErrorNotSupported;
+
+  const int64_t QC = (CH + 3) / 4;  // chunk columns of the four K groups
+  int T = 0;
+  for (int t : {1, 2, 4, 8}) {
+    if ((QC + t - 1) / t <= 16) { T = t; break; }
+  }
+  if (T == 0) return hipErrorNotSupported;
+  const int P = (int)((QC + T - 1) / T);
+  const int Q = 16 / P;
+  const int threads = P * Q * kWave;
+  const int rows_unit = 16 * Q;
+
+  const int mode = choose_cb_mode(p.C, d);
+  const int cb_bytes = (int)cb_lds_bytes(mode, p.C, d);
+  const int xs = (int)(p.M == 1 ? p.K * 2 : p.K * 2 + 16);
+  const int64_t x_bytes = p.M * (int64_t)xs;
+  const int64_t red_per_unit = (int64_t)rows_unit * p.M * P * 4;
+  const int64_t avail = dev.lds_per_block - cb_bytes - x_bytes;
+  if (avail < red_per_unit) return hipErrorNotSupported;
+
+  const int64_t units = (p.N + rows_unit - 1) / rows_unit;
+  int64_t nwg = dev.num_cus;
+  if (nwg > units) nwg = units;
+  int64_t rw_units = (units + nwg - 1) / nwg;
+  if (rw_units > avail / red_per_unit) rw_units = avail / red_per_unit;
+  const int64_t RW = rw_units * rows_unit;
+  nwg = (p.N + RW - 1) / RW;
+  if (nwg > 0x7fffffff) return hipErrorNotSupported;
+  const int lds = (int)(cb_bytes + x_bytes + RW * p.M * P * 4);
+
+  GemvArgs a;
+  a.x = static_cast<const half_t*>(p.x);
+  a.M = p.M;
+  a.K = p.K;
+  a.N = p.N;
+  a.idx = static_cast<const uint8_t*>(p.idx);
+  a.R = p.R;
+  a.CH = CH;
+  a.cb = static_cast<const half_t*>(p.codebook);
+  a.C = (int)p.C;
+  a.P = P;
+  a.RW = (int)RW;
+  a.cb_bytes = cb_bytes;
+  a.xs = xs;
+  a.x_bytes = (int)x_bytes;
+  a.y = static_cast<half_t*>(p.y);
+  switch (d) {
+    case 1: return launch_gemv_mode<BITS, MR, 1>(a, mode, T, threads, (int)nwg, lds, stream);
+    case 2: return launch_gemv_mode<BITS, MR, 2>(a, mode, T, threads, (int)nwg, lds, stream);
+    case 4: return launch_gemv_mode<BITS, MR, 4>(a, mode, T, threads, (int)nwg, lds, stream);
+    default: return launch_gemv_mode<BITS, MR, 8>(a, mode, T, threads, (int)nwg, lds, stream);
+  }
+}
+
+}  // namespace fasq

@@ -1,0 +1,8 @@
+// Decode GEMV kernels: 8-bit ids, one token (M = 1).
+#include "fasq_gemv_launch.h"
+
+namespace fasq {
+hipError_t launch_gemv_u8_m1(const Problem& p, const DeviceInfo& dev, hipStream_t stream) {
+  return launch_gemv_bits<8, 1>(p, dev, stream);
+}
+}  // namespace fasq

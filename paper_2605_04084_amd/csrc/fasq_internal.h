@@ -32,9 +32,9 @@ hipError_t device_info(DeviceInfo* out);
 hipError_t launch_reconstruct(const Problem& p, void* w, hipStream_t stream);
 hipError_t launch_generic(const Problem& p, hipStream_t stream);
 
-// Tuned decode kernel for M == 1.  Returns hipErrorNotSupported (without
+// Tuned decode kernel for M <= 16.  Returns hipErrorNotSupported (without
 // launching) when no tuned variant applies.
-hipError_t launch_gemv_m1(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
+hipError_t launch_gemv(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
 
 // Tuned MFMA prefill kernel.  hipErrorNotSupported when no variant applies.
 hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
