@@ -40,7 +40,7 @@ struct GemvArgs {
   const half_t* cb;
   int C;
   int P;         // waves per row (K split inside the workgroup)
-  int RW;        // rows per workgroup, a multiple of 16 * (waves / P)
+  int TW;        // 16-row tiles per workgroup, a multiple of waves / P
   int cb_bytes;  // LDS bytes of the codebook (x follows)
   int xs;        // LDS bytes between rows of x
   int x_bytes;   // LDS bytes of x (partials follow)
@@ -50,7 +50,10 @@ struct GemvArgs {
 constexpr int kGemvPipe = 8;      // load units per wave in the software pipeline
 constexpr int kXWordsPerThread = 8;  // first-round x words (16 B) per thread for M > 1
 
-template <int BITS, int D, int T, int MODE, int MR>
+// MASK: some lanes of the last wave of a row see chunk columns past the end
+// of the row (the row is not a whole number of wave spans); their operands
+// are zeroed.
+template <int BITS, int D, int T, int MODE, int MR, bool MASK>
 __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
   constexpr int G = Chunk<BITS>::G;      // ids per chunk
   constexpr int DW = Chunk<BITS>::DW;    // dwords per chunk
@@ -72,14 +75,13 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
   const int g = lane >> 4;    // K group
   const int nl = lane & 15;   // row within a 16-row tile
   const int M = (int)a.M;
-  const int64_t r0 = (int64_t)blockIdx.x * a.RW;
-  const int rows_q = a.RW / Q;
-  const int nrt = rows_q / 16;             // row tiles of this wave
+  // Row tiles are dealt to workgroups round-robin (tile j of workgroup w is
+  // global tile w + j * gridDim.x), so that at any moment the tiles being
+  // streamed form one contiguous stretch of the table and load every HBM
+  // channel; a block per workgroup would put all streams at the same
+  // offset within equal-sized blocks.  Wave q takes local tiles q, q + Q, ...
+  const int nrt = a.TW / Q;                // row tiles of this wave
   const int nunits = nrt * T;
-  const int64_t rowbase = r0 + (int64_t)q * rows_q + nl;
-  // A chunk column is valid for every lane of the wave or for none but the
-  // last few; `full` selects the unmasked path for the whole wave.
-  const bool full = (int64_t)(p * T + T) * 4 <= a.CH;
 
   // chunk column of (t): raw value, and clamped into the row for loads
   const int CH = (int)a.CH;
@@ -89,27 +91,26 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
   // Units past the end of this wave's work load the first chunk of the table
   // (one address for the whole wave: a single request) so that every
   // iteration issues exactly one load and the waits stay exact.
-  // Rows past N read row N - 1 (computed, never stored).
-  const int64_t row0 = rowbase < a.N ? rowbase : a.N - 1;
-  int rtmax = 0;
-  if (rowbase < a.N) {
-    const int64_t last = (a.N - 1 - rowbase) / 16;
-    rtmax = (int)(last < nrt - 1 ? last : nrt - 1);
-  }
-  const uint8_t* lp = a.idx + row0 * a.R;
-  const int64_t tile_stride = 16 * a.R;
+  // Byte offsets into the index table are 32-bit (the host checks that the
+  // table is below 4 GiB) from one uniform base.  Rows past N load the first
+  // chunk of the table (computed, never stored), as do units past the end.
+  auto tile_of = [&](int rt) { return (int64_t)blockIdx.x + (int64_t)(rt * Q + q) * gridDim.x; };
+  const uint32_t lane_off0 = (uint32_t)(nl * a.R);
+  const uint32_t tile_stride = (uint32_t)(16 * a.R);
   uint32_t buf[L][DW];
   auto load_unit = [&](int slot, int u, int t) {
-    int rt = u / T;
-    rt = rt < rtmax ? rt : rtmax;
-    const uint8_t* src = u < nunits ? lp + rt * tile_stride + ccol(t) * CBY : a.idx;
-    load_chunk<BITS>(src, buf[slot]);
+    const int64_t tile = tile_of(u / T);
+    const bool live = u < nunits && tile * 16 + nl < a.N;
+    const uint32_t off = (uint32_t)tile * tile_stride + lane_off0 + (uint32_t)ccol(t) * CBY;
+    load_chunk<BITS>(a.idx + (live ? off : 0u), buf[slot]);
   };
 
   // ---- prologue.  The vector L1 returns loads in order, so an L2-resident
-  // load queued behind HBM loads waits for them: the codebook and x are
-  // fetched and written to LDS first, and the index stream starts after the
-  // barrier.
+  // load queued behind HBM loads waits for them.  All waves of the
+  // workgroup (the only one on its CU) issue their codebook and x loads,
+  // meet at a barrier (which does not wait for memory), and only then issue
+  // the first index loads: the codebook and x come back first while the
+  // index stream is already in flight.
   CbStage cst;
   cb_fetch<D, MODE>(a.cb, a.C, cst);
   constexpr int XWT = MR == 1 ? 2 : kXWordsPerThread;
@@ -122,6 +123,10 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
     w = w < xw_total ? w : xw_total - 1;
     xst[k] = reinterpret_cast<const u32x4*>(a.x)[w];
   }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < L - 1; ++i) load_unit(i, i, i % T);
+
   cb_store<D, MODE>(smem, a.cb, a.C, cst);
 #pragma unroll
   for (int k = 0; k < XWT; ++k) {
@@ -137,35 +142,24 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
   }
   __syncthreads();
 
-#pragma unroll
-  for (int i = 0; i < L - 1; ++i) load_unit(i, i, i % T);
-
   const uint32_t lane_off = repl_lane_off<D>(lane);
   const int mrow = MR == 1 ? 0 : (nl < M ? nl : M - 1);  // x row this lane feeds to the A operand
   const uint8_t* xrow = xl + mrow * a.xs;
 
+  // A operands (x) live in registers when they fit, else are read from LDS
+  // at every step.
+  constexpr bool kXInRegs = !MASK && T * SPC <= 8;
+  half8_t xreg[kXInRegs ? T * SPC : 1];
+  if constexpr (kXInRegs) {
+#pragma unroll
+    for (int t = 0; t < T; ++t)
+#pragma unroll
+      for (int s = 0; s < SPC; ++s)
+        xreg[t * SPC + s] = *reinterpret_cast<const half8_t*>(xrow + ccol(t) * (G * D * 2) + s * 16);
+  }
+
   float4_t acc0 = {0.f, 0.f, 0.f, 0.f};
   float4_t acc1 = {0.f, 0.f, 0.f, 0.f};
-
-  // One chunk: SPC MFMA steps.  MASKED zeroes both operands of lanes whose
-  // chunk column lies past the end of the row (only the last wave of a
-  // ragged row needs it).
-  auto chunk_steps = [&](const uint32_t* w, int t, bool masked) {
-    const uint8_t* xa = xrow + ccol(t) * (G * D * 2);
-    const bool cval = ccol_raw(t) < CH;
-#pragma unroll
-    for (int s = 0; s < SPC; ++s) {
-      half8_t bop = gather8<BITS, D, MODE>(smem, a.cb, lane_off, w, s * (8 / D));
-      half8_t aop = *reinterpret_cast<const half8_t*>(xa + s * 16);
-      if (masked && !cval) {
-        bop = half8_t{};
-        aop = half8_t{};
-      }
-      if (s & 1) acc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc1, 0, 0, 0);
-      else acc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc0, 0, 0, 0);
-    }
-  };
-  const bool full_wave = __builtin_amdgcn_readfirstlane((int)full) != 0;
 
   for (int base = 0; base < nunits; base += L) {
 #pragma unroll
@@ -174,11 +168,25 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
       const int t = i % T;
       load_unit((i + L - 1) % L, u + L - 1, (i + L - 1) % T);
       if (u < nunits) {
-        if (full_wave) chunk_steps(buf[i], t, false);
-        else chunk_steps(buf[i], t, true);
+        const uint32_t* w = buf[i];
+        const uint8_t* xa = xrow + ccol(t) * (G * D * 2);
+        const bool cval = !MASK || ccol_raw(t) < CH;
+#pragma unroll
+        for (int s = 0; s < SPC; ++s) {
+          half8_t bop = gather8<BITS, D, MODE>(smem, a.cb, lane_off, w, s * (8 / D));
+          half8_t aop;
+          if constexpr (kXInRegs) aop = xreg[t * SPC + s];
+          else aop = *reinterpret_cast<const half8_t*>(xa + s * 16);
+          if (!cval) {
+            bop = half8_t{};
+            aop = half8_t{};
+          }
+          if (s & 1) acc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc1, 0, 0, 0);
+          else acc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc0, 0, 0, 0);
+        }
         if (t == T - 1) {
           // lane l holds rows m = 4g .. 4g + 3 of column nl of the 16 x 16 tile
-          const int lrow = q * rows_q + (u / T) * 16 + nl;
+          const int lrow = ((u / T) * Q + q) * 16 + nl;
 #pragma unroll
           for (int k = 0; k < 4; ++k) {
             const int m = 4 * g + k;
@@ -192,17 +200,187 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
   }
   __syncthreads();
 
-  // fixed-order sum over the P waves, one fp16 rounding, row-contiguous stores
-  const int outs = a.RW * M;
+  // fixed-order sum over the P waves, one fp16 rounding
+  const int RW = a.TW * 16;
+  const int outs = RW * M;
   for (int o = threadIdx.x; o < outs; o += blockDim.x) {
-    const int m = o / a.RW;
-    const int r = o - m * a.RW;
-    const int64_t n = r0 + r;
+    const int m = o / RW;
+    const int r = o - m * RW;
+    const int64_t n = ((int64_t)blockIdx.x + (int64_t)(r / 16) * gridDim.x) * 16 + (r & 15);
     if (n < a.N) {
       float sum = 0.f;
       const float* pr = red + (r * M + m) * P;
       for (int pp = 0; pp < P; ++pp) sum += pr[pp];
       a.y[(int64_t)m * a.N + n] = static_cast<half_t>(sum);
+    }
+  }
+}
+
+}  // namespace fasq
+
+namespace fasq {
+
+// ---------------------------------------------------------------------------
+// One token (M = 1).  Reading 16 rows x 64 bytes per wave-wide load (the
+// layout above) streams at well under half the rate of reading 1 KB of one
+// row, so the single-token kernel maps the MFMA differently: the 16 "rows"
+// of the A operand are 16 consecutive 64-byte segments of ONE weight row
+// (lane l: segment l % 16, K group l / 16), B carries the matching slices
+// of x (segment n in column n), and the wanted partial sums are the
+// diagonal of the 16 x 16 result.  One wave-wide load is 64 consecutive
+// chunks of one row.  The matrix core does 16x the useful MACs, which it
+// has to spare at decode arithmetic intensity.
+// ---------------------------------------------------------------------------
+struct GemvM1Args {
+  const half_t* x;
+  int64_t K, N;
+  const uint8_t* idx;
+  int64_t R;   // bytes per row (= CH * chunk bytes)
+  int64_t CH;  // chunks per row
+  const half_t* cb;
+  int C;
+  int P;         // waves per row (K split inside the workgroup)
+  int NRW;       // rows per row group
+  int cb_bytes;  // LDS bytes of the codebook (x follows)
+  int x_bytes;   // LDS bytes of x (partials follow)
+  half_t* y;
+};
+
+template <int BITS, int D, int T, int MODE, bool MASK>
+__global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
+  constexpr int G = Chunk<BITS>::G;
+  constexpr int DW = Chunk<BITS>::DW;
+  constexpr int CBY = DW * 4;
+  constexpr int SPC = G * D / 8;     // MFMA steps per chunk
+  constexpr int L = kGemvPipe;
+  static_assert(L % T == 0, "pipeline depth must be a multiple of T");
+  constexpr bool kXInRegs = T * SPC <= 8;
+
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  uint8_t* xl = smem + a.cb_bytes;
+  float* red = reinterpret_cast<float*>(smem + a.cb_bytes + a.x_bytes);  // [Q * NRW][P]
+
+  const int wave = threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  const int P = a.P;
+  const int Q = (blockDim.x / kWave) / P;
+  const int p = wave % P;
+  const int q = wave / P;
+  const int j = lane & 15;   // segment (A row / B column)
+  const int g = lane >> 4;   // K group
+  const int CH = (int)a.CH;
+  const int nunits = a.NRW * T;
+
+  // chunk of this lane in unit t of its row part: 4 chunks per segment
+  auto ccol_raw = [&](int t) { return (p * T + t) * 64 + j * 4 + g; };
+  auto ccol = [&](int t) { const int c = ccol_raw(t); return c < CH ? c : CH - 1; };
+  // rows are dealt round-robin: local row rr of row group q of workgroup w
+  auto row_of = [&](int rr) { return (int64_t)blockIdx.x + (int64_t)(rr * Q + q) * gridDim.x; };
+
+  uint32_t buf[L][DW];
+  auto load_unit = [&](int slot, int u, int t) {
+    const int64_t n = row_of(u / T);
+    const bool live = u < nunits && n < a.N;
+    const uint32_t off = (uint32_t)n * (uint32_t)a.R + (uint32_t)ccol(t) * CBY;
+    load_chunk<BITS>(a.idx + (live ? off : 0u), buf[slot]);
+  };
+
+  // ---- prologue (see k_gemv): codebook and x first, then the index stream
+  CbStage cst;
+  cb_fetch<D, MODE>(a.cb, a.C, cst);
+  constexpr int XWT = 2;
+  const int xw_total = (int)(a.K / 8);
+  u32x4 xst[XWT];
+#pragma unroll
+  for (int k = 0; k < XWT; ++k) {
+    int w = threadIdx.x + k * blockDim.x;
+    w = w < xw_total ? w : xw_total - 1;
+    xst[k] = reinterpret_cast<const u32x4*>(a.x)[w];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < L - 1; ++i) load_unit(i, i, i % T);
+
+  cb_store<D, MODE>(smem, a.cb, a.C, cst);
+#pragma unroll
+  for (int k = 0; k < XWT; ++k) {
+    const int w = threadIdx.x + k * blockDim.x;
+    if (w < xw_total) reinterpret_cast<u32x4*>(xl)[w] = xst[k];
+  }
+  for (int w = threadIdx.x + XWT * blockDim.x; w < xw_total; w += blockDim.x)
+    reinterpret_cast<u32x4*>(xl)[w] = reinterpret_cast<const u32x4*>(a.x)[w];
+  __syncthreads();
+
+  const uint32_t lane_off = repl_lane_off<D>(lane);
+  half8_t xreg[kXInRegs ? T * SPC : 1];
+  if constexpr (kXInRegs) {
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const bool ok = !MASK || ccol_raw(t) < CH;
+#pragma unroll
+      for (int s = 0; s < SPC; ++s) {
+        const half8_t v = *reinterpret_cast<const half8_t*>(xl + ccol(t) * (G * D * 2) + s * 16);
+        xreg[t * SPC + s] = ok ? v : half8_t{};
+      }
+    }
+  }
+
+  // lane l holds D[4g + i][j]; the diagonal element D[j][j] sits in lane
+  // j + 16 * (j / 4), register j % 4
+  const bool on_diag = (j >> 2) == g;
+  const int diag_reg = j & 3;
+
+  float4_t acc0 = {0.f, 0.f, 0.f, 0.f};
+  float4_t acc1 = {0.f, 0.f, 0.f, 0.f};
+  for (int base = 0; base < nunits; base += L) {
+#pragma unroll
+    for (int i = 0; i < L; ++i) {
+      const int u = base + i;
+      const int t = i % T;
+      load_unit((i + L - 1) % L, u + L - 1, (i + L - 1) % T);
+      if (u < nunits) {
+        const uint32_t* w = buf[i];
+        const bool cval = !MASK || ccol_raw(t) < CH;
+#pragma unroll
+        for (int s = 0; s < SPC; ++s) {
+          half8_t aop = gather8<BITS, D, MODE>(smem, a.cb, lane_off, w, s * (8 / D));
+          half8_t bop;
+          if constexpr (kXInRegs) bop = xreg[t * SPC + s];
+          else bop = *reinterpret_cast<const half8_t*>(xl + ccol(t) * (G * D * 2) + s * 16);
+          if (MASK && !cval) {
+            aop = half8_t{};
+            bop = half8_t{};
+          }
+          if (s & 1) acc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc1, 0, 0, 0);
+          else acc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc0, 0, 0, 0);
+        }
+        if (t == T - 1) {
+          const float4_t acc = acc0 + acc1;
+          float v = diag_reg == 0 ? acc[0] : diag_reg == 1 ? acc[1] : diag_reg == 2 ? acc[2] : acc[3];
+          v = on_diag ? v : 0.f;
+          v = group_sum<16>(v);
+          // the four rows of 16 lanes hold partial sums: combine in a fixed order
+          const float sum = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0)) +
+                            __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16)) +
+                            __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32)) +
+                            __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+          if (lane == 0) red[((u / T) * Q + q) * P + p] = sum;
+          acc0 = float4_t{0.f, 0.f, 0.f, 0.f};
+          acc1 = float4_t{0.f, 0.f, 0.f, 0.f};
+        }
+      }
+    }
+  }
+  __syncthreads();
+
+  // fixed-order sum over the P waves of each row, one fp16 rounding
+  const int rows = Q * a.NRW;
+  for (int r = threadIdx.x; r < rows; r += blockDim.x) {
+    const int64_t n = (int64_t)blockIdx.x + (int64_t)r * gridDim.x;
+    if (n < a.N) {
+      float sum = 0.f;
+      for (int pp = 0; pp < P; ++pp) sum += red[r * P + pp];
+      a.y[n] = static_cast<half_t>(sum);
     }
   }
 }

@@ -37,8 +37,8 @@ inline int choose_cb_mode(int64_t C, int d) {
 }
 
 template <int BITS, int D, int T, int MODE, int MR>
-hipError_t launch_gemv_variant(const GemvArgs& a, int threads, int blocks, int lds, hipStream_t stream) {
-  auto kern = k_gemv<BITS, D, T, MODE, MR>;
+hipError_t launch_gemv_variant(const GemvArgs& a, bool mask, int threads, int blocks, int lds, hipStream_t stream) {
+  auto kern = mask ? k_gemv<BITS, D, T, MODE, MR, true> : k_gemv<BITS, D, T, MODE, MR, false>;
   hipError_t e = allow_lds(kern, lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, dim3(blocks), dim3(threads), lds, stream, a);
@@ -46,22 +46,23 @@ hipError_t launch_gemv_variant(const GemvArgs& a, int threads, int blocks, int l
 }
 
 template <int BITS, int MR, int D, int MODE>
-hipError_t launch_gemv_t(const GemvArgs& a, int T, int threads, int blocks, int lds, hipStream_t stream) {
+hipError_t launch_gemv_t(const GemvArgs& a, int T, bool mask, int threads, int blocks, int lds,
+                         hipStream_t stream) {
   switch (T) {
-    case 1: return launch_gemv_variant<BITS, D, 1, MODE, MR>(a, threads, blocks, lds, stream);
-    case 2: return launch_gemv_variant<BITS, D, 2, MODE, MR>(a, threads, blocks, lds, stream);
-    case 4: return launch_gemv_variant<BITS, D, 4, MODE, MR>(a, threads, blocks, lds, stream);
-    default: return launch_gemv_variant<BITS, D, 8, MODE, MR>(a, threads, blocks, lds, stream);
+    case 1: return launch_gemv_variant<BITS, D, 1, MODE, MR>(a, mask, threads, blocks, lds, stream);
+    case 2: return launch_gemv_variant<BITS, D, 2, MODE, MR>(a, mask, threads, blocks, lds, stream);
+    case 4: return launch_gemv_variant<BITS, D, 4, MODE, MR>(a, mask, threads, blocks, lds, stream);
+    default: return launch_gemv_variant<BITS, D, 8, MODE, MR>(a, mask, threads, blocks, lds, stream);
   }
 }
 
 template <int BITS, int MR, int D>
-hipError_t launch_gemv_mode(const GemvArgs& a, int mode, int T, int threads, int blocks, int lds,
+hipError_t launch_gemv_mode(const GemvArgs& a, int mode, int T, bool mask, int threads, int blocks, int lds,
                             hipStream_t stream) {
   switch (mode) {
-    case CB_REPL: return launch_gemv_t<BITS, MR, D, CB_REPL>(a, T, threads, blocks, lds, stream);
-    case CB_LDS: return launch_gemv_t<BITS, MR, D, CB_LDS>(a, T, threads, blocks, lds, stream);
-    default: return launch_gemv_t<BITS, MR, D, CB_GLOBAL>(a, T, threads, blocks, lds, stream);
+    case CB_REPL: return launch_gemv_t<BITS, MR, D, CB_REPL>(a, T, mask, threads, blocks, lds, stream);
+    case CB_LDS: return launch_gemv_t<BITS, MR, D, CB_LDS>(a, T, mask, threads, blocks, lds, stream);
+    default: return launch_gemv_t<BITS, MR, D, CB_GLOBAL>(a, T, mask, threads, blocks, lds, stream);
   }
 }
 
@@ -77,6 +78,7 @@ hipError_t launch_gemv_bits(const Problem& p, const DeviceInfo& dev, hipStream_t
   if (p.S % G || p.K % 8) return hipErrorNotSupported;
   const int64_t CH = p.S / G;
   if (CH * CBY != p.R) return hipErrorNotSupported;
+  if (p.N * p.R >= (int64_t(1) << 32) || 16 * p.R >= (int64_t(1) << 24)) return hipErrorNotSupported;
   const uintptr_t ia = reinterpret_cast<uintptr_t>(p.idx);
   if ((ia & (CBY == 16 ? 15 : 3)) || (reinterpret_cast<uintptr_t>(p.x) & 15) ||
       (reinterpret_cast<uintptr_t>(p.codebook) & 15))
@@ -90,26 +92,30 @@ hipError_t launch_gemv_bits(const Problem& p, const DeviceInfo& dev, hipStream_t
   if (T == 0) return hipErrorNotSupported;
   const int P = (int)((QC + T - 1) / T);
   const int Q = 16 / P;
+  const bool mask = (int64_t)P * T * 4 != CH;  // the last wave sees columns past the row end
   const int threads = P * Q * kWave;
-  const int rows_unit = 16 * Q;
 
   const int mode = choose_cb_mode(p.C, d);
   const int cb_bytes = (int)cb_lds_bytes(mode, p.C, d);
   const int xs = (int)(p.M == 1 ? p.K * 2 : p.K * 2 + 16);
   const int64_t x_bytes = p.M * (int64_t)xs;
-  const int64_t red_per_unit = (int64_t)rows_unit * p.M * P * 4;
   const int64_t avail = dev.lds_per_block - cb_bytes - x_bytes;
-  if (avail < red_per_unit) return hipErrorNotSupported;
 
-  const int64_t units = (p.N + rows_unit - 1) / rows_unit;
+  // Row tiles of 16 are dealt round-robin to at most one workgroup per CU;
+  // each workgroup gets a whole number of tiles per row group.
+  const int64_t ntiles = (p.N + 15) / 16;
   int64_t nwg = dev.num_cus;
-  if (nwg > units) nwg = units;
-  int64_t rw_units = (units + nwg - 1) / nwg;
-  if (rw_units > avail / red_per_unit) rw_units = avail / red_per_unit;
-  const int64_t RW = rw_units * rows_unit;
-  nwg = (p.N + RW - 1) / RW;
-  if (nwg > 0x7fffffff) return hipErrorNotSupported;
-  const int lds = (int)(cb_bytes + x_bytes + RW * p.M * P * 4);
+  if (nwg > (ntiles + Q - 1) / Q) nwg = (ntiles + Q - 1) / Q;
+  int64_t tw = (ntiles + nwg - 1) / nwg;
+  tw = (tw + Q - 1) / Q * Q;
+  const int64_t tw_max = avail / (16 * p.M * P * 4) / Q * Q;
+  if (tw_max < Q) return hipErrorNotSupported;
+  if (tw > tw_max) {
+    tw = tw_max;
+    nwg = (ntiles + tw - 1) / tw;
+  }
+  if (nwg > 0x7fffffff || tw * 16 > 0x7fffffff) return hipErrorNotSupported;
+  const int lds = (int)(cb_bytes + x_bytes + tw * 16 * p.M * P * 4);
 
   GemvArgs a;
   a.x = static_cast<const half_t*>(p.x);
@@ -122,16 +128,137 @@ hipError_t launch_gemv_bits(const Problem& p, const DeviceInfo& dev, hipStream_t
   a.cb = static_cast<const half_t*>(p.codebook);
   a.C = (int)p.C;
   a.P = P;
-  a.RW = (int)RW;
+  a.TW = (int)tw;
   a.cb_bytes = cb_bytes;
   a.xs = xs;
   a.x_bytes = (int)x_bytes;
   a.y = static_cast<half_t*>(p.y);
   switch (d) {
-    case 1: return launch_gemv_mode<BITS, MR, 1>(a, mode, T, threads, (int)nwg, lds, stream);
-    case 2: return launch_gemv_mode<BITS, MR, 2>(a, mode, T, threads, (int)nwg, lds, stream);
-    case 4: return launch_gemv_mode<BITS, MR, 4>(a, mode, T, threads, (int)nwg, lds, stream);
-    default: return launch_gemv_mode<BITS, MR, 8>(a, mode, T, threads, (int)nwg, lds, stream);
+    case 1: return launch_gemv_mode<BITS, MR, 1>(a, mode, T, mask, threads, (int)nwg, lds, stream);
+    case 2: return launch_gemv_mode<BITS, MR, 2>(a, mode, T, mask, threads, (int)nwg, lds, stream);
+    case 4: return launch_gemv_mode<BITS, MR, 4>(a, mode, T, mask, threads, (int)nwg, lds, stream);
+    default: return launch_gemv_mode<BITS, MR, 8>(a, mode, T, mask, threads, (int)nwg, lds, stream);
+  }
+}
+
+}  // namespace fasq
+
+namespace fasq {
+
+template <int BITS, int D, int T, int MODE>
+hipError_t launch_gemv_m1_variant(const GemvM1Args& a, bool mask, int threads, int blocks, int lds,
+                                  hipStream_t stream) {
+  auto kern = mask ? k_gemv_m1<BITS, D, T, MODE, true> : k_gemv_m1<BITS, D, T, MODE, false>;
+  hipError_t e = allow_lds(kern, lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3(blocks), dim3(threads), lds, stream, a);
+  return hipGetLastError();
+}
+
+template <int BITS, int D, int MODE>
+hipError_t launch_gemv_m1_t(const GemvM1Args& a, int T, bool mask, int threads, int blocks, int lds,
+                            hipStream_t stream) {
+  switch (T) {
+    case 1: return launch_gemv_m1_variant<BITS, D, 1, MODE>(a, mask, threads, blocks, lds, stream);
+    case 2: return launch_gemv_m1_variant<BITS, D, 2, MODE>(a, mask, threads, blocks, lds, stream);
+    case 4: return launch_gemv_m1_variant<BITS, D, 4, MODE>(a, mask, threads, blocks, lds, stream);
+    default: return launch_gemv_m1_variant<BITS, D, 8, MODE>(a, mask, threads, blocks, lds, stream);
+  }
+}
+
+template <int BITS, int D>
+hipError_t launch_gemv_m1_mode(const GemvM1Args& a, int mode, int T, bool mask, int threads, int blocks, int lds,
+                               hipStream_t stream) {
+  switch (mode) {
+    case CB_REPL: return launch_gemv_m1_t<BITS, D, CB_REPL>(a, T, mask, threads, blocks, lds, stream);
+    case CB_LDS: return launch_gemv_m1_t<BITS, D, CB_LDS>(a, T, mask, threads, blocks, lds, stream);
+    default: return launch_gemv_m1_t<BITS, D, CB_GLOBAL>(a, T, mask, threads, blocks, lds, stream);
+  }
+}
+
+// One token: choose T (wave-wide loads per row part), P (waves per row), Q
+// (row groups per workgroup) and the grid; hipErrorNotSupported when another
+// kernel has to take the call.
+template <int BITS>
+hipError_t launch_gemv_m1_bits(const Problem& p, const DeviceInfo& dev, hipStream_t stream) {
+  constexpr int G = Chunk<BITS>::G;
+  constexpr int CBY = Chunk<BITS>::DW * 4;
+  const int d = p.d;
+  if (p.M != 1) return hipErrorNotSupported;
+  if (!(d == 1 || d == 2 || d == 4 || d == 8)) return hipErrorNotSupported;
+  if (p.S % G || p.K % 8) return hipErrorNotSupported;
+  const int64_t CH = p.S / G;
+  if (CH * CBY != p.R) return hipErrorNotSupported;
+  if (p.N * p.R >= (int64_t(1) << 32)) return hipErrorNotSupported;
+  const uintptr_t ia = reinterpret_cast<uintptr_t>(p.idx);
+  if ((ia & (CBY == 16 ? 15 : 3)) || (reinterpret_cast<uintptr_t>(p.x) & 15) ||
+      (reinterpret_cast<uintptr_t>(p.codebook) & 15))
+    return hipErrorNotSupported;
+
+  const int SPC = G * d / 8;
+  const int64_t CHW = (CH + 63) / 64;  // wave-wide loads per row
+  const int tx = SPC <= 8 ? 8 / SPC : 0;  // largest T whose x slices fit the register budget
+  int T = 0;
+  bool mask = false;
+  for (int t : {8, 4, 2, 1}) {  // exact split, x in registers
+    if (t <= tx && CHW % t == 0 && CHW / t <= 16) { T = t; break; }
+  }
+  if (T == 0) {
+    for (int t : {1, 2, 4, 8}) {  // exact split, x from LDS
+      if (CHW % t == 0 && CHW / t <= 16) { T = t; break; }
+    }
+  }
+  if (T == 0) {
+    for (int t : {1, 2, 4, 8}) {
+      if ((CHW + t - 1) / t <= 16) { T = t; break; }
+    }
+  }
+  if (T == 0) return hipErrorNotSupported;
+  const int P = (int)((CHW + T - 1) / T);
+  mask = (int64_t)P * T * 64 != CH;
+
+  const int mode = choose_cb_mode(p.C, d);
+  const int cb_bytes = (int)cb_lds_bytes(mode, p.C, d);
+  const int64_t x_bytes = (p.K * 2 + 15) / 16 * 16;
+  const int64_t avail = dev.lds_per_block - cb_bytes - x_bytes;
+
+  // Q row groups per workgroup: enough workgroups to cover every CU for
+  // small N, up to 16 waves per workgroup.
+  int64_t Q = (p.N + dev.num_cus - 1) / dev.num_cus;
+  if (Q > 16 / P) Q = 16 / P;
+  if (Q < 1) Q = 1;
+  int64_t nwg = (p.N + Q - 1) / Q;
+  if (nwg > dev.num_cus) nwg = dev.num_cus;
+  int64_t nrw = (p.N + nwg * Q - 1) / (nwg * Q);
+  const int64_t nrw_max = avail / (4 * Q * P);
+  if (nrw_max < 1) return hipErrorNotSupported;
+  if (nrw > nrw_max) {
+    nrw = nrw_max;
+    nwg = (p.N + nrw * Q - 1) / (nrw * Q);
+  }
+  if (nwg > 0x7fffffff || nrw * T > 0x7fffffff) return hipErrorNotSupported;
+  const int lds = (int)(cb_bytes + x_bytes + Q * nrw * P * 4);
+  const int threads = (int)(P * Q * kWave);
+
+  GemvM1Args a;
+  a.x = static_cast<const half_t*>(p.x);
+  a.K = p.K;
+  a.N = p.N;
+  a.idx = static_cast<const uint8_t*>(p.idx);
+  a.R = p.R;
+  a.CH = CH;
+  a.cb = static_cast<const half_t*>(p.codebook);
+  a.C = (int)p.C;
+  a.P = P;
+  a.NRW = (int)nrw;
+  a.cb_bytes = cb_bytes;
+  a.x_bytes = (int)x_bytes;
+  a.y = static_cast<half_t*>(p.y);
+  switch (d) {
+    case 1: return launch_gemv_m1_mode<BITS, 1>(a, mode, T, mask, threads, (int)nwg, lds, stream);
+    case 2: return launch_gemv_m1_mode<BITS, 2>(a, mode, T, mask, threads, (int)nwg, lds, stream);
+    case 4: return launch_gemv_m1_mode<BITS, 4>(a, mode, T, mask, threads, (int)nwg, lds, stream);
+    default: return launch_gemv_m1_mode<BITS, 8>(a, mode, T, mask, threads, (int)nwg, lds, stream);
   }
 }
 

@@ -3,6 +3,6 @@
 
 namespace fasq {
 hipError_t launch_gemv_u12_m1(const Problem& p, const DeviceInfo& dev, hipStream_t stream) {
-  return launch_gemv_bits<12, 1>(p, dev, stream);
+  return launch_gemv_m1_bits<12>(p, dev, stream);
 }
 }  // namespace fasq

@@ -3,6 +3,6 @@
 
 namespace fasq {
 hipError_t launch_gemv_u16_m1(const Problem& p, const DeviceInfo& dev, hipStream_t stream) {
-  return launch_gemv_bits<16, 1>(p, dev, stream);
+  return launch_gemv_m1_bits<16>(p, dev, stream);
 }
 }  // namespace fasq
