@@ -9,8 +9,10 @@ read cold from HBM: the inputs are rotated over enough distinct copies
 The timed region replays one HIP graph per step (the seven launches of one
 layer, as deployed).  Separately, every launch is bracketed with HIP events
 on the launch stream (behind a spin kernel, so that host launch latency does
-not enter the measurement) to get per-kernel durations: these give the
-roofline figures and the kernel-sum microseconds per layer.
+not enter the measurement) to get per-kernel durations; the time an empty
+event pair takes on the same stream (measured in the same run) is
+subtracted.  These give the roofline figures and the kernel-sum
+microseconds per layer.
 
 Also reported: the effective 3-bit layer plus lm_head (d = 4, C = 4096,
 12-bit ids) and the prefill GEMM (M = 128 / 512 / 2048 tokens, d = 4,
@@ -137,6 +139,36 @@ class MatrixSet:
         return per
 
 
+def event_pair_overhead(torch, reps=30):
+    """Median time of an empty HIP event pair queued behind a spin kernel."""
+    stream = torch.cuda.current_stream()
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(SPACER_CYCLES)
+        e0.record(stream)
+        e1.record(stream)
+        e1.synchronize()
+        ts.append(e0.elapsed_time(e1) * 1e-3)
+    return float(np.median(ts))
+
+
+CALIBRATION_BYTES = 256 << 20
+
+
+def calibration_kernel(torch, nbytes=CALIBRATION_BYTES, reps=3):
+    """A plain elementwise kernel of known traffic (fp16 negation: reads and
+    writes nbytes each), for scaling the HBM traffic counters (FETCH_SIZE,
+    WRITE_SIZE) of the profiled kernels."""
+    a = torch.ones(nbytes // 2, dtype=torch.float16, device="cuda:0")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        torch.neg(a, out=b)
+    torch.cuda.synchronize()
+    del a, b
+
+
 def source_hash():
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2605_04084_amd", "csrc")
@@ -147,21 +179,112 @@ def source_hash():
     return h.hexdigest()[:16]
 
 
-def load_traffic(kernel_key):
-    """HBM traffic per launch from the committed rocprofv3 counter summary, if
-    it was taken on the current kernel sources."""
-    path = os.path.join(ROOT, "profiles", "traffic.json")
-    if not os.path.exists(path):
+TRAFFIC_PATH = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def load_traffic(kernel, names):
+    """HBM bytes per launch of `kernel` over the matrices `names`, from the
+    committed rocprofv3 counter summary; None unless that summary was taken
+    on the current kernel sources."""
+    if not os.path.exists(TRAFFIC_PATH):
         return None
     try:
-        with open(path) as f:
+        with open(TRAFFIC_PATH) as f:
             data = json.load(f)
     except (OSError, ValueError):
         return None
     if data.get("source_hash") != source_hash():
         return None
-    entry = data.get("kernels", {}).get(kernel_key)
-    return None if entry is None else entry.get("hbm_bytes_per_launch")
+    per = data.get("matrices", {})
+    vals = []
+    for n in names:
+        e = per.get(n)
+        if e is None or e.get("kernel") != kernel:
+            return None
+        vals.append(e["hbm_bytes_per_launch"])
+    return float(np.mean(vals))
+
+
+# ---------------------------------------------------------------------------
+# Counter passes: rocprofv3 --pmc runs a short fixed launch sequence, once for
+# FETCH_SIZE and once for WRITE_SIZE; --pmc-summarize turns the two CSVs into
+# profiles/traffic.json.
+# ---------------------------------------------------------------------------
+
+PMC_REPS = 4
+
+
+def pmc_pass(torch, fasq, pi, manifest_path):
+    """The calibration kernel, then PMC_REPS cold launches of each matrix of
+    the effective-4-bit layer, in order.  Writes the launch manifest."""
+    calibration_kernel(torch)
+    wl = pi.workload("llama3_8b_4bit")
+    problems = [wl.problem(i) for i in range(len(wl.matrices))]
+    names = [m.name for m in wl.matrices]
+    ms = MatrixSet(torch, fasq, problems, names, "gemv", min_copies=PMC_REPS)
+    stream = torch.cuda.current_stream().cuda_stream
+    torch.cuda.synchronize()
+    seq = []
+    for i, (p, name) in enumerate(zip(problems, names)):
+        for r in range(PMC_REPS):
+            ms.launch(r % ms.copies, i, stream)
+        torch.cuda.synchronize()
+        seq.append(dict(name=name, reps=PMC_REPS, bytes=gemv_bytes(p.M, p.K, p.N, p.d, p.C, p.idx_bits),
+                        kernel=fasq.plan("gemv", p.M, p.K, p.N, p.idx_bits, p.d, p.C)))
+    with open(manifest_path, "w") as f:
+        json.dump(dict(source_hash=source_hash(), calibration_bytes=CALIBRATION_BYTES, launches=seq), f, indent=1)
+    log(f"[bench] pmc pass: {len(seq)} matrices x {PMC_REPS} launches, manifest {manifest_path}")
+
+
+def _read_counter_csv(path_or_dir, counter):
+    import csv
+    import glob
+
+    files = [path_or_dir] if os.path.isfile(path_or_dir) else sorted(
+        glob.glob(os.path.join(path_or_dir, "**", "*counter_collection.csv"), recursive=True))
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {path_or_dir}")
+    rows = []
+    for fn in files:
+        with open(fn) as f:
+            for r in csv.DictReader(f):
+                if r["Counter_Name"] == counter:
+                    rows.append((int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"])))
+    rows.sort()
+    return rows
+
+
+def pmc_summarize(manifest_path, fetch_dir, write_dir, out_path):
+    with open(manifest_path) as f:
+        man = json.load(f)
+    result = dict(source_hash=man["source_hash"], counters_kib_per_dispatch=True, matrices={})
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rows = _read_counter_csv(d, counter)
+        cal = [v for _, k, v in rows if "neg" in k]
+        ours = [(k, v) for _, k, v in rows if "fasq::" in k]
+        if not cal:
+            raise SystemExit(f"{counter}: calibration kernel not found")
+        factor = float(np.median(cal)) * 1024.0 / man["calibration_bytes"]
+        result[f"{counter.lower()}_calibration_factor"] = factor
+        want = sum(e["reps"] for e in man["launches"])
+        if len(ours) != want:
+            raise SystemExit(f"{counter}: {len(ours)} library dispatches, manifest lists {want}")
+        pos = 0
+        for e in man["launches"]:
+            vals = [v for _, v in ours[pos:pos + e["reps"]]]
+            pos += e["reps"]
+            m = result["matrices"].setdefault(e["name"], dict(kernel=e["kernel"], algorithmic_bytes=e["bytes"]))
+            m[f"{counter.lower()}_kib_raw"] = float(np.mean(vals))
+            m[f"{counter.lower()}_bytes"] = float(np.mean(vals)) * 1024.0 / factor
+    for m in result["matrices"].values():
+        m["hbm_bytes_per_launch"] = m["fetch_size_bytes"] + m["write_size_bytes"]
+        m["traffic_over_algorithmic"] = m["hbm_bytes_per_launch"] / m["algorithmic_bytes"]
+    with open(out_path, "w") as f:
+        json.dump(result, f, indent=1)
+        f.write("\n")
+    for name, m in result["matrices"].items():
+        log(f"{name:8s} {m['kernel']:28s} traffic {m['hbm_bytes_per_launch'] / 1e6:8.3f} MB, "
+            f"algorithmic {m['algorithmic_bytes'] / 1e6:8.3f} MB, ratio {m['traffic_over_algorithmic']:.3f}")
 
 
 # ---------------------------------------------------------------------------
@@ -187,14 +310,18 @@ def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None):
     wall = time.perf_counter() - t0
     del graphs
     per = ms.time_kernels(max(steps, 10))
-    med = [float(np.median(v)) for v in per]
-    mean = [float(np.mean(v)) for v in per]
+    ovh = event_pair_overhead(torch)
+    med = [max(float(np.median(v)) - ovh, 1e-7) for v in per]
+    mean = [max(float(np.mean(v)) - ovh, 1e-7) for v in per]
+    raw = [float(np.median(v)) for v in per]
     rows = []
-    for p, name, tm, ta in zip(problems, names, med, mean):
+    for p, name, tm, ta, tr in zip(problems, names, med, mean, raw):
         b = gemv_bytes(p.M, p.K, p.N, p.d, p.C, p.idx_bits)
-        rows.append(dict(name=name, N=p.N, K=p.K, bytes=b, us_median=tm * 1e6, us_mean=ta * 1e6,
-                         gbs=b / tm / 1e9, pct_hbm=100.0 * b / tm / 1e9 / HBM_PEAK_GBS))
+        rows.append(dict(name=name, N=p.N, K=p.K, kernel=fasq.plan("gemv", p.M, p.K, p.N, p.idx_bits, p.d, p.C),
+                         bytes=b, us_median=tm * 1e6, us_mean=ta * 1e6,
+                         us_event_raw=tr * 1e6, gbs=b / tm / 1e9, pct_hbm=100.0 * b / tm / 1e9 / HBM_PEAK_GBS))
     res = dict(workload=wl_name, M=M, bytes_per_layer=ms.bytes_per_set, copies=ms.copies,
+               event_overhead_us=ovh * 1e6,
                wall_s=wall, steps=steps, us_per_layer_graph=wall / steps * 1e6,
                us_per_layer_kernel_sum=sum(med) * 1e6, matrices=rows)
     res["gbs_graph"] = ms.bytes_per_set * steps / wall / 1e9
@@ -207,6 +334,7 @@ def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None):
 def prefill(torch, fasq, pi, Ms, reps):
     wl = pi.workload("prefill")
     out = []
+    ovh = event_pair_overhead(torch)
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
     for i, spec in enumerate(wl.matrices):
@@ -229,7 +357,7 @@ def prefill(torch, fasq, pi, Ms, reps):
                 e1.record(stream)
                 e1.synchronize()
                 times.append(e0.elapsed_time(e1) * 1e-3)
-            t = float(np.median(times))
+            t = max(float(np.median(times)) - ovh, 1e-7)
             fl = 2.0 * M * spec.N * spec.K
             out.append(dict(name=spec.name, M=M, N=spec.N, K=spec.K, us=t * 1e6, tflops=fl / t / 1e12,
                             pct_mfma=100.0 * fl / t / 1e12 / FP16_MFMA_PEAK_TFLOPS))
@@ -277,7 +405,15 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-extra", action="store_true", help="only the effective-4-bit decode layer")
     ap.add_argument("--out", default=None, help="also write the JSON record to this file")
+    ap.add_argument("--pmc-pass", metavar="MANIFEST", default=None,
+                    help="run the short launch sequence for a rocprofv3 --pmc pass and write its manifest")
+    ap.add_argument("--pmc-summarize", nargs=4, metavar=("MANIFEST", "FETCH_DIR", "WRITE_DIR", "OUT"),
+                    default=None, help="turn two --pmc passes (FETCH_SIZE, WRITE_SIZE) into a traffic summary")
     args = ap.parse_args()
+
+    if args.pmc_summarize:
+        pmc_summarize(*args.pmc_summarize)
+        return
 
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the library has no "
@@ -298,31 +434,34 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
 
+    if args.pmc_pass:
+        pmc_pass(torch, fasq, pi, args.pmc_pass)
+        return
+
     main_res = decode_layer(torch, fasq, pi, "llama3_8b_4bit", args.steps, args.warmup)
     for r in main_res["matrices"]:
         log(f"[bench] 4bit {r['name']:10s} N={r['N']:6d} K={r['K']:6d}: {r['us_median']:7.2f} us "
-            f"{r['gbs']:7.1f} GB/s ({r['pct_hbm']:.1f}% of HBM peak)")
+            f"{r['gbs']:7.1f} GB/s ({r['pct_hbm']:.1f}% of HBM peak) {r['kernel']}")
     log(f"[bench] 4bit layer: graph {main_res['us_per_layer_graph']:.2f} us/layer "
         f"({main_res['gbs_graph']:.1f} GB/s), kernel sum {main_res['us_per_layer_kernel_sum']:.2f} us "
         f"({main_res['gbs_kernel_sum']:.1f} GB/s)")
 
-    # dominant kernel: the instantiation with the largest share of the layer's kernel time.
-    # Matrices with the same K share one kernel instantiation in this workload.
+    # dominant kernel: the instantiation with the largest share of the layer's kernel time
+    # (matrices that map to the same instantiation are pooled).
     groups = {}
     for r in main_res["matrices"]:
-        g = groups.setdefault(r["K"], dict(us=0.0, bytes=0, n=0, names=[]))
+        g = groups.setdefault(r["kernel"], dict(us=0.0, bytes=0, n=0, names=[]))
         g["us"] += r["us_median"]
         g["bytes"] += r["bytes"]
         g["n"] += 1
         g["names"].append(r["name"])
-    domK, dom = max(groups.items(), key=lambda kv: kv[1]["us"])
-    kernel_key = f"gemv_m1_u8_d2_K{domK}"
+    dom_kernel, dom = max(groups.items(), key=lambda kv: kv[1]["us"])
     achieved = (dom["bytes"] / dom["n"]) / (dom["us"] / dom["n"] * 1e-6) / 1e9
     roofline = dict(bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
-                    frac=achieved / HBM_PEAK_GBS, traffic=load_traffic(kernel_key),
-                    kernel=f"k_gemv_m1 (8-bit ids, d=2, replicated LDS codebook) on the K={domK} "
-                           f"matrices: {', '.join(dom['names'])}",
-                    bytes_per_launch=dom["bytes"] / dom["n"], us_per_launch=dom["us"] / dom["n"])
+                    frac=achieved / HBM_PEAK_GBS, traffic=load_traffic(dom_kernel, dom["names"]),
+                    kernel=f"{dom_kernel} on {', '.join(dom['names'])}",
+                    bytes_per_launch=dom["bytes"] / dom["n"], us_per_launch=dom["us"] / dom["n"],
+                    event_overhead_us=main_res["event_overhead_us"])
 
     extra = {}
     if not args.no_extra:

@@ -127,6 +127,16 @@ const char* fasq_last_error(void);
 /* FASQ_ABI_VERSION of the built library. */
 int fasq_abi_version(void);
 
+/*
+ * Diagnostic: the name of the kernel instantiation that fasq_pq_gemv
+ * (regime 0) or fasq_pq_gemm (regime 1) would launch for these sizes with
+ * 16-byte-aligned buffers, e.g. "k_gemv_m1<8, 2, 2, 0, 0>" (template
+ * arguments in declaration order).  Launches nothing; needs a current HIP
+ * device.  Returns "" for invalid arguments or when no device is available.
+ * The string is thread-local and valid until the thread's next fasq_* call.
+ */
+const char* fasq_pq_plan(int regime, int64_t M, int64_t K, int64_t N, int idx_bits, int d, int64_t C);
+
 #ifdef __cplusplus
 }
 #endif

@@ -25,6 +25,7 @@ __all__ = [
     "library_loaded",
     "abi_version",
     "idx_row_bytes",
+    "plan",
     "status_string",
     "last_error",
     "pq_gemv",
@@ -55,6 +56,7 @@ EXPORTED_SYMBOLS = (
     "fasq_status_string",
     "fasq_last_error",
     "fasq_abi_version",
+    "fasq_pq_plan",
 )
 
 
@@ -102,6 +104,8 @@ def lib() -> ctypes.CDLL:
         L.fasq_last_error.restype = ctypes.c_char_p
         L.fasq_abi_version.argtypes = []
         L.fasq_abi_version.restype = _c_int
+        L.fasq_pq_plan.argtypes = [_c_int, _c_i64, _c_i64, _c_i64, _c_int, _c_int, _c_i64]
+        L.fasq_pq_plan.restype = ctypes.c_char_p
         _lib = L
         return L
 
@@ -116,6 +120,11 @@ def abi_version() -> int:
 
 def idx_row_bytes(K: int, d: int, idx_bits: int) -> int:
     return lib().fasq_idx_row_bytes(K, d, idx_bits)
+
+
+def plan(regime: str, M: int, K: int, N: int, idx_bits: int, d: int, C: int) -> str:
+    """Kernel instantiation a call would launch ("gemv" or "gemm" regime)."""
+    return lib().fasq_pq_plan(1 if regime == "gemm" else 0, M, K, N, idx_bits, d, C).decode()
 
 
 def status_string(status: int) -> str:

@@ -136,6 +136,25 @@ hipError_t device_info(DeviceInfo* out) {
   return hipSuccess;
 }
 
+Plan& plan() {
+  static thread_local Plan p;
+  return p;
+}
+
+bool plan_record(const char* base, std::initializer_list<int> params) {
+  Plan& p = plan();
+  if (!p.active) return false;
+  int n = std::snprintf(p.name, sizeof(p.name), "%s<", base);
+  bool first = true;
+  for (int v : params) {
+    if (n < 0 || n >= (int)sizeof(p.name)) break;
+    n += std::snprintf(p.name + n, sizeof(p.name) - n, first ? "%d" : ", %d", v);
+    first = false;
+  }
+  if (n >= 0 && n < (int)sizeof(p.name) - 1) std::snprintf(p.name + n, sizeof(p.name) - n, ">");
+  return true;
+}
+
 bool force_generic() {
   const char* v = std::getenv("FASQ_FORCE_PATH");
   return v != nullptr && std::strcmp(v, "generic") == 0;
@@ -191,5 +210,20 @@ const char* fasq_status_string(fasq_status s) {
 const char* fasq_last_error(void) { return fasq::t_last_error.c_str(); }
 
 int fasq_abi_version(void) { return FASQ_ABI_VERSION; }
+
+const char* fasq_pq_plan(int regime, int64_t M, int64_t K, int64_t N, int idx_bits, int d, int64_t C) {
+  // Placeholder, suitably aligned, never dereferenced: nothing is launched.
+  const void* fake = reinterpret_cast<const void*>(uintptr_t(1) << 20);
+  fasq_status s = fasq::validate(M, K, N, idx_bits, d, C, fake, fake, fake, fake, true);
+  if (s != FASQ_OK) return "";
+  fasq::Plan& pl = fasq::plan();
+  pl.active = true;
+  pl.name[0] = 0;
+  Problem p = fasq::make_problem(fake, M, K, N, fake, idx_bits, d, fake, C, const_cast<void*>(fake));
+  s = fasq::run(p, regime == 1 ? fasq::Regime::kGemm : fasq::Regime::kGemv, nullptr);
+  pl.active = false;
+  if (s != FASQ_OK) return "";
+  return pl.name;
+}
 
 }  // extern "C"

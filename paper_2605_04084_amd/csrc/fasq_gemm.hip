@@ -9,6 +9,7 @@ namespace {
 template <int BITS, int D, int MODE, int BM, int BN>
 hipError_t launch_gemm_variant(const GemmArgs& a, int lds, hipStream_t stream) {
   auto kern = k_gemm_mfma<BITS, D, MODE, BM, BN>;
+  if (plan_record("k_gemm_mfma", {BITS, D, MODE, BM, BN})) return hipSuccess;
   hipError_t e = allow_lds(kern, lds);
   if (e != hipSuccess) return e;
   dim3 grid((unsigned)((a.N + BN - 1) / BN), (unsigned)((a.M + BM - 1) / BM));

@@ -39,6 +39,7 @@ inline int choose_cb_mode(int64_t C, int d) {
 template <int BITS, int D, int T, int MODE, int MR>
 hipError_t launch_gemv_variant(const GemvArgs& a, bool mask, int threads, int blocks, int lds, hipStream_t stream) {
   auto kern = mask ? k_gemv<BITS, D, T, MODE, MR, true> : k_gemv<BITS, D, T, MODE, MR, false>;
+  if (plan_record("k_gemv", {BITS, D, T, MODE, MR, mask ? 1 : 0})) return hipSuccess;
   hipError_t e = allow_lds(kern, lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, dim3(blocks), dim3(threads), lds, stream, a);
@@ -149,6 +150,7 @@ template <int BITS, int D, int T, int MODE>
 hipError_t launch_gemv_m1_variant(const GemvM1Args& a, bool mask, int threads, int blocks, int lds,
                                   hipStream_t stream) {
   auto kern = mask ? k_gemv_m1<BITS, D, T, MODE, true> : k_gemv_m1<BITS, D, T, MODE, false>;
+  if (plan_record("k_gemv_m1", {BITS, D, T, MODE, mask ? 1 : 0})) return hipSuccess;
   hipError_t e = allow_lds(kern, lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, dim3(blocks), dim3(threads), lds, stream, a);

@@ -91,6 +91,7 @@ hipError_t launch_reconstruct(const Problem& p, void* w, hipStream_t stream) {
 }
 
 hipError_t launch_generic(const Problem& p, hipStream_t stream) {
+  if (plan_record("k_pq_generic", {p.idx_bits})) return hipSuccess;
   const int blocks = grid_for(p.N, 4, 8192);
   const half_t* x = static_cast<const half_t*>(p.x);
   const uint8_t* idx = static_cast<const uint8_t*>(p.idx);

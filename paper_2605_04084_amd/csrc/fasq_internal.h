@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <initializer_list>
+
 namespace fasq {
 
 // One validated call: y[M x N] = x[M x K] . W_hat^T.
@@ -38,6 +40,16 @@ hipError_t launch_gemv(const Problem& p, const DeviceInfo& dev, hipStream_t stre
 
 // Tuned MFMA prefill kernel.  hipErrorNotSupported when no variant applies.
 hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
+
+// Planning mode (per thread): while active, launchers record the name of the
+// kernel instantiation they would launch instead of launching it.
+struct Plan {
+  bool active = false;
+  char name[128] = {0};
+};
+Plan& plan();
+// Record `base<params...>` as the planned kernel; returns true when planning.
+bool plan_record(const char* base, std::initializer_list<int> params);
 
 // Environment overrides used by tests and ablations: FASQ_FORCE_PATH=generic
 // makes every call take the general kernel.
