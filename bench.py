@@ -7,12 +7,12 @@ read cold from HBM: the inputs are rotated over enough distinct copies
 (>= 1 GiB) that the 256 MB Infinity Cache cannot serve them.
 
 The timed region replays one HIP graph per step (the seven launches of one
-layer, as deployed).  Separately, every launch is bracketed with HIP events
-on the launch stream (behind a spin kernel, so that host launch latency does
-not enter the measurement) to get per-kernel durations; the time an empty
-event pair takes on the same stream (measured in the same run) is
-subtracted.  These give the roofline figures and the kernel-sum
-microseconds per layer.
+layer, as deployed).  Separately, per-kernel durations come from HIP events
+on the launch stream around back-to-back launches of one matrix on distinct
+cold copies (behind a spin kernel, so that host launch latency does not
+enter the measurement): the difference between a 10-launch and a 2-launch
+batch, divided by 8, which cancels the cost of the event pair.  These give
+the roofline figures and the kernel-sum microseconds per layer.
 
 Also reported: the effective 3-bit layer plus lm_head (d = 4, C = 4096,
 12-bit ids) and the prefill GEMM (M = 128 / 512 / 2048 tokens, d = 4,
@@ -46,6 +46,7 @@ FP16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 matrix peak
 METRIC = "PQ GEMV HBM GB/s (% of peak) + us per Llama-3-8B layer; prefill PQ GEMM TFLOP/s"
 ROTATION_BYTES = 1 << 30
 SPACER_CYCLES = 2_000_000      # spin kernel queued ahead of event-timed launches
+TIMING_COPIES = 12             # distinct copies one timing sample walks through
 
 
 def log(*a):
@@ -114,43 +115,38 @@ class MatrixSet:
         torch.cuda.synchronize()
         return graphs
 
-    def time_kernels(self, steps):
-        """Per-launch durations (seconds) from HIP events around each launch.
+    def time_kernels(self, steps, short=2, long=10):
+        """Per-launch duration (seconds) of each matrix, from HIP events on the
+        launch stream around back-to-back launches on distinct cold copies.
 
-        A spin kernel is queued first so that the events and launches of one
-        step reach the GPU back to back, whatever the host launch latency.
+        Each sample is (t(long launches) - t(short launches)) / (long - short),
+        which cancels the fixed cost of the event pair.  A spin kernel is queued
+        ahead of every batch so that the launches reach the GPU back to back,
+        whatever the host launch latency.
         """
+        assert self.copies >= short + long
         torch = self.torch
         n = len(self.problems)
         per = [[] for _ in range(n)]
         stream = torch.cuda.current_stream()
         handle = stream.cuda_stream
-        for s in range(steps):
-            c = s % self.copies
-            ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+
+        def batch(i, first, count):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             torch.cuda._sleep(SPACER_CYCLES)
-            ev[0].record(stream)
+            e0.record(stream)
+            for j in range(count):
+                self.launch(first + j, i, handle)
+            e1.record(stream)
+            e1.synchronize()
+            return e0.elapsed_time(e1) * 1e-3
+
+        for _ in range(steps):
             for i in range(n):
-                self.launch(c, i, handle)
-                ev[i + 1].record(stream)
-            ev[-1].synchronize()
-            for i in range(n):
-                per[i].append(ev[i].elapsed_time(ev[i + 1]) * 1e-3)
+                t_short = batch(i, long, short)
+                t_long = batch(i, 0, long)
+                per[i].append((t_long - t_short) / (long - short))
         return per
-
-
-def event_pair_overhead(torch, reps=30):
-    """Median time of an empty HIP event pair queued behind a spin kernel."""
-    stream = torch.cuda.current_stream()
-    ts = []
-    for _ in range(reps):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda._sleep(SPACER_CYCLES)
-        e0.record(stream)
-        e1.record(stream)
-        e1.synchronize()
-        ts.append(e0.elapsed_time(e1) * 1e-3)
-    return float(np.median(ts))
 
 
 CALIBRATION_BYTES = 256 << 20
@@ -297,7 +293,7 @@ def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None):
     log(f"[bench] {wl_name} M={M}: generating {len(mats)} matrices")
     problems = [wl.problem(i, M=M) for i in mats]
     names = [wl.matrices[i].name for i in mats]
-    ms = MatrixSet(torch, fasq, problems, names, "gemv")
+    ms = MatrixSet(torch, fasq, problems, names, "gemv", min_copies=TIMING_COPIES)
     log(f"[bench] {wl_name}: {ms.bytes_per_set / 1e6:.1f} MB per layer, {ms.copies} copies")
     graphs = ms.capture_graphs()
     for s in range(warmup):
@@ -309,19 +305,16 @@ def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     del graphs
-    per = ms.time_kernels(max(steps, 10))
-    ovh = event_pair_overhead(torch)
-    med = [max(float(np.median(v)) - ovh, 1e-7) for v in per]
-    mean = [max(float(np.mean(v)) - ovh, 1e-7) for v in per]
-    raw = [float(np.median(v)) for v in per]
+    per = ms.time_kernels(max(steps // 2, 10))
+    med = [max(float(np.median(v)), 1e-7) for v in per]
+    mean = [max(float(np.mean(v)), 1e-7) for v in per]
     rows = []
-    for p, name, tm, ta, tr in zip(problems, names, med, mean, raw):
+    for p, name, tm, ta in zip(problems, names, med, mean):
         b = gemv_bytes(p.M, p.K, p.N, p.d, p.C, p.idx_bits)
         rows.append(dict(name=name, N=p.N, K=p.K, kernel=fasq.plan("gemv", p.M, p.K, p.N, p.idx_bits, p.d, p.C),
                          bytes=b, us_median=tm * 1e6, us_mean=ta * 1e6,
-                         us_event_raw=tr * 1e6, gbs=b / tm / 1e9, pct_hbm=100.0 * b / tm / 1e9 / HBM_PEAK_GBS))
+                         gbs=b / tm / 1e9, pct_hbm=100.0 * b / tm / 1e9 / HBM_PEAK_GBS))
     res = dict(workload=wl_name, M=M, bytes_per_layer=ms.bytes_per_set, copies=ms.copies,
-               event_overhead_us=ovh * 1e6,
                wall_s=wall, steps=steps, us_per_layer_graph=wall / steps * 1e6,
                us_per_layer_kernel_sum=sum(med) * 1e6, matrices=rows)
     res["gbs_graph"] = ms.bytes_per_set * steps / wall / 1e9
@@ -331,10 +324,12 @@ def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None):
     return res
 
 
-def prefill(torch, fasq, pi, Ms, reps):
+def prefill(torch, fasq, pi, Ms, reps, short=1, long=4):
+    """Prefill GEMM per-launch time, from back-to-back launches (the same
+    operands each time: at these sizes the GEMM is bound by the matrix cores,
+    not by reading its inputs)."""
     wl = pi.workload("prefill")
     out = []
-    ovh = event_pair_overhead(torch)
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
     for i, spec in enumerate(wl.matrices):
@@ -348,19 +343,25 @@ def prefill(torch, fasq, pi, Ms, reps):
             args = (x.data_ptr(), M, spec.K, spec.N, idx.data_ptr(), base.idx_bits, base.d, cb.data_ptr(),
                     base.C, y.data_ptr(), stream.cuda_stream)
             assert fasq.gemm_raw(*args) == 0, fasq.last_error()
-            times = []
-            for _ in range(reps):
+
+            def batch(count):
                 e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 torch.cuda._sleep(SPACER_CYCLES)
                 e0.record(stream)
-                assert fasq.gemm_raw(*args) == 0
+                for _ in range(count):
+                    assert fasq.gemm_raw(*args) == 0
                 e1.record(stream)
                 e1.synchronize()
-                times.append(e0.elapsed_time(e1) * 1e-3)
-            t = max(float(np.median(times)) - ovh, 1e-7)
+                return e0.elapsed_time(e1) * 1e-3
+
+            times = []
+            for _ in range(reps):
+                times.append((batch(long) - batch(short)) / (long - short))
+            t = max(float(np.median(times)), 1e-7)
             fl = 2.0 * M * spec.N * spec.K
             out.append(dict(name=spec.name, M=M, N=spec.N, K=spec.K, us=t * 1e6, tflops=fl / t / 1e12,
-                            pct_mfma=100.0 * fl / t / 1e12 / FP16_MFMA_PEAK_TFLOPS))
+                            pct_mfma=100.0 * fl / t / 1e12 / FP16_MFMA_PEAK_TFLOPS,
+                            kernel=fasq.plan("gemm", M, spec.K, spec.N, base.idx_bits, base.d, base.C)))
             log(f"[bench] prefill {spec.name} M={M}: {t * 1e6:.1f} us, {fl / t / 1e12:.1f} TFLOP/s")
         del x_all, idx, cb
     torch.cuda.empty_cache()
@@ -460,8 +461,7 @@ def main():
     roofline = dict(bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=achieved / HBM_PEAK_GBS, traffic=load_traffic(dom_kernel, dom["names"]),
                     kernel=f"{dom_kernel} on {', '.join(dom['names'])}",
-                    bytes_per_launch=dom["bytes"] / dom["n"], us_per_launch=dom["us"] / dom["n"],
-                    event_overhead_us=main_res["event_overhead_us"])
+                    bytes_per_launch=dom["bytes"] / dom["n"], us_per_launch=dom["us"] / dom["n"])
 
     extra = {}
     if not args.no_extra:
