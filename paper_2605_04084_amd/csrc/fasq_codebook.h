@@ -54,35 +54,40 @@ __device__ __forceinline__ void load_chunk(const uint8_t* __restrict__ p, uint32
   }
 }
 
-// Replicated layout: entry e owns one LDS row of STRIDE bytes holding COPIES
-// copies of ESZ bytes, and lane slot c reads copy c.  gfx950 serves 32 lanes
-// per cycle for 4- and 8-byte LDS reads and 16 lanes per cycle for 16-byte
-// reads, so the lanes of one cycle always address distinct banks.
+// Replicated layout: entry e owns one 256-byte LDS row (address e << 8)
+// holding COPIES copies of its ESZ bytes from the start of the row, and lane
+// l reads copy l % COPIES.  gfx950 serves 32 lanes per cycle for 4- and
+// 8-byte LDS reads and 16 lanes per cycle for 16-byte reads, so the lanes of
+// one cycle always address distinct banks.  With 256-byte rows the address of
+// id u is (u << 8) | lane_off: for 8-bit ids one byte permute builds it
+// straight from the packed id bytes.  (For ESZ = 4 only the first 128 bytes
+// of a row are used.)
 template <int D>
 struct Repl {
-  static constexpr int ESZ = (D == 1) ? 4 : 2 * D;
-  static constexpr int STRIDE = (ESZ <= 4) ? 128 : 256;
-  static constexpr int COPIES = STRIDE / ESZ;
-  static constexpr int WPE = STRIDE / 16;                  // 16-byte words per replicated row
+  static constexpr int ESZ = (D <= 2) ? 4 : 2 * D;
+  static constexpr int STRIDE = 256;
+  static constexpr int COPIES = (ESZ == 4) ? 32 : STRIDE / ESZ;
+  static constexpr int WPE = COPIES * ESZ / 16;  // 16-byte words staged per row
 };
 
 // LDS bytes a codebook of C entries takes in a given placement.
 __host__ __device__ constexpr int64_t cb_lds_bytes(int mode, int64_t C, int d) {
-  return mode == CB_REPL ? C * (d <= 2 ? 128 : 256) : mode == CB_LDS ? C * d * 2 : 0;
+  return mode == CB_REPL ? C * 256 : mode == CB_LDS ? C * d * 2 : 0;
 }
 
 // ---------------------------------------------------------------------------
 // Staging.  The unit is one 16-byte LDS word; consecutive threads write
 // consecutive words, so the stores are conflict-free.
-//   CB_LDS : word w is source word w (C * d * 2 must be a multiple of 16).
-//   CB_REPL: word w of the replicated table holds copies of entry
-//            w / Repl::WPE, which the thread loads on its own (the loads of
-//            one wave touch one or two cache lines).
+//   CB_LDS : word w is source word w, stored at LDS byte 16 w (C * d * 2 must
+//            be a multiple of 16).
+//   CB_REPL: word w holds copies of entry e = w / WPE and is stored at
+//            (e << 8) + 16 (w % WPE); the thread loads the entry itself (the
+//            loads of one wave touch one or two cache lines).
 // The fetch phase issues the global loads and the store phase writes LDS, so
 // that a kernel can issue its index-stream loads in between without waiting
 // on them here.
 // ---------------------------------------------------------------------------
-constexpr int kCbWordsPerThread = 4;  // first-round words per thread (64 KB at 1024 threads)
+constexpr int kCbWordsPerThread = 8;  // first-round words per thread
 
 struct CbStage {
   u32x4 w[kCbWordsPerThread];
@@ -91,6 +96,12 @@ struct CbStage {
 template <int D, int MODE>
 __device__ __forceinline__ int cb_words(int C) {
   return MODE == CB_REPL ? C * Repl<D>::WPE : C * D * 2 / 16;
+}
+
+template <int D, int MODE>
+__device__ __forceinline__ uint32_t cb_word_addr(int w) {
+  if constexpr (MODE == CB_REPL) return ((uint32_t)(w / Repl<D>::WPE) << 8) + (uint32_t)(w % Repl<D>::WPE) * 16;
+  else return (uint32_t)w * 16;
 }
 
 template <int D, int MODE>
@@ -131,35 +142,62 @@ __device__ __forceinline__ void cb_store(uint8_t* __restrict__ lds, const half_t
                                          const CbStage& st) {
   if constexpr (MODE != CB_GLOBAL) {
     const int n = cb_words<D, MODE>(C);
-    u32x4* dst = reinterpret_cast<u32x4*>(lds);
 #pragma unroll
     for (int k = 0; k < kCbWordsPerThread; ++k) {
       const int w = threadIdx.x + k * blockDim.x;
-      if (w < n) dst[w] = st.w[k];
+      if (w < n) *reinterpret_cast<u32x4*>(lds + cb_word_addr<D, MODE>(w)) = st.w[k];
     }
-    for (int w = threadIdx.x + kCbWordsPerThread * blockDim.x; w < n; w += blockDim.x) dst[w] = cb_word<D, MODE>(cb, w);
+    for (int w = threadIdx.x + kCbWordsPerThread * blockDim.x; w < n; w += blockDim.x)
+      *reinterpret_cast<u32x4*>(lds + cb_word_addr<D, MODE>(w)) = cb_word<D, MODE>(cb, w);
   }
 }
 
-// Gather codeword u into `out` (D == 1: one fp16 in the low half of out[0];
-// D >= 2: D / 2 dwords of packed fp16 pairs).
-template <int D, int MODE>
-__device__ __forceinline__ void gather(const uint8_t* __restrict__ lds, const half_t* __restrict__ gcb,
-                                       uint32_t lane_off, uint32_t u, uint32_t* out) {
-  const uint8_t* p;
-  if constexpr (MODE == CB_REPL) p = lds + u * Repl<D>::STRIDE + lane_off;
-  else if constexpr (MODE == CB_LDS) p = lds + u * (2 * D);
-  else p = reinterpret_cast<const uint8_t*>(gcb) + (size_t)u * (2 * D);
+// LDS-resident codebooks start at LDS address 0: the kernels that use them
+// declare no static LDS (the launchers check this), so the dynamic segment
+// begins at 0 and an LDS address can be formed as a plain integer.
+template <typename T>
+__device__ __forceinline__ const __attribute__((address_space(3))) T* lds_at(uint32_t addr) {
+  return (const __attribute__((address_space(3))) T*)(size_t)addr;
+}
+
+// Codeword at LDS byte address addr (D == 1: one fp16 in the low half of
+// out[0]; D >= 2: D / 2 dwords of packed fp16 pairs).
+template <int D>
+__device__ __forceinline__ void read_codeword_lds(uint32_t addr, uint32_t* out) {
   if constexpr (D == 1) {
-    out[0] = *reinterpret_cast<const uint16_t*>(p);
+    out[0] = *lds_at<uint16_t>(addr);
   } else if constexpr (D == 2) {
-    out[0] = *reinterpret_cast<const uint32_t*>(p);
+    out[0] = *lds_at<uint32_t>(addr);
   } else if constexpr (D == 4) {
-    const u32x2 v = *reinterpret_cast<const u32x2*>(p);
+    const u32x2 v = *lds_at<u32x2>(addr);
     out[0] = v[0]; out[1] = v[1];
   } else {
-    const u32x4 v = *reinterpret_cast<const u32x4*>(p);
+    const u32x4 v = *lds_at<u32x4>(addr);
     out[0] = v[0]; out[1] = v[1]; out[2] = v[2]; out[3] = v[3];
+  }
+}
+
+// Gather codeword u into `out` (layout as for read_codeword_lds).
+template <int D, int MODE>
+__device__ __forceinline__ void gather(const half_t* __restrict__ gcb, uint32_t lane_off, uint32_t u,
+                                       uint32_t* out) {
+  if constexpr (MODE == CB_REPL) {
+    read_codeword_lds<D>((u << 8) | lane_off, out);
+  } else if constexpr (MODE == CB_LDS) {
+    read_codeword_lds<D>(u * (2 * D), out);
+  } else {
+    const uint8_t* p = reinterpret_cast<const uint8_t*>(gcb) + (size_t)u * (2 * D);
+    if constexpr (D == 1) {
+      out[0] = *reinterpret_cast<const uint16_t*>(p);
+    } else if constexpr (D == 2) {
+      out[0] = *reinterpret_cast<const uint32_t*>(p);
+    } else if constexpr (D == 4) {
+      const u32x2 v = *reinterpret_cast<const u32x2*>(p);
+      out[0] = v[0]; out[1] = v[1];
+    } else {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(p);
+      out[0] = v[0]; out[1] = v[1]; out[2] = v[2]; out[3] = v[3];
+    }
   }
 }
 
@@ -168,18 +206,32 @@ __device__ __forceinline__ uint32_t repl_lane_off(int lane) {
   return (uint32_t)(lane % Repl<D>::COPIES) * Repl<D>::ESZ;
 }
 
+// Gather the codeword of id i of chunk w[].  For 8-bit ids in the replicated
+// layout the LDS address is one byte permute: byte 0 = the lane's copy
+// offset, byte 1 = the id byte, bytes 2 and 3 = 0.
+template <int BITS, int D, int MODE>
+__device__ __forceinline__ void gather_id(const half_t* __restrict__ gcb, uint32_t lane_off, const uint32_t* w,
+                                          int i, uint32_t* out) {
+  if constexpr (BITS == 8 && MODE == CB_REPL) {
+    const uint32_t sel = 0x0C0C0000u | ((4u + (uint32_t)(i & 3)) << 8);
+    read_codeword_lds<D>(__builtin_amdgcn_perm(w[i >> 2], lane_off, sel), out);
+  } else {
+    gather<D, MODE>(gcb, lane_off, stream_id<BITS>(w, i), out);
+  }
+}
+
 // Eight consecutive K values of W_hat for one lane, as an MFMA operand:
 // ids first .. first + 8/D - 1 of the lane's chunk w[], gathered and packed.
 template <int BITS, int D, int MODE>
-__device__ __forceinline__ half8_t gather8(const uint8_t* __restrict__ lds, const half_t* __restrict__ gcb,
-                                           uint32_t lane_off, const uint32_t* w, int first) {
+__device__ __forceinline__ half8_t gather8(const half_t* __restrict__ gcb, uint32_t lane_off, const uint32_t* w,
+                                           int first) {
   uint32_t o[4];
   if constexpr (D == 1) {
 #pragma unroll
     for (int e = 0; e < 8; e += 2) {
       uint32_t c0[1], c1[1];
-      gather<D, MODE>(lds, gcb, lane_off, stream_id<BITS>(w, first + e), c0);
-      gather<D, MODE>(lds, gcb, lane_off, stream_id<BITS>(w, first + e + 1), c1);
+      gather_id<BITS, D, MODE>(gcb, lane_off, w, first + e, c0);
+      gather_id<BITS, D, MODE>(gcb, lane_off, w, first + e + 1, c1);
       o[e / 2] = (c0[0] & 0xFFFFu) | (c1[0] << 16);
     }
   } else {
@@ -187,12 +239,35 @@ __device__ __forceinline__ half8_t gather8(const uint8_t* __restrict__ lds, cons
 #pragma unroll
     for (int e = 0; e < 8 / D; ++e) {
       uint32_t c[CW];
-      gather<D, MODE>(lds, gcb, lane_off, stream_id<BITS>(w, first + e), c);
+      gather_id<BITS, D, MODE>(gcb, lane_off, w, first + e, c);
 #pragma unroll
       for (int k = 0; k < CW; ++k) o[e * CW + k] = c[k];
     }
   }
   return __builtin_bit_cast(half8_t, u32x4{o[0], o[1], o[2], o[3]});
+}
+
+// ---------------------------------------------------------------------------
+// Raw buffer loads of the index stream.  The resource covers exactly the
+// index table, so a load whose offset lies past its end returns zeros and
+// touches no memory; kernels use that for rows past N instead of clamping.
+// Offsets are 32-bit: callers check N * R (plus the rows a pipeline reads
+// ahead) against 2^32 on the host.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t idx_rsrc(const uint8_t* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+template <int BITS>
+__device__ __forceinline__ void buffer_chunk(__amdgpu_buffer_rsrc_t r, uint32_t off, uint32_t* w) {
+  if constexpr (Chunk<BITS>::DW == 4) {
+    const u32x4 v = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+    w[0] = v[0]; w[1] = v[1]; w[2] = v[2]; w[3] = v[3];
+  } else {
+    typedef uint32_t u32x3 __attribute__((ext_vector_type(3)));
+    const u32x3 v = __builtin_bit_cast(u32x3, __builtin_amdgcn_raw_buffer_load_b96(r, (int)off, 0, 0));
+    w[0] = v[0]; w[1] = v[1]; w[2] = v[2];
+  }
 }
 
 }  // namespace fasq

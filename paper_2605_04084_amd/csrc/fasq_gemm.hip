@@ -10,7 +10,7 @@ template <int BITS, int D, int MODE, int BM, int BN>
 hipError_t launch_gemm_variant(const GemmArgs& a, int lds, hipStream_t stream) {
   auto kern = k_gemm_mfma<BITS, D, MODE, BM, BN>;
   if (plan_record("k_gemm_mfma", {BITS, D, MODE, BM, BN})) return hipSuccess;
-  hipError_t e = allow_lds(kern, lds);
+  hipError_t e = prepare_kernel(kern);
   if (e != hipSuccess) return e;
   dim3 grid((unsigned)((a.N + BN - 1) / BN), (unsigned)((a.M + BM - 1) / BM));
   hipLaunchKernelGGL(kern, grid, dim3(256), lds, stream, a);

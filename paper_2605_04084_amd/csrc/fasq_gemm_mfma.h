@@ -142,7 +142,7 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(GemmArgs a) {
     for (int t = 0; t < 4; ++t) {
       half8_t bop[FN];
 #pragma unroll
-      for (int fn = 0; fn < FN; ++fn) bop[fn] = gather8<BITS, D, MODE>(smem, a.cb, lane_off, ids[fn], t * IPS);
+      for (int fn = 0; fn < FN; ++fn) bop[fn] = gather8<BITS, D, MODE>(a.cb, lane_off, ids[fn], t * IPS);
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm) {
         const int r = wm * WM + fm * 32 + l32;

@@ -48,6 +48,7 @@ struct GemvArgs {
 };
 
 constexpr int kGemvPipe = 8;      // load units per wave in the software pipeline
+constexpr int kM1EarlyLoads = 2;  // index loads per wave issued before the codebook barrier (M = 1)
 constexpr int kXWordsPerThread = 8;  // first-round x words (16 B) per thread for M > 1
 
 // MASK: some lanes of the last wave of a row see chunk columns past the end
@@ -173,7 +174,7 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
         const bool cval = !MASK || ccol_raw(t) < CH;
 #pragma unroll
         for (int s = 0; s < SPC; ++s) {
-          half8_t bop = gather8<BITS, D, MODE>(smem, a.cb, lane_off, w, s * (8 / D));
+          half8_t bop = gather8<BITS, D, MODE>(a.cb, lane_off, w, s * (8 / D));
           half8_t aop;
           if constexpr (kXInRegs) aop = xreg[t * SPC + s];
           else aop = *reinterpret_cast<const half8_t*>(xa + s * 16);
@@ -223,13 +224,14 @@ namespace fasq {
 // ---------------------------------------------------------------------------
 // One token (M = 1).  Reading 16 rows x 64 bytes per wave-wide load (the
 // layout above) streams at well under half the rate of reading 1 KB of one
-// row, so the single-token kernel maps the MFMA differently: the 16 "rows"
-// of the A operand are 16 consecutive 64-byte segments of ONE weight row
-// (lane l: segment l % 16, K group l / 16), B carries the matching slices
-// of x (segment n in column n), and the wanted partial sums are the
-// diagonal of the 16 x 16 result.  One wave-wide load is 64 consecutive
-// chunks of one row.  The matrix core does 16x the useful MACs, which it
-// has to spare at decode arithmetic intensity.
+// row, so the single-token kernel maps the MFMA differently: lane l of a
+// wave-wide load holds chunk l of a 1 KB span of ONE weight row (lanes in
+// address order, so every quarter-wave reads 256 contiguous bytes), and the
+// A operand's "row" i is the set of chunks {i, i + 16, i + 32, i + 48} (K
+// group g = chunk / 16).  B carries the x slice of each lane's own chunk, so
+// the wanted partial sums are the diagonal of the 16 x 16 result.  The
+// matrix core does 16x the useful MACs, which it has to spare at decode
+// arithmetic intensity.
 // ---------------------------------------------------------------------------
 struct GemvM1Args {
   const half_t* x;
@@ -266,23 +268,28 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
   const int Q = (blockDim.x / kWave) / P;
   const int p = wave % P;
   const int q = wave / P;
-  const int j = lane & 15;   // segment (A row / B column)
-  const int g = lane >> 4;   // K group
+  const int j = lane & 15;   // A row / B column of the lane's chunk
+  const int g = lane >> 4;   // K group of the lane's chunk
   const int CH = (int)a.CH;
   const int nunits = a.NRW * T;
 
-  // chunk of this lane in unit t of its row part: 4 chunks per segment
-  auto ccol_raw = [&](int t) { return (p * T + t) * 64 + j * 4 + g; };
+  // chunk of this lane in unit t of its row part
+  auto ccol_raw = [&](int t) { return (p * T + t) * 64 + lane; };
   auto ccol = [&](int t) { const int c = ccol_raw(t); return c < CH ? c : CH - 1; };
-  // rows are dealt round-robin: local row rr of row group q of workgroup w
-  auto row_of = [&](int rr) { return (int64_t)blockIdx.x + (int64_t)(rr * Q + q) * gridDim.x; };
+
+  // Rows are dealt round-robin: local row rr of row group q of workgroup w is
+  // row w + (rr * Q + q) * gridDim.x.  The byte offset of the lane's chunk in
+  // unit t of local row rr is row0 + rr * rstride + t * 64 * CBY.  Rows past N
+  // (the pipeline reads up to L / T rows ahead) lie past the end of the
+  // buffer resource and load zeros.
+  const __amdgpu_buffer_rsrc_t rsrc = idx_rsrc(a.idx, (uint32_t)(a.N * a.R));
+  const uint32_t rstride = (uint32_t)Q * gridDim.x * (uint32_t)a.R;
+  const uint32_t row0 = ((uint32_t)blockIdx.x + (uint32_t)q * gridDim.x) * (uint32_t)a.R +
+                        (uint32_t)ccol_raw(0) * CBY;
 
   uint32_t buf[L][DW];
-  auto load_unit = [&](int slot, int u, int t) {
-    const int64_t n = row_of(u / T);
-    const bool live = u < nunits && n < a.N;
-    const uint32_t off = (uint32_t)n * (uint32_t)a.R + (uint32_t)ccol(t) * CBY;
-    load_chunk<BITS>(a.idx + (live ? off : 0u), buf[slot]);
+  auto load_unit = [&](int slot, uint32_t roff, int t) {
+    buffer_chunk<BITS>(rsrc, roff + (uint32_t)t * (64 * CBY), buf[slot]);
   };
 
   // ---- prologue (see k_gemv): codebook and x first, then the index stream
@@ -297,9 +304,14 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
     w = w < xw_total ? w : xw_total - 1;
     xst[k] = reinterpret_cast<const u32x4*>(a.x)[w];
   }
+  // Every wave's codebook and x requests enter the CU's (in-order) memory
+  // queue before any index load, and only kM1EarlyLoads index loads per wave
+  // go out before the staging barrier: the barrier then waits for the small
+  // staging data alone, not for the whole workgroup to get its pipeline
+  // loads accepted by a saturated memory queue.
   __syncthreads();
 #pragma unroll
-  for (int i = 0; i < L - 1; ++i) load_unit(i, i, i % T);
+  for (int i = 0; i < kM1EarlyLoads; ++i) load_unit(i, row0 + (uint32_t)(i / T) * rstride, i % T);
 
   cb_store<D, MODE>(smem, a.cb, a.C, cst);
 #pragma unroll
@@ -310,6 +322,8 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
   for (int w = threadIdx.x + XWT * blockDim.x; w < xw_total; w += blockDim.x)
     reinterpret_cast<u32x4*>(xl)[w] = reinterpret_cast<const u32x4*>(a.x)[w];
   __syncthreads();
+#pragma unroll
+  for (int i = kM1EarlyLoads; i < L - 1; ++i) load_unit(i, row0 + (uint32_t)(i / T) * rstride, i % T);
 
   const uint32_t lane_off = repl_lane_off<D>(lane);
   half8_t xreg[kXInRegs ? T * SPC : 1];
@@ -332,18 +346,19 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
 
   float4_t acc0 = {0.f, 0.f, 0.f, 0.f};
   float4_t acc1 = {0.f, 0.f, 0.f, 0.f};
-  for (int base = 0; base < nunits; base += L) {
+  uint32_t rbase = row0;  // offset of local row base / T
+  for (int base = 0; base < nunits; base += L, rbase += (uint32_t)(L / T) * rstride) {
 #pragma unroll
     for (int i = 0; i < L; ++i) {
       const int u = base + i;
       const int t = i % T;
-      load_unit((i + L - 1) % L, u + L - 1, (i + L - 1) % T);
+      load_unit((i + L - 1) % L, rbase + (uint32_t)((i + L - 1) / T) * rstride, (i + L - 1) % T);
       if (u < nunits) {
         const uint32_t* w = buf[i];
         const bool cval = !MASK || ccol_raw(t) < CH;
 #pragma unroll
         for (int s = 0; s < SPC; ++s) {
-          half8_t aop = gather8<BITS, D, MODE>(smem, a.cb, lane_off, w, s * (8 / D));
+          half8_t aop = gather8<BITS, D, MODE>(a.cb, lane_off, w, s * (8 / D));
           half8_t bop;
           if constexpr (kXInRegs) bop = xreg[t * SPC + s];
           else bop = *reinterpret_cast<const half8_t*>(xl + ccol(t) * (G * D * 2) + s * 16);

@@ -10,17 +10,22 @@ namespace fasq {
 
 constexpr int kLdsCodebookBudget = 64 * 1024;  // bytes of LDS a codebook may take
 
-// Raise a kernel's dynamic-LDS limit to the 160 KB a gfx950 CU offers, once
-// per device (one bit per device ordinal; ordinals >= 64 set it every time).
+// Once per device and kernel: check that the kernel declares no static LDS
+// (its LDS-resident codebook is addressed from LDS address 0) and raise its
+// dynamic-LDS limit to the 160 KB a gfx950 CU offers.  One bit per device
+// ordinal; ordinals >= 64 repeat the set-up on every call.
 template <typename K>
-hipError_t allow_lds(K kernel, int bytes) {
+hipError_t prepare_kernel(K kernel) {
   static std::atomic<uint64_t> done{0};
-  if (bytes <= 64 * 1024) return hipSuccess;
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   const uint64_t bit = dev < 64 ? (uint64_t(1) << dev) : 0;
   if (bit && (done.load(std::memory_order_acquire) & bit)) return hipSuccess;
+  hipFuncAttributes attr;
+  e = hipFuncGetAttributes(&attr, reinterpret_cast<const void*>(kernel));
+  if (e != hipSuccess) return e;
+  if (attr.sharedSizeBytes != 0) return hipErrorInvalidDeviceFunction;
   e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
                           160 * 1024);
   if (e == hipSuccess && bit) done.fetch_or(bit, std::memory_order_acq_rel);
@@ -40,7 +45,7 @@ template <int BITS, int D, int T, int MODE, int MR>
 hipError_t launch_gemv_variant(const GemvArgs& a, bool mask, int threads, int blocks, int lds, hipStream_t stream) {
   auto kern = mask ? k_gemv<BITS, D, T, MODE, MR, true> : k_gemv<BITS, D, T, MODE, MR, false>;
   if (plan_record("k_gemv", {BITS, D, T, MODE, MR, mask ? 1 : 0})) return hipSuccess;
-  hipError_t e = allow_lds(kern, lds);
+  hipError_t e = prepare_kernel(kern);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, dim3(blocks), dim3(threads), lds, stream, a);
   return hipGetLastError();
@@ -151,7 +156,7 @@ hipError_t launch_gemv_m1_variant(const GemvM1Args& a, bool mask, int threads, i
                                   hipStream_t stream) {
   auto kern = mask ? k_gemv_m1<BITS, D, T, MODE, true> : k_gemv_m1<BITS, D, T, MODE, false>;
   if (plan_record("k_gemv_m1", {BITS, D, T, MODE, mask ? 1 : 0})) return hipSuccess;
-  hipError_t e = allow_lds(kern, lds);
+  hipError_t e = prepare_kernel(kern);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, dim3(blocks), dim3(threads), lds, stream, a);
   return hipGetLastError();
@@ -239,6 +244,9 @@ hipError_t launch_gemv_m1_bits(const Problem& p, const DeviceInfo& dev, hipStrea
     nwg = (p.N + nrw * Q - 1) / (nrw * Q);
   }
   if (nwg > 0x7fffffff || nrw * T > 0x7fffffff) return hipErrorNotSupported;
+  // 32-bit buffer offsets must cover every row the pipeline reads, including
+  // the rows it reads ahead past the last one (those load zeros).
+  if ((nwg * Q * (nrw + kGemvPipe / T + 1)) * p.R >= (int64_t(1) << 32)) return hipErrorNotSupported;
   const int lds = (int)(cb_bytes + x_bytes + Q * nrw * P * 4);
   const int threads = (int)(P * Q * kWave);
 
