@@ -49,6 +49,12 @@ struct GemvArgs {
 
 constexpr int kGemvPipe = 8;      // load units per wave in the software pipeline
 constexpr int kM1EarlyLoads = 2;  // index loads per wave issued before the codebook barrier (M = 1)
+
+// Highest unit whose load has been issued once unit i of the first window has
+// been computed (i = -1: before any): two more per unit, at most L ahead.
+__host__ __device__ constexpr int m1_ramp_hi(int i) {
+  return (kM1EarlyLoads - 1 + 2 * (i + 1)) < (i + kGemvPipe) ? (kM1EarlyLoads - 1 + 2 * (i + 1)) : (i + kGemvPipe);
+}
 constexpr int kXWordsPerThread = 8;  // first-round x words (16 B) per thread for M > 1
 
 // MASK: some lanes of the last wave of a row see chunk columns past the end
@@ -322,8 +328,6 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
   for (int w = threadIdx.x + XWT * blockDim.x; w < xw_total; w += blockDim.x)
     reinterpret_cast<u32x4*>(xl)[w] = reinterpret_cast<const u32x4*>(a.x)[w];
   __syncthreads();
-#pragma unroll
-  for (int i = kM1EarlyLoads; i < L - 1; ++i) load_unit(i, row0 + (uint32_t)(i / T) * rstride, i % T);
 
   const uint32_t lane_off = repl_lane_off<D>(lane);
   half8_t xreg[kXInRegs ? T * SPC : 1];
@@ -346,44 +350,56 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
 
   float4_t acc0 = {0.f, 0.f, 0.f, 0.f};
   float4_t acc1 = {0.f, 0.f, 0.f, 0.f};
-  uint32_t rbase = row0;  // offset of local row base / T
-  for (int base = 0; base < nunits; base += L, rbase += (uint32_t)(L / T) * rstride) {
+  auto compute_unit = [&](int slot, int u, int t) {
+    const uint32_t* w = buf[slot];
+    const bool cval = !MASK || ccol_raw(t) < CH;
+#pragma unroll
+    for (int s = 0; s < SPC; ++s) {
+      half8_t aop = gather8<BITS, D, MODE>(a.cb, lane_off, w, s * (8 / D));
+      half8_t bop;
+      if constexpr (kXInRegs) bop = xreg[t * SPC + s];
+      else bop = *reinterpret_cast<const half8_t*>(xl + ccol(t) * (G * D * 2) + s * 16);
+      if (MASK && !cval) {
+        aop = half8_t{};
+        bop = half8_t{};
+      }
+      if (s & 1) acc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc1, 0, 0, 0);
+      else acc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc0, 0, 0, 0);
+    }
+    if (t == T - 1) {
+      const float4_t acc = acc0 + acc1;
+      float v = diag_reg == 0 ? acc[0] : diag_reg == 1 ? acc[1] : diag_reg == 2 ? acc[2] : acc[3];
+      v = on_diag ? v : 0.f;
+      v = group_sum<16>(v);
+      // the four rows of 16 lanes hold partial sums: combine in a fixed order
+      const float sum = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0)) +
+                        __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16)) +
+                        __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32)) +
+                        __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+      if (lane == 0) red[((u / T) * Q + q) * P + p] = sum;
+      acc0 = float4_t{0.f, 0.f, 0.f, 0.f};
+      acc1 = float4_t{0.f, 0.f, 0.f, 0.f};
+    }
+  };
+
+  // Unit k lives in slot k % L.  A wave computes a unit before it issues more
+  // loads, so data that has arrived is never held up behind a load waiting
+  // for room in the memory queue.  First window: the loads not issued before
+  // the barrier go out two per computed unit until L are in flight.
+#pragma unroll
+  for (int i = 0; i < L; ++i) {
+    if (i < nunits) compute_unit(i, i, i % T);
+#pragma unroll
+    for (int k = m1_ramp_hi(i - 1) + 1; k <= m1_ramp_hi(i); ++k)
+      load_unit(k % L, row0 + (uint32_t)(k / T) * rstride, k % T);
+  }
+  // Steady state: after unit base + i, issue unit base + i + L into its slot.
+  uint32_t rbase = row0 + (uint32_t)(L / T) * rstride;  // offset of local row base / T
+  for (int base = L; base < nunits; base += L, rbase += (uint32_t)(L / T) * rstride) {
 #pragma unroll
     for (int i = 0; i < L; ++i) {
-      const int u = base + i;
-      const int t = i % T;
-      load_unit((i + L - 1) % L, rbase + (uint32_t)((i + L - 1) / T) * rstride, (i + L - 1) % T);
-      if (u < nunits) {
-        const uint32_t* w = buf[i];
-        const bool cval = !MASK || ccol_raw(t) < CH;
-#pragma unroll
-        for (int s = 0; s < SPC; ++s) {
-          half8_t aop = gather8<BITS, D, MODE>(a.cb, lane_off, w, s * (8 / D));
-          half8_t bop;
-          if constexpr (kXInRegs) bop = xreg[t * SPC + s];
-          else bop = *reinterpret_cast<const half8_t*>(xl + ccol(t) * (G * D * 2) + s * 16);
-          if (MASK && !cval) {
-            aop = half8_t{};
-            bop = half8_t{};
-          }
-          if (s & 1) acc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc1, 0, 0, 0);
-          else acc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc0, 0, 0, 0);
-        }
-        if (t == T - 1) {
-          const float4_t acc = acc0 + acc1;
-          float v = diag_reg == 0 ? acc[0] : diag_reg == 1 ? acc[1] : diag_reg == 2 ? acc[2] : acc[3];
-          v = on_diag ? v : 0.f;
-          v = group_sum<16>(v);
-          // the four rows of 16 lanes hold partial sums: combine in a fixed order
-          const float sum = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0)) +
-                            __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16)) +
-                            __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32)) +
-                            __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
-          if (lane == 0) red[((u / T) * Q + q) * P + p] = sum;
-          acc0 = float4_t{0.f, 0.f, 0.f, 0.f};
-          acc1 = float4_t{0.f, 0.f, 0.f, 0.f};
-        }
-      }
+      if (base + i < nunits) compute_unit(i, base + i, i % T);
+      load_unit(i, rbase + (uint32_t)((i + L) / T) * rstride, i % T);
     }
   }
   __syncthreads();
