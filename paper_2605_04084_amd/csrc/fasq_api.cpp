@@ -1,5 +1,5 @@
 // libfasq C ABI: argument validation, kernel selection, error reporting.
-#include "../../include/fasq.h"
+#include "fasq.h"
 
 #include <hip/hip_runtime.h>
 

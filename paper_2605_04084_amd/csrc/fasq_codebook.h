@@ -89,6 +89,13 @@ __host__ __device__ constexpr int64_t cb_lds_bytes(int mode, int64_t C, int d) {
 // ---------------------------------------------------------------------------
 constexpr int kCbWordsPerThread = 8;  // first-round words per thread
 
+// Replicated two-fp16 codewords (d = 2, C <= 256) take a shorter route: every
+// wave loads the whole raw codebook (one 16-byte load per lane, 4 entries per
+// lane) and the replicated rows are written from registers, each entry's
+// codeword fetched from the lane that holds it with a cross-lane permute.
+template <int D, int MODE>
+constexpr bool cb_fast_stage() { return MODE == CB_REPL && D == 2; }
+
 struct CbStage {
   u32x4 w[kCbWordsPerThread];
 };
@@ -127,7 +134,11 @@ __device__ __forceinline__ u32x4 cb_word(const half_t* __restrict__ cb, int w) {
 
 template <int D, int MODE>
 __device__ __forceinline__ void cb_fetch(const half_t* __restrict__ cb, int C, CbStage& st) {
-  if constexpr (MODE != CB_GLOBAL) {
+  if constexpr (cb_fast_stage<D, MODE>()) {
+    const int chunks = C / 4;  // 16-byte chunks of the raw codebook (C * 4 % 16 == 0)
+    const int l = threadIdx.x % kWave;
+    st.w[0] = reinterpret_cast<const u32x4*>(cb)[l < chunks ? l : chunks - 1];
+  } else if constexpr (MODE != CB_GLOBAL) {
     const int n = cb_words<D, MODE>(C);
 #pragma unroll
     for (int k = 0; k < kCbWordsPerThread; ++k) {
@@ -140,7 +151,23 @@ __device__ __forceinline__ void cb_fetch(const half_t* __restrict__ cb, int C, C
 template <int D, int MODE>
 __device__ __forceinline__ void cb_store(uint8_t* __restrict__ lds, const half_t* __restrict__ cb, int C,
                                          const CbStage& st) {
-  if constexpr (MODE != CB_GLOBAL) {
+  if constexpr (cb_fast_stage<D, MODE>()) {
+    // Wave v writes entry blocks v, v + waves, ... of 32 entries; in step k,
+    // lane l writes 16 bytes of row e = 32 b + 4 (l / 8) + k, whose codeword
+    // is dword k of lane e / 4.
+    const int l = threadIdx.x % kWave;
+    const int waves = blockDim.x / kWave;
+    for (int b = threadIdx.x / kWave; b * 32 < C; b += waves) {
+      uint32_t c[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) c[k] = (uint32_t)__shfl((int)st.w[0][k], 8 * b + l / 8, kWave);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int e = 32 * b + 4 * (l / 8) + k;
+        if (e < C) *reinterpret_cast<u32x4*>(lds + ((uint32_t)e << 8) + (uint32_t)(l % 8) * 16) = u32x4{c[k], c[k], c[k], c[k]};
+      }
+    }
+  } else if constexpr (MODE != CB_GLOBAL) {
     const int n = cb_words<D, MODE>(C);
 #pragma unroll
     for (int k = 0; k < kCbWordsPerThread; ++k) {

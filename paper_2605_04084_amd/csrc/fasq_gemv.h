@@ -301,14 +301,18 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
   // ---- prologue (see k_gemv): codebook and x first, then the index stream
   CbStage cst;
   cb_fetch<D, MODE>(a.cb, a.C, cst);
+  // x in 16-byte words: thread t stages words t and t + blockDim.x; waves
+  // whose words all lie past the end of x issue no load for them.
   constexpr int XWT = 2;
   const int xw_total = (int)(a.K / 8);
   u32x4 xst[XWT];
 #pragma unroll
   for (int k = 0; k < XWT; ++k) {
-    int w = threadIdx.x + k * blockDim.x;
-    w = w < xw_total ? w : xw_total - 1;
-    xst[k] = reinterpret_cast<const u32x4*>(a.x)[w];
+    if (wave * kWave + k * (int)blockDim.x < xw_total) {
+      int w = threadIdx.x + k * blockDim.x;
+      w = w < xw_total ? w : xw_total - 1;
+      xst[k] = reinterpret_cast<const u32x4*>(a.x)[w];
+    }
   }
   // Every wave's codebook and x requests enter the CU's (in-order) memory
   // queue before any index load, and only kM1EarlyLoads index loads per wave
