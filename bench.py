@@ -6,13 +6,17 @@ One step = one Llama-3-8B decoder layer of decode GEMVs at effective 4 bits
 read cold from HBM: the inputs are rotated over enough distinct copies
 (>= 1 GiB) that the 256 MB Infinity Cache cannot serve them.
 
-The timed region replays one HIP graph per step (the seven launches of one
-layer, as deployed).  Separately, per-kernel durations come from HIP events
-on the launch stream around back-to-back launches of one matrix on distinct
-cold copies (behind a spin kernel, so that host launch latency does not
-enter the measurement): the difference between a 10-launch and a 2-launch
-batch, divided by 8, which cancels the cost of the event pair.  These give
-the roofline figures and the kernel-sum microseconds per layer.
+The timed region replays HIP graphs holding several consecutive layers each
+(a decode step replays the whole model from one graph); each layer is four
+launches, as deployed, since matrices that read the same activations go out as one
+grouped call (q + k + v and gate + up through fasq_pq_gemv_batched; o and
+down alone).  Separately, per-launch durations come from HIP events on the
+launch stream around back-to-back launches of one group on distinct cold
+copies (behind a spin kernel, so that host launch latency does not enter the
+measurement): the difference between a 10-launch and a 2-launch batch,
+divided by 8, which cancels the cost of the event pair.  These give the
+roofline figures and the kernel-sum microseconds per layer.  --per-matrix
+adds the same layer with one launch per matrix.
 
 Also reported: the effective 3-bit layer plus lm_head (d = 4, C = 4096,
 12-bit ids) and the prefill GEMM (M = 128 / 512 / 2048 tokens, d = 4,
@@ -20,7 +24,8 @@ C = 256, 8-bit ids) in TFLOP/s.  --sweep adds the Qwen3-8B decode sweep
 (M = 1, 4, 16; C = 65536, 16-bit ids, codebook in L2).
 
 Algorithmic bytes of one GEMV: N*R (packed ids) + C*d*2 (codebook) +
-M*K*2 (x) + M*N*2 (y); flops of one GEMM: 2*M*N*K.
+M*K*2 (x) + M*N*2 (y), with x counted once per grouped launch; flops of one
+GEMM: 2*M*N*K.
 
 Prints ONE JSON line on stdout; progress goes to stderr.
 """
@@ -59,16 +64,46 @@ def gemv_bytes(M, K, N, d, C, bits):
 
 
 # ---------------------------------------------------------------------------
+# Launch groups: matrices of a decoder layer that read the same activations go
+# out as one grouped call (q, k, v; gate, up), the others alone.
+# ---------------------------------------------------------------------------
+
+SHARED_INPUT = (("q_proj", "k_proj", "v_proj"), ("gate_proj", "up_proj"))
+
+
+def launch_groups(names):
+    """Partition matrix indices into launch groups, in layer order."""
+    groups, seen = [], set()
+    for i, n in enumerate(names):
+        if i in seen:
+            continue
+        g = [i]
+        for members in SHARED_INPUT:
+            if n in members:
+                g = [j for j, m in enumerate(names) if m in members]
+        seen.update(g)
+        groups.append(g)
+    return groups
+
+
+# ---------------------------------------------------------------------------
 # A set of matrices with rotating device copies
 # ---------------------------------------------------------------------------
 
 class MatrixSet:
-    """Device copies of a list of PQ problems, rotated to defeat the MALL."""
+    """Device copies of a list of PQ problems, rotated to defeat the MALL.
 
-    def __init__(self, torch, fasq, problems, names, entry, min_copies=1, rotation_bytes=ROTATION_BYTES):
+    ``groups`` lists the launch groups (lists of matrix indices); a group of
+    several matrices is one fasq_pq_gemv_batched call on the x of its first
+    matrix, a group of one is one fasq_pq_gemv call.
+    """
+
+    def __init__(self, torch, fasq, problems, names, groups=None, min_copies=1, rotation_bytes=ROTATION_BYTES):
         self.torch, self.fasq = torch, fasq
-        self.problems, self.names, self.entry = problems, names, entry
-        self.bytes_per_set = sum(gemv_bytes(p.M, p.K, p.N, p.d, p.C, p.idx_bits) for p in problems)
+        self.problems, self.names = problems, names
+        self.groups = groups if groups is not None else [[i] for i in range(len(problems))]
+        self.bytes = [gemv_bytes(p.M, p.K, p.N, p.d, p.C, p.idx_bits) for p in problems]
+        self.bytes_per_set = sum(self.bytes)
         self.copies = max(min_copies, math.ceil(rotation_bytes / self.bytes_per_set) + 1)
         dev = torch.device("cuda:0")
         base = []
@@ -87,19 +122,42 @@ class MatrixSet:
         del base
         torch.cuda.synchronize()
 
-    def launch(self, c, i, stream):
-        p, t = self.problems[i], self.sets[c][i]
-        fn = self.fasq.gemv_raw if self.entry == "gemv" else self.fasq.gemm_raw
-        st = fn(t["x"].data_ptr(), p.M, p.K, p.N, t["idx"].data_ptr(), p.idx_bits, p.d,
-                t["cb"].data_ptr(), p.C, t["y"].data_ptr(), stream)
+    def group_bytes(self, g):
+        """Algorithmic bytes of one launch of group g (x is read once)."""
+        ps = [self.problems[i] for i in self.groups[g]]
+        x_extra = sum(p.M * p.K * 2 for p in ps[1:])
+        return sum(self.bytes[i] for i in self.groups[g]) - x_extra
+
+    def group_name(self, g):
+        return "+".join(self.names[i] for i in self.groups[g])
+
+    def group_kernel(self, g):
+        p = self.problems[self.groups[g][0]]
+        return self.fasq.plan("gemv", p.M, p.K, p.N, p.idx_bits, p.d, p.C)
+
+    def launch(self, c, g, stream):
+        members = self.groups[g]
+        s = self.sets[c]
+        p0, x = self.problems[members[0]], s[members[0]]["x"].data_ptr()
+        if len(members) == 1:
+            t = s[members[0]]
+            st = self.fasq.gemv_raw(x, p0.M, p0.K, p0.N, t["idx"].data_ptr(), p0.idx_bits, p0.d,
+                                    t["cb"].data_ptr(), p0.C, t["y"].data_ptr(), stream)
+        else:
+            st = self.fasq.gemv_batched_raw(
+                x, p0.M, p0.K, [s[i]["idx"].data_ptr() for i in members], [self.problems[i].N for i in members],
+                [s[i]["cb"].data_ptr() for i in members], [self.problems[i].C for i in members],
+                [s[i]["y"].data_ptr() for i in members], p0.idx_bits, p0.d, stream)
         if st != 0:
             raise RuntimeError(f"launch failed: {self.fasq.status_string(st)}: {self.fasq.last_error()}")
 
     def launch_all(self, c, stream):
-        for i in range(len(self.problems)):
-            self.launch(c, i, stream)
+        for g in range(len(self.groups)):
+            self.launch(c, g, stream)
 
-    def capture_graphs(self):
+    def capture_graphs(self, layers_per_graph=1):
+        """Graph c replays the layer on copies c, c + 1, ... (layers_per_graph
+        of them, modulo the number of copies)."""
         torch = self.torch
         s = torch.cuda.Stream()
         # eager warm-up first: one-time host-side set-up happens outside capture
@@ -110,14 +168,16 @@ class MatrixSet:
         for c in range(self.copies):
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g, stream=s):
-                self.launch_all(c, torch.cuda.current_stream().cuda_stream)
+                for k in range(layers_per_graph):
+                    self.launch_all((c + k) % self.copies, torch.cuda.current_stream().cuda_stream)
             graphs.append(g)
         torch.cuda.synchronize()
         return graphs
 
     def time_kernels(self, steps, short=2, long=10):
-        """Per-launch duration (seconds) of each matrix, from HIP events on the
-        launch stream around back-to-back launches on distinct cold copies.
+        """Per-launch duration (seconds) of each launch group, from HIP events
+        on the launch stream around back-to-back launches on distinct cold
+        copies.
 
         Each sample is (t(long launches) - t(short launches)) / (long - short),
         which cancels the fixed cost of the event pair.  A spin kernel is queued
@@ -126,26 +186,26 @@ class MatrixSet:
         """
         assert self.copies >= short + long
         torch = self.torch
-        n = len(self.problems)
+        n = len(self.groups)
         per = [[] for _ in range(n)]
         stream = torch.cuda.current_stream()
         handle = stream.cuda_stream
 
-        def batch(i, first, count):
+        def batch(g, first, count):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             torch.cuda._sleep(SPACER_CYCLES)
             e0.record(stream)
             for j in range(count):
-                self.launch(first + j, i, handle)
+                self.launch(first + j, g, handle)
             e1.record(stream)
             e1.synchronize()
             return e0.elapsed_time(e1) * 1e-3
 
         for _ in range(steps):
-            for i in range(n):
-                t_short = batch(i, long, short)
-                t_long = batch(i, 0, long)
-                per[i].append((t_long - t_short) / (long - short))
+            for g in range(n):
+                t_short = batch(g, long, short)
+                t_long = batch(g, 0, long)
+                per[g].append((t_long - t_short) / (long - short))
         return per
 
 
@@ -179,9 +239,9 @@ TRAFFIC_PATH = os.path.join(ROOT, "profiles", "traffic.json")
 
 
 def load_traffic(kernel, names):
-    """HBM bytes per launch of `kernel` over the matrices `names`, from the
-    committed rocprofv3 counter summary; None unless that summary was taken
-    on the current kernel sources."""
+    """Mean HBM bytes per launch of `kernel` over the launches `names` (launch
+    group names), from the committed rocprofv3 counter summary; None unless
+    that summary was taken on the current kernel sources."""
     if not os.path.exists(TRAFFIC_PATH):
         return None
     try:
@@ -191,7 +251,7 @@ def load_traffic(kernel, names):
         return None
     if data.get("source_hash") != source_hash():
         return None
-    per = data.get("matrices", {})
+    per = data.get("launches", {})
     vals = []
     for n in names:
         e = per.get(n)
@@ -211,25 +271,24 @@ PMC_REPS = 4
 
 
 def pmc_pass(torch, fasq, pi, manifest_path):
-    """The calibration kernel, then PMC_REPS cold launches of each matrix of
-    the effective-4-bit layer, in order.  Writes the launch manifest."""
+    """The calibration kernel, then PMC_REPS cold launches of each launch group
+    of the effective-4-bit layer, in order.  Writes the launch manifest."""
     calibration_kernel(torch)
     wl = pi.workload("llama3_8b_4bit")
     problems = [wl.problem(i) for i in range(len(wl.matrices))]
     names = [m.name for m in wl.matrices]
-    ms = MatrixSet(torch, fasq, problems, names, "gemv", min_copies=PMC_REPS)
+    ms = MatrixSet(torch, fasq, problems, names, launch_groups(names), min_copies=PMC_REPS)
     stream = torch.cuda.current_stream().cuda_stream
     torch.cuda.synchronize()
     seq = []
-    for i, (p, name) in enumerate(zip(problems, names)):
+    for g in range(len(ms.groups)):
         for r in range(PMC_REPS):
-            ms.launch(r % ms.copies, i, stream)
+            ms.launch(r % ms.copies, g, stream)
         torch.cuda.synchronize()
-        seq.append(dict(name=name, reps=PMC_REPS, bytes=gemv_bytes(p.M, p.K, p.N, p.d, p.C, p.idx_bits),
-                        kernel=fasq.plan("gemv", p.M, p.K, p.N, p.idx_bits, p.d, p.C)))
+        seq.append(dict(name=ms.group_name(g), reps=PMC_REPS, bytes=ms.group_bytes(g), kernel=ms.group_kernel(g)))
     with open(manifest_path, "w") as f:
         json.dump(dict(source_hash=source_hash(), calibration_bytes=CALIBRATION_BYTES, launches=seq), f, indent=1)
-    log(f"[bench] pmc pass: {len(seq)} matrices x {PMC_REPS} launches, manifest {manifest_path}")
+    log(f"[bench] pmc pass: {len(seq)} launch groups x {PMC_REPS} launches, manifest {manifest_path}")
 
 
 def _read_counter_csv(path_or_dir, counter):
@@ -253,7 +312,7 @@ def _read_counter_csv(path_or_dir, counter):
 def pmc_summarize(manifest_path, fetch_dir, write_dir, out_path):
     with open(manifest_path) as f:
         man = json.load(f)
-    result = dict(source_hash=man["source_hash"], counters_kib_per_dispatch=True, matrices={})
+    result = dict(source_hash=man["source_hash"], counters_kib_per_dispatch=True, launches={})
     for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         rows = _read_counter_csv(d, counter)
         cal = [v for _, k, v in rows if "neg" in k]
@@ -269,17 +328,17 @@ def pmc_summarize(manifest_path, fetch_dir, write_dir, out_path):
         for e in man["launches"]:
             vals = [v for _, v in ours[pos:pos + e["reps"]]]
             pos += e["reps"]
-            m = result["matrices"].setdefault(e["name"], dict(kernel=e["kernel"], algorithmic_bytes=e["bytes"]))
+            m = result["launches"].setdefault(e["name"], dict(kernel=e["kernel"], algorithmic_bytes=e["bytes"]))
             m[f"{counter.lower()}_kib_raw"] = float(np.mean(vals))
             m[f"{counter.lower()}_bytes"] = float(np.mean(vals)) * 1024.0 / factor
-    for m in result["matrices"].values():
+    for m in result["launches"].values():
         m["hbm_bytes_per_launch"] = m["fetch_size_bytes"] + m["write_size_bytes"]
         m["traffic_over_algorithmic"] = m["hbm_bytes_per_launch"] / m["algorithmic_bytes"]
     with open(out_path, "w") as f:
         json.dump(result, f, indent=1)
         f.write("\n")
-    for name, m in result["matrices"].items():
-        log(f"{name:8s} {m['kernel']:28s} traffic {m['hbm_bytes_per_launch'] / 1e6:8.3f} MB, "
+    for name, m in result["launches"].items():
+        log(f"{name:26s} {m['kernel']:28s} traffic {m['hbm_bytes_per_launch'] / 1e6:8.3f} MB, "
             f"algorithmic {m['algorithmic_bytes'] / 1e6:8.3f} MB, ratio {m['traffic_over_algorithmic']:.3f}")
 
 
@@ -287,21 +346,28 @@ def pmc_summarize(manifest_path, fetch_dir, write_dir, out_path):
 # Workload runners
 # ---------------------------------------------------------------------------
 
-def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None):
+def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None, grouped=True):
     wl = pi.workload(wl_name)
     mats = list(range(len(wl.matrices))) if include is None else include
     log(f"[bench] {wl_name} M={M}: generating {len(mats)} matrices")
     problems = [wl.problem(i, M=M) for i in mats]
     names = [wl.matrices[i].name for i in mats]
-    ms = MatrixSet(torch, fasq, problems, names, "gemv", min_copies=TIMING_COPIES)
-    log(f"[bench] {wl_name}: {ms.bytes_per_set / 1e6:.1f} MB per layer, {ms.copies} copies")
-    graphs = ms.capture_graphs()
+    groups = launch_groups(names) if grouped else None
+    ms = MatrixSet(torch, fasq, problems, names, groups, min_copies=TIMING_COPIES)
+    log(f"[bench] {wl_name}: {ms.bytes_per_set / 1e6:.1f} MB per layer, {ms.copies} copies, "
+        f"{len(ms.groups)} launches")
+    # Consecutive layers go into one graph, as a decode step replays every
+    # layer of the model from one graph: the graph launch boundary is paid
+    # once per lpg layers, lpg the largest divisor of the step count that is
+    # at most the number of copies.
+    lpg = max(k for k in range(1, min(steps, ms.copies) + 1) if steps % k == 0)
+    graphs = ms.capture_graphs(lpg)
     for s in range(warmup):
         graphs[s % ms.copies].replay()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for s in range(steps):
-        graphs[(warmup + s) % ms.copies].replay()
+    for r in range(steps // lpg):
+        graphs[(r * lpg) % ms.copies].replay()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     del graphs
@@ -309,16 +375,19 @@ def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None):
     med = [max(float(np.median(v)), 1e-7) for v in per]
     mean = [max(float(np.mean(v)), 1e-7) for v in per]
     rows = []
-    for p, name, tm, ta in zip(problems, names, med, mean):
-        b = gemv_bytes(p.M, p.K, p.N, p.d, p.C, p.idx_bits)
-        rows.append(dict(name=name, N=p.N, K=p.K, kernel=fasq.plan("gemv", p.M, p.K, p.N, p.idx_bits, p.d, p.C),
+    for g, (tm, ta) in enumerate(zip(med, mean)):
+        b = ms.group_bytes(g)
+        ps = [problems[i] for i in ms.groups[g]]
+        rows.append(dict(name=ms.group_name(g), N=[p.N for p in ps], K=ps[0].K, kernel=ms.group_kernel(g),
                          bytes=b, us_median=tm * 1e6, us_mean=ta * 1e6,
                          gbs=b / tm / 1e9, pct_hbm=100.0 * b / tm / 1e9 / HBM_PEAK_GBS))
-    res = dict(workload=wl_name, M=M, bytes_per_layer=ms.bytes_per_set, copies=ms.copies,
+    step_bytes = sum(r["bytes"] for r in rows)
+    res = dict(workload=wl_name, M=M, bytes_per_layer=step_bytes, copies=ms.copies, launches=len(rows),
+               layers_per_graph=lpg,
                wall_s=wall, steps=steps, us_per_layer_graph=wall / steps * 1e6,
-               us_per_layer_kernel_sum=sum(med) * 1e6, matrices=rows)
-    res["gbs_graph"] = ms.bytes_per_set * steps / wall / 1e9
-    res["gbs_kernel_sum"] = ms.bytes_per_set / sum(med) / 1e9
+               us_per_layer_kernel_sum=sum(med) * 1e6, launch_table=rows)
+    res["gbs_graph"] = step_bytes * steps / wall / 1e9
+    res["gbs_kernel_sum"] = step_bytes / sum(med) / 1e9
     del ms
     torch.cuda.empty_cache()
     return res
@@ -397,6 +466,15 @@ def cpu_baseline(pi, frac=1.0):
                        f"{blas} BLAS threads; {len(os.sched_getaffinity(0))} cores in the affinity mask")
 
 
+def report_layer(tag, res):
+    for r in res["launch_table"]:
+        log(f"[bench] {tag} {r['name']:26s} K={r['K']:6d}: {r['us_median']:7.2f} us "
+            f"{r['gbs']:7.1f} GB/s ({r['pct_hbm']:.1f}% of HBM peak) {r['kernel']}")
+    log(f"[bench] {tag} layer: graph {res['us_per_layer_graph']:.2f} us/layer "
+        f"({res['gbs_graph']:.1f} GB/s), kernel sum {res['us_per_layer_kernel_sum']:.2f} us "
+        f"({res['gbs_kernel_sum']:.1f} GB/s)")
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -405,6 +483,7 @@ def main():
     ap.add_argument("--sweep", action="store_true", help="add the Qwen3-8B M=1/4/16 decode sweep")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-extra", action="store_true", help="only the effective-4-bit decode layer")
+    ap.add_argument("--per-matrix", action="store_true", help="add the 4-bit layer with one launch per matrix")
     ap.add_argument("--out", default=None, help="also write the JSON record to this file")
     ap.add_argument("--pmc-pass", metavar="MANIFEST", default=None,
                     help="run the short launch sequence for a rocprofv3 --pmc pass and write its manifest")
@@ -440,23 +519,18 @@ def main():
         return
 
     main_res = decode_layer(torch, fasq, pi, "llama3_8b_4bit", args.steps, args.warmup)
-    for r in main_res["matrices"]:
-        log(f"[bench] 4bit {r['name']:10s} N={r['N']:6d} K={r['K']:6d}: {r['us_median']:7.2f} us "
-            f"{r['gbs']:7.1f} GB/s ({r['pct_hbm']:.1f}% of HBM peak) {r['kernel']}")
-    log(f"[bench] 4bit layer: graph {main_res['us_per_layer_graph']:.2f} us/layer "
-        f"({main_res['gbs_graph']:.1f} GB/s), kernel sum {main_res['us_per_layer_kernel_sum']:.2f} us "
-        f"({main_res['gbs_kernel_sum']:.1f} GB/s)")
+    report_layer("4bit", main_res)
 
     # dominant kernel: the instantiation with the largest share of the layer's kernel time
-    # (matrices that map to the same instantiation are pooled).
-    groups = {}
-    for r in main_res["matrices"]:
-        g = groups.setdefault(r["kernel"], dict(us=0.0, bytes=0, n=0, names=[]))
+    # (launches that map to the same instantiation are pooled).
+    pools = {}
+    for r in main_res["launch_table"]:
+        g = pools.setdefault(r["kernel"], dict(us=0.0, bytes=0, n=0, names=[]))
         g["us"] += r["us_median"]
         g["bytes"] += r["bytes"]
         g["n"] += 1
         g["names"].append(r["name"])
-    dom_kernel, dom = max(groups.items(), key=lambda kv: kv[1]["us"])
+    dom_kernel, dom = max(pools.items(), key=lambda kv: kv[1]["us"])
     achieved = (dom["bytes"] / dom["n"]) / (dom["us"] / dom["n"] * 1e-6) / 1e9
     roofline = dict(bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=achieved / HBM_PEAK_GBS, traffic=load_traffic(dom_kernel, dom["names"]),
@@ -466,11 +540,13 @@ def main():
     extra = {}
     if not args.no_extra:
         r3 = decode_layer(torch, fasq, pi, "llama3_8b_3bit", max(10, args.steps // 2), 3)
-        for r in r3["matrices"]:
-            log(f"[bench] 3bit {r['name']:10s} N={r['N']:6d} K={r['K']:6d}: {r['us_median']:7.2f} us "
-                f"{r['gbs']:7.1f} GB/s ({r['pct_hbm']:.1f}%)")
+        report_layer("3bit", r3)
         extra["llama3_8b_3bit"] = r3
         extra["prefill"] = prefill(torch, fasq, pi, (128, 512, 2048), 10)
+    if args.per_matrix:
+        r1 = decode_layer(torch, fasq, pi, "llama3_8b_4bit", max(10, args.steps // 2), 3, grouped=False)
+        report_layer("4bit, one launch per matrix", r1)
+        extra["llama3_8b_4bit_per_matrix"] = r1
     if args.sweep:
         for M in (1, 4, 16):
             r5 = decode_layer(torch, fasq, pi, "qwen3_8b_sweep", max(10, args.steps // 2), 3, M=M)
@@ -504,13 +580,14 @@ def main():
                         "M=1, d=2, C=256, 8-bit ids, one fp16 codebook per matrix, uniform ids, seed 0",
             "bytes_per_step": main_res["bytes_per_layer"],
             "rotation_copies": main_res["copies"],
-            "timed_region": "HIP graph replay per layer (7 launches), inputs cold in HBM",
+            "timed_region": f"HIP graph replays, {main_res['layers_per_graph']} consecutive layers per graph, "
+                            "4 launches per layer (q+k+v and gate+up grouped, o, down), inputs cold in HBM",
         },
         "pct_of_hbm_peak": 100.0 * value / HBM_PEAK_GBS,
         "us_per_layer": main_res["us_per_layer_graph"],
         "us_per_layer_kernel_sum": main_res["us_per_layer_kernel_sum"],
         "gbs_kernel_sum": main_res["gbs_kernel_sum"],
-        "per_matrix": main_res["matrices"],
+        "launch_table": main_res["launch_table"],
         "roofline": roofline,
         "cpu_baseline": cpu,
         "extra": extra,

@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define FASQ_ABI_VERSION 1
+#define FASQ_ABI_VERSION 2
 
 typedef enum {
   FASQ_OK = 0,
@@ -85,6 +85,31 @@ fasq_status fasq_pq_gemv(const void* x, int64_t M, int64_t K, int64_t N,
                          const void* idx, int idx_bits, int d,
                          const void* codebook, int64_t C,
                          void* y, hipStream_t stream);
+
+/*
+ * Decode regime over several weight matrices that read the same activations
+ * (FASQ Sec. 4.1; in a decoder layer the q, k and v projections share their
+ * input, and so do the gate and up projections): for i < count,
+ *
+ *   y[i][M x N[i]] = x[M x K] . W_hat_i^T
+ *
+ * with W_hat_i given by idx[i] (N[i] rows of fasq_idx_row_bytes(K, d,
+ * idx_bits) bytes) and codebook[i] (fp16 [C[i] x d]).  x, M, K, idx_bits and d
+ * are shared; every array holds `count` entries and lives in HOST memory,
+ * while the buffers it points to are device memory.  For M = 1 up to eight
+ * matrices run in one launch; otherwise, or when the grouped kernel does not
+ * apply, the matrices are computed one call after another.  Every y[i] is
+ * bit-for-bit what fasq_pq_gemv would write for matrix i alone.
+ *
+ * Returns FASQ_ERR_INVALID_ARG when count < 1, an array is NULL, or any
+ * matrix fails the checks of fasq_pq_gemv (fasq_last_error() names the
+ * matrix); FASQ_ERR_HIP on a launch error.  The y buffers must not overlap
+ * one another or any input.
+ */
+fasq_status fasq_pq_gemv_batched(const void* x, int64_t M, int64_t K, int count,
+                                 const void* const* idx, const int64_t* N,
+                                 const void* const* codebook, const int64_t* C,
+                                 void* const* y, int idx_bits, int d, hipStream_t stream);
 
 /*
  * Prefill regime (FASQ Sec. 4.2: many tokens share one weight matrix).  Same

@@ -31,7 +31,9 @@ __all__ = [
     "pq_gemv",
     "pq_gemm",
     "pq_reconstruct",
+    "pq_gemv_batched",
     "gemv_raw",
+    "gemv_batched_raw",
     "gemm_raw",
     "reconstruct_raw",
     "FASQ_OK",
@@ -39,9 +41,12 @@ __all__ = [
     "FASQ_ERR_UNSUPPORTED",
     "FASQ_ERR_HIP",
     "EXPORTED_SYMBOLS",
+    "ABI_VERSION",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfasq.so")
+
+ABI_VERSION = 2  # FASQ_ABI_VERSION of include/fasq.h
 
 FASQ_OK = 0
 FASQ_ERR_INVALID_ARG = 1
@@ -51,6 +56,7 @@ FASQ_ERR_HIP = 3
 EXPORTED_SYMBOLS = (
     "fasq_pq_gemv",
     "fasq_pq_gemm",
+    "fasq_pq_gemv_batched",
     "fasq_pq_reconstruct",
     "fasq_idx_row_bytes",
     "fasq_status_string",
@@ -94,6 +100,11 @@ def lib() -> ctypes.CDLL:
             f = getattr(L, name)
             f.argtypes = mm
             f.restype = _c_int
+        _pp = ctypes.POINTER(_c_vp)
+        _pi64 = ctypes.POINTER(_c_i64)
+        L.fasq_pq_gemv_batched.argtypes = [_c_vp, _c_i64, _c_i64, _c_int, _pp, _pi64, _pp, _pi64, _pp, _c_int,
+                                           _c_int, _c_vp]
+        L.fasq_pq_gemv_batched.restype = _c_int
         L.fasq_pq_reconstruct.argtypes = [_c_vp, _c_i64, _c_i64, _c_int, _c_int, _c_vp, _c_i64, _c_vp, _c_vp]
         L.fasq_pq_reconstruct.restype = _c_int
         L.fasq_idx_row_bytes.argtypes = [_c_i64, _c_int, _c_int]
@@ -150,6 +161,18 @@ def gemv_raw(x, M, K, N, idx, idx_bits, d, codebook, C, y, stream=0) -> int:
 
 def gemm_raw(x, M, K, N, idx, idx_bits, d, codebook, C, y, stream=0) -> int:
     return lib().fasq_pq_gemm(x, M, K, N, idx, idx_bits, d, codebook, C, y, stream)
+
+
+def gemv_batched_raw(x, M, K, idx, N, codebook, C, y, idx_bits, d, stream=0) -> int:
+    """``idx``, ``N``, ``codebook``, ``C`` and ``y`` are equal-length sequences of
+    integers (device addresses, sizes); they are marshalled into host arrays."""
+    n = len(idx)
+    if not (len(N) == len(codebook) == len(C) == len(y) == n):
+        raise ValueError("the matrix sequences must have equal lengths")
+    arr_p = _c_vp * max(n, 1)
+    arr_i = _c_i64 * max(n, 1)
+    return lib().fasq_pq_gemv_batched(x, M, K, n, arr_p(*idx), arr_i(*N), arr_p(*codebook), arr_i(*C),
+                                      arr_p(*y), idx_bits, d, stream)
 
 
 def reconstruct_raw(idx, N, K, idx_bits, d, codebook, C, w, stream=0) -> int:
@@ -223,6 +246,43 @@ def pq_gemv(x, idx, idx_bits: int, d: int, codebook, out=None):
 def pq_gemm(x, idx, idx_bits: int, d: int, codebook, out=None):
     """Prefill-regime ``y = x . W_hat^T`` (MFMA path); see ``fasq_pq_gemm``."""
     return _matmul(lib().fasq_pq_gemm, x, idx, idx_bits, d, codebook, out)
+
+
+def pq_gemv_batched(x, idxs, idx_bits: int, d: int, codebooks, outs=None):
+    """Decode-regime ``y_i = x . W_hat_i^T`` for several matrices sharing x;
+    see ``fasq_pq_gemv_batched``.  Returns the list of outputs."""
+    torch = _torch()
+    _require(x, "x", torch.float16, 2)
+    M, K = x.shape
+    if len(idxs) != len(codebooks) or (outs is not None and len(outs) != len(idxs)):
+        raise ValueError("idxs, codebooks and outs must have equal lengths")
+    want = idx_row_bytes(K, d, idx_bits)
+    if want < 0:
+        raise ValueError("invalid (K, d, idx_bits)")
+    ys = []
+    for i, (idx, cb) in enumerate(zip(idxs, codebooks)):
+        _require(idx, f"idx[{i}]", torch.uint8, 2)
+        _require(cb, f"codebook[{i}]", torch.float16, 2)
+        if cb.shape[1] != d:
+            raise ValueError(f"codebook[{i}] is [C x {cb.shape[1]}] but d = {d}")
+        if idx.shape[1] != want:
+            raise ValueError(f"idx[{i}] rows are {idx.shape[1]} bytes, expected {want}")
+        if outs is None:
+            y = torch.empty((M, idx.shape[0]), dtype=torch.float16, device=x.device)
+        else:
+            y = outs[i]
+            _require(y, f"out[{i}]", torch.float16, 2)
+            if tuple(y.shape) != (M, idx.shape[0]):
+                raise ValueError(f"out[{i}] must be [M x N]")
+        for t in (idx, cb, y):
+            if t.device != x.device:
+                raise ValueError("all tensors must be on one device")
+        ys.append(y)
+    with torch.cuda.device(x.device):
+        _check(gemv_batched_raw(x.data_ptr(), M, K, [t.data_ptr() for t in idxs], [t.shape[0] for t in idxs],
+                                [t.data_ptr() for t in codebooks], [t.shape[0] for t in codebooks],
+                                [t.data_ptr() for t in ys], idx_bits, d, _stream_handle(x)))
+    return ys
 
 
 def pq_reconstruct(idx, K: int, idx_bits: int, d: int, codebook, out=None):

@@ -13,21 +13,23 @@
 
 namespace fasq {
 
-hipError_t launch_gemv_u8_m1(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
-hipError_t launch_gemv_u12_m1(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
-hipError_t launch_gemv_u16_m1(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
+hipError_t launch_gemv_u8_m1(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream);
+hipError_t launch_gemv_u12_m1(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream);
+hipError_t launch_gemv_u16_m1(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream);
 hipError_t launch_gemv_u8_m16(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
 hipError_t launch_gemv_u12_m16(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
 hipError_t launch_gemv_u16_m16(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
 
-hipError_t launch_gemv(const Problem& p, const DeviceInfo& dev, hipStream_t stream) {
-  if (p.M == 1) {
-    switch (p.idx_bits) {
-      case 8: return launch_gemv_u8_m1(p, dev, stream);
-      case 12: return launch_gemv_u12_m1(p, dev, stream);
-      default: return launch_gemv_u16_m1(p, dev, stream);
-    }
+hipError_t launch_gemv_m1_group(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream) {
+  switch (ps[0].idx_bits) {
+    case 8: return launch_gemv_u8_m1(ps, count, dev, stream);
+    case 12: return launch_gemv_u12_m1(ps, count, dev, stream);
+    default: return launch_gemv_u16_m1(ps, count, dev, stream);
   }
+}
+
+hipError_t launch_gemv(const Problem& p, const DeviceInfo& dev, hipStream_t stream) {
+  if (p.M == 1) return launch_gemv_m1_group(&p, 1, dev, stream);
   if (p.M > 16) return hipErrorNotSupported;
   switch (p.idx_bits) {
     case 8: return launch_gemv_u8_m16(p, dev, stream);
@@ -171,6 +173,43 @@ fasq_status fasq_pq_gemv(const void* x, int64_t M, int64_t K, int64_t N, const v
   fasq_status s = fasq::validate(M, K, N, idx_bits, d, C, x, idx, codebook, y, true);
   if (s != FASQ_OK) return s;
   return fasq::run(fasq::make_problem(x, M, K, N, idx, idx_bits, d, codebook, C, y), fasq::Regime::kGemv, stream);
+}
+
+fasq_status fasq_pq_gemv_batched(const void* x, int64_t M, int64_t K, int count, const void* const* idx,
+                                 const int64_t* N, const void* const* codebook, const int64_t* C, void* const* y,
+                                 int idx_bits, int d, hipStream_t stream) {
+  if (count < 1) return fasq::fail(FASQ_ERR_INVALID_ARG, "count must be >= 1");
+  if (idx == nullptr || N == nullptr || codebook == nullptr || C == nullptr || y == nullptr)
+    return fasq::fail(FASQ_ERR_INVALID_ARG, "a matrix array is NULL");
+  for (int i = 0; i < count; ++i) {
+    fasq_status s = fasq::validate(M, K, N[i], idx_bits, d, C[i], x, idx[i], codebook[i], y[i], true);
+    if (s != FASQ_OK) {
+      fasq::t_last_error = "matrix " + std::to_string(i) + ": " + fasq::t_last_error;
+      return s;
+    }
+  }
+  fasq::DeviceInfo dev;
+  hipError_t e = fasq::device_info(&dev);
+  if (e != hipSuccess) return fasq::hip_fail("querying the current device", e);
+  Problem ps[fasq::kMaxBatchLaunch];
+  for (int off = 0; off < count; off += fasq::kMaxBatchLaunch) {
+    const int n = count - off < fasq::kMaxBatchLaunch ? count - off : fasq::kMaxBatchLaunch;
+    for (int i = 0; i < n; ++i)
+      ps[i] = fasq::make_problem(x, M, K, N[off + i], idx[off + i], idx_bits, d, codebook[off + i], C[off + i],
+                                 y[off + i]);
+    e = hipErrorNotSupported;
+    if (M == 1 && !fasq::force_generic()) e = fasq::launch_gemv_m1_group(ps, n, dev, stream);
+    if (e == hipErrorNotSupported) {
+      for (int i = 0; i < n; ++i) {
+        fasq_status s = fasq::run(ps[i], fasq::Regime::kGemv, stream);
+        if (s != FASQ_OK) return s;
+      }
+    } else if (e != hipSuccess) {
+      return fasq::hip_fail("kernel launch", e);
+    }
+  }
+  fasq::t_last_error.clear();
+  return FASQ_OK;
 }
 
 fasq_status fasq_pq_gemm(const void* x, int64_t M, int64_t K, int64_t N, const void* idx, int idx_bits, int d,

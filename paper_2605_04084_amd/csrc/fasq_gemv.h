@@ -239,19 +239,31 @@ namespace fasq {
 // matrix core does 16x the useful MACs, which it has to spare at decode
 // arithmetic intensity.
 // ---------------------------------------------------------------------------
-struct GemvM1Args {
-  const half_t* x;
-  int64_t K, N;
+// One matrix of a single-token launch.  Workgroups [wg_begin, wg_begin +
+// wg_count) of the grid work on it.
+struct GemvM1Mat {
   const uint8_t* idx;
-  int64_t R;   // bytes per row (= CH * chunk bytes)
-  int64_t CH;  // chunks per row
   const half_t* cb;
+  half_t* y;
+  int64_t N;
   int C;
+  int wg_begin;
+  int wg_count;
+};
+
+constexpr int kM1MaxMats = 8;  // matrices one single-token launch can take
+
+struct GemvM1Args {
+  const half_t* x;  // shared by every matrix of the launch
+  int64_t K;
+  int64_t R;     // bytes per row (= CH * chunk bytes)
+  int64_t CH;    // chunks per row
   int P;         // waves per row (K split inside the workgroup)
   int NRW;       // rows per row group
   int cb_bytes;  // LDS bytes of the codebook (x follows)
   int x_bytes;   // LDS bytes of x (partials follow)
-  half_t* y;
+  int nmat;
+  GemvM1Mat mat[kM1MaxMats];
 };
 
 template <int BITS, int D, int T, int MODE, bool MASK>
@@ -265,6 +277,20 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
   constexpr bool kXInRegs = T * SPC <= 8;
 
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+
+  // the matrix of this workgroup, and the workgroup's place among its own
+  int m = 0;
+#pragma unroll
+  for (int i = 1; i < kM1MaxMats; ++i)
+    if (i < a.nmat && (int)blockIdx.x >= a.mat[i].wg_begin) m = i;
+  const uint8_t* __restrict__ idx = a.mat[m].idx;
+  const half_t* __restrict__ cb = a.mat[m].cb;
+  half_t* __restrict__ y = a.mat[m].y;
+  const int64_t N = a.mat[m].N;
+  const int C = a.mat[m].C;
+  const uint32_t wg = (uint32_t)blockIdx.x - (uint32_t)a.mat[m].wg_begin;
+  const uint32_t nwg = (uint32_t)a.mat[m].wg_count;
+
   uint8_t* xl = smem + a.cb_bytes;
   float* red = reinterpret_cast<float*>(smem + a.cb_bytes + a.x_bytes);  // [Q * NRW][P]
 
@@ -284,13 +310,13 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
   auto ccol = [&](int t) { const int c = ccol_raw(t); return c < CH ? c : CH - 1; };
 
   // Rows are dealt round-robin: local row rr of row group q of workgroup w is
-  // row w + (rr * Q + q) * gridDim.x.  The byte offset of the lane's chunk in
+  // row w + (rr * Q + q) * nwg.  The byte offset of the lane's chunk in
   // unit t of local row rr is row0 + rr * rstride + t * 64 * CBY.  Rows past N
   // (the pipeline reads up to L / T rows ahead) lie past the end of the
   // buffer resource and load zeros.
-  const __amdgpu_buffer_rsrc_t rsrc = idx_rsrc(a.idx, (uint32_t)(a.N * a.R));
-  const uint32_t rstride = (uint32_t)Q * gridDim.x * (uint32_t)a.R;
-  const uint32_t row0 = ((uint32_t)blockIdx.x + (uint32_t)q * gridDim.x) * (uint32_t)a.R +
+  const __amdgpu_buffer_rsrc_t rsrc = idx_rsrc(idx, (uint32_t)(N * a.R));
+  const uint32_t rstride = (uint32_t)Q * nwg * (uint32_t)a.R;
+  const uint32_t row0 = (wg + (uint32_t)q * nwg) * (uint32_t)a.R +
                         (uint32_t)ccol_raw(0) * CBY;
 
   uint32_t buf[L][DW];
@@ -300,7 +326,7 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
 
   // ---- prologue (see k_gemv): codebook and x first, then the index stream
   CbStage cst;
-  cb_fetch<D, MODE>(a.cb, a.C, cst);
+  cb_fetch<D, MODE>(cb, C, cst);
   // x in 16-byte words: thread t stages words t and t + blockDim.x; waves
   // whose words all lie past the end of x issue no load for them.
   constexpr int XWT = 2;
@@ -323,7 +349,7 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
 #pragma unroll
   for (int i = 0; i < kM1EarlyLoads; ++i) load_unit(i, row0 + (uint32_t)(i / T) * rstride, i % T);
 
-  cb_store<D, MODE>(smem, a.cb, a.C, cst);
+  cb_store<D, MODE>(smem, cb, C, cst);
 #pragma unroll
   for (int k = 0; k < XWT; ++k) {
     const int w = threadIdx.x + k * blockDim.x;
@@ -359,7 +385,7 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
     const bool cval = !MASK || ccol_raw(t) < CH;
 #pragma unroll
     for (int s = 0; s < SPC; ++s) {
-      half8_t aop = gather8<BITS, D, MODE>(a.cb, lane_off, w, s * (8 / D));
+      half8_t aop = gather8<BITS, D, MODE>(cb, lane_off, w, s * (8 / D));
       half8_t bop;
       if constexpr (kXInRegs) bop = xreg[t * SPC + s];
       else bop = *reinterpret_cast<const half8_t*>(xl + ccol(t) * (G * D * 2) + s * 16);
@@ -411,11 +437,11 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
   // fixed-order sum over the P waves of each row, one fp16 rounding
   const int rows = Q * a.NRW;
   for (int r = threadIdx.x; r < rows; r += blockDim.x) {
-    const int64_t n = (int64_t)blockIdx.x + (int64_t)r * gridDim.x;
-    if (n < a.N) {
+    const int64_t n = (int64_t)wg + (int64_t)r * nwg;
+    if (n < N) {
       float sum = 0.f;
       for (int pp = 0; pp < P; ++pp) sum += red[r * P + pp];
-      a.y[n] = static_cast<half_t>(sum);
+      y[n] = static_cast<half_t>(sum);
     }
   }
 }

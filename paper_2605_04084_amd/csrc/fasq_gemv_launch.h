@@ -9,6 +9,7 @@
 namespace fasq {
 
 constexpr int kLdsCodebookBudget = 64 * 1024;  // bytes of LDS a codebook may take
+static_assert(kM1MaxMats == kMaxBatchLaunch, "grouped launches and their kernel disagree on the group size");
 
 // Once per device and kernel: check that the kernel declares no static LDS
 // (its LDS-resident codebook is addressed from LDS address 0) and raise its
@@ -183,30 +184,39 @@ hipError_t launch_gemv_m1_mode(const GemvM1Args& a, int mode, int T, bool mask, 
   }
 }
 
-// One token: choose T (wave-wide loads per row part), P (waves per row), Q
-// (row groups per workgroup) and the grid; hipErrorNotSupported when another
-// kernel has to take the call.
+// One token, one launch over `count` <= kM1MaxMats matrices that share x, K,
+// d and the id width: choose T (wave-wide loads per row part), P (waves per
+// row), Q (row groups per workgroup), the workgroups of each matrix and the
+// rows per row group; hipErrorNotSupported when another kernel has to take
+// the call.
 template <int BITS>
-hipError_t launch_gemv_m1_bits(const Problem& p, const DeviceInfo& dev, hipStream_t stream) {
+hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream) {
   constexpr int G = Chunk<BITS>::G;
   constexpr int CBY = Chunk<BITS>::DW * 4;
+  if (count < 1 || count > kM1MaxMats) return hipErrorNotSupported;
+  const Problem& p = ps[0];
   const int d = p.d;
   if (p.M != 1) return hipErrorNotSupported;
   if (!(d == 1 || d == 2 || d == 4 || d == 8)) return hipErrorNotSupported;
   if (p.S % G || p.K % 8) return hipErrorNotSupported;
   const int64_t CH = p.S / G;
   if (CH * CBY != p.R) return hipErrorNotSupported;
-  if (p.N * p.R >= (int64_t(1) << 32)) return hipErrorNotSupported;
-  const uintptr_t ia = reinterpret_cast<uintptr_t>(p.idx);
-  if ((ia & (CBY == 16 ? 15 : 3)) || (reinterpret_cast<uintptr_t>(p.x) & 15) ||
-      (reinterpret_cast<uintptr_t>(p.codebook) & 15))
-    return hipErrorNotSupported;
+  if (reinterpret_cast<uintptr_t>(p.x) & 15) return hipErrorNotSupported;
+  int64_t maxC = 0, total_rows = 0;
+  for (int i = 0; i < count; ++i) {
+    const Problem& pi = ps[i];
+    if (pi.M != 1 || pi.K != p.K || pi.d != d || pi.idx_bits != p.idx_bits || pi.x != p.x) return hipErrorNotSupported;
+    if (pi.N * pi.R >= (int64_t(1) << 32)) return hipErrorNotSupported;
+    if ((reinterpret_cast<uintptr_t>(pi.idx) & (CBY == 16 ? 15 : 3)) || (reinterpret_cast<uintptr_t>(pi.codebook) & 15))
+      return hipErrorNotSupported;
+    if (pi.C > maxC) maxC = pi.C;
+    total_rows += pi.N;
+  }
 
   const int SPC = G * d / 8;
   const int64_t CHW = (CH + 63) / 64;  // wave-wide loads per row
   const int tx = SPC <= 8 ? 8 / SPC : 0;  // largest T whose x slices fit the register budget
   int T = 0;
-  bool mask = false;
   for (int t : {8, 4, 2, 1}) {  // exact split, x in registers
     if (t <= tx && CHW % t == 0 && CHW / t <= 16) { T = t; break; }
   }
@@ -222,48 +232,90 @@ hipError_t launch_gemv_m1_bits(const Problem& p, const DeviceInfo& dev, hipStrea
   }
   if (T == 0) return hipErrorNotSupported;
   const int P = (int)((CHW + T - 1) / T);
-  mask = (int64_t)P * T * 64 != CH;
+  const bool mask = (int64_t)P * T * 64 != CH;
 
-  const int mode = choose_cb_mode(p.C, d);
-  const int cb_bytes = (int)cb_lds_bytes(mode, p.C, d);
+  // One codebook placement for the launch: the largest codebook decides it.
+  const int mode = choose_cb_mode(maxC, d);
+  if (mode != CB_GLOBAL)  // every codebook must be whole 16-byte words to be staged
+    for (int i = 0; i < count; ++i)
+      if ((ps[i].C * d * 2) % 16 != 0) return hipErrorNotSupported;
+  const int cb_bytes = (int)cb_lds_bytes(mode, maxC, d);
   const int64_t x_bytes = (p.K * 2 + 15) / 16 * 16;
   const int64_t avail = dev.lds_per_block - cb_bytes - x_bytes;
 
   // Q row groups per workgroup: enough workgroups to cover every CU for
-  // small N, up to 16 waves per workgroup.
-  int64_t Q = (p.N + dev.num_cus - 1) / dev.num_cus;
+  // small N, up to 16 waves per workgroup.  Workgroups are shared out in
+  // proportion to the rows of each matrix, one per CU in all.
+  const int64_t ncu = dev.num_cus;
+  int64_t Q = (total_rows + ncu - 1) / ncu;
   if (Q > 16 / P) Q = 16 / P;
   if (Q < 1) Q = 1;
-  int64_t nwg = (p.N + Q - 1) / Q;
-  if (nwg > dev.num_cus) nwg = dev.num_cus;
-  int64_t nrw = (p.N + nwg * Q - 1) / (nwg * Q);
+  int64_t wgs[kM1MaxMats];
+  int64_t used = 0;
+  for (int i = 0; i < count; ++i) {
+    int64_t w = ncu * ps[i].N / total_rows;
+    const int64_t cap = (ps[i].N + Q - 1) / Q;  // no workgroup without a row group
+    if (w > cap) w = cap;
+    if (w < 1) w = 1;
+    wgs[i] = w;
+    used += w;
+  }
+  // hand the remaining CUs to the matrices with the most rows per workgroup
+  while (used < ncu) {
+    int best = -1;
+    int64_t best_load = 0;
+    for (int i = 0; i < count; ++i) {
+      const int64_t load = (ps[i].N + wgs[i] - 1) / wgs[i];
+      if (wgs[i] < (ps[i].N + Q - 1) / Q && load > best_load) { best = i; best_load = load; }
+    }
+    if (best < 0) break;
+    ++wgs[best];
+    ++used;
+  }
+  int64_t nrw = 1;
+  for (int i = 0; i < count; ++i) {
+    const int64_t r = (ps[i].N + wgs[i] * Q - 1) / (wgs[i] * Q);
+    if (r > nrw) nrw = r;
+  }
   const int64_t nrw_max = avail / (4 * Q * P);
   if (nrw_max < 1) return hipErrorNotSupported;
-  if (nrw > nrw_max) {
+  if (nrw > nrw_max) {  // LDS bound: more workgroups than CUs
     nrw = nrw_max;
-    nwg = (p.N + nrw * Q - 1) / (nrw * Q);
+    for (int i = 0; i < count; ++i) wgs[i] = (ps[i].N + nrw * Q - 1) / (nrw * Q);
+  }
+  int64_t nwg = 0;
+  for (int i = 0; i < count; ++i) {
+    // 32-bit buffer offsets must cover every row the pipeline reads, including
+    // the rows it reads ahead past the last one (those load zeros).
+    if ((wgs[i] * Q * (nrw + kGemvPipe / T + 1)) * ps[i].R >= (int64_t(1) << 32)) return hipErrorNotSupported;
+    nwg += wgs[i];
   }
   if (nwg > 0x7fffffff || nrw * T > 0x7fffffff) return hipErrorNotSupported;
-  // 32-bit buffer offsets must cover every row the pipeline reads, including
-  // the rows it reads ahead past the last one (those load zeros).
-  if ((nwg * Q * (nrw + kGemvPipe / T + 1)) * p.R >= (int64_t(1) << 32)) return hipErrorNotSupported;
   const int lds = (int)(cb_bytes + x_bytes + Q * nrw * P * 4);
   const int threads = (int)(P * Q * kWave);
 
-  GemvM1Args a;
+  GemvM1Args a = {};
   a.x = static_cast<const half_t*>(p.x);
   a.K = p.K;
-  a.N = p.N;
-  a.idx = static_cast<const uint8_t*>(p.idx);
   a.R = p.R;
   a.CH = CH;
-  a.cb = static_cast<const half_t*>(p.codebook);
-  a.C = (int)p.C;
   a.P = P;
   a.NRW = (int)nrw;
   a.cb_bytes = cb_bytes;
   a.x_bytes = (int)x_bytes;
-  a.y = static_cast<half_t*>(p.y);
+  a.nmat = count;
+  int64_t begin = 0;
+  for (int i = 0; i < count; ++i) {
+    GemvM1Mat& mt = a.mat[i];
+    mt.idx = static_cast<const uint8_t*>(ps[i].idx);
+    mt.cb = static_cast<const half_t*>(ps[i].codebook);
+    mt.y = static_cast<half_t*>(ps[i].y);
+    mt.N = ps[i].N;
+    mt.C = (int)ps[i].C;
+    mt.wg_begin = (int)begin;
+    mt.wg_count = (int)wgs[i];
+    begin += wgs[i];
+  }
   switch (d) {
     case 1: return launch_gemv_m1_mode<BITS, 1>(a, mode, T, mask, threads, (int)nwg, lds, stream);
     case 2: return launch_gemv_m1_mode<BITS, 2>(a, mode, T, mask, threads, (int)nwg, lds, stream);

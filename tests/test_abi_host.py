@@ -39,7 +39,9 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_abi_version(L):
-    assert fasq.abi_version() == 1
+    assert fasq.abi_version() == fasq.ABI_VERSION
+    m = re.search(r"#define FASQ_ABI_VERSION (\d+)", open(HEADER).read())
+    assert int(m.group(1)) == fasq.ABI_VERSION
 
 
 def test_status_strings(L):
@@ -110,3 +112,36 @@ def test_binding_has_no_cpu_compute_path():
     for f in os.listdir(os.path.join(ROOT, "paper_2605_04084_amd", "csrc")):
         text = open(os.path.join(ROOT, "paper_2605_04084_amd", "csrc", f)).read()
         assert "oracle" not in text.lower(), f
+
+
+def _batched(**kw):
+    a = dict(x=DUMMY, M=1, K=16, idx=[DUMMY, DUMMY], N=[4, 8], codebook=[DUMMY, DUMMY], C=[256, 16],
+             y=[DUMMY + 64, DUMMY + 128], idx_bits=8, d=2)
+    a.update(kw)
+    return fasq.gemv_batched_raw(a["x"], a["M"], a["K"], a["idx"], a["N"], a["codebook"], a["C"], a["y"],
+                                 a["idx_bits"], a["d"], 0)
+
+
+@pytest.mark.parametrize("args,why", [
+    (dict(idx=[], N=[], codebook=[], C=[], y=[]), "count"),
+    (dict(N=[4, 0]), "matrix 1: M, K and N"),
+    (dict(C=[256, 257]), "matrix 1: C must"),
+    (dict(idx=[0, DUMMY]), "matrix 0: a buffer pointer is NULL"),
+    (dict(y=[DUMMY, 0]), "matrix 1: a buffer pointer is NULL"),
+    (dict(x=0), "matrix 0: a buffer pointer is NULL"),
+    (dict(K=10, d=4), "matrix 0: K must be a multiple of d"),
+])
+def test_batched_invalid_arguments_rejected_without_launch(L, args, why):
+    assert _batched(**args) == fasq.FASQ_ERR_INVALID_ARG
+    assert why in fasq.last_error()
+
+
+def test_batched_null_arrays_rejected(L):
+    st = L.fasq_pq_gemv_batched(DUMMY, 1, 16, 2, None, None, None, None, None, 8, 2, None)
+    assert st == fasq.FASQ_ERR_INVALID_ARG
+    assert "array is NULL" in fasq.last_error()
+
+
+def test_batched_binding_checks_lengths(L):
+    with pytest.raises(ValueError):
+        fasq.gemv_batched_raw(DUMMY, 1, 16, [DUMMY], [4, 4], [DUMMY], [16], [DUMMY], 8, 2)

@@ -287,3 +287,73 @@ def test_errors_surface_as_exceptions():
         fasq.pq_gemv(torch.zeros((16, 2), dtype=torch.float16, device="cuda:0").t(), idx, 8, 2, cb)
     st = fasq.gemv_raw(x.data_ptr(), 1, 16, 4, idx.data_ptr(), 8, 2, cb.data_ptr(), 300, x.data_ptr(), 0)
     assert st == fasq.FASQ_ERR_INVALID_ARG
+
+
+# ---------------------------------------------------------------------------
+# Several matrices sharing x in one call (fasq_pq_gemv_batched)
+# ---------------------------------------------------------------------------
+
+def _batched(x, probs, bits, d):
+    ys = fasq.pq_gemv_batched(to_dev(x), [to_dev(p.idx) for p in probs], bits, d,
+                              [to_dev(p.codebook) for p in probs])
+    return [to_np(y) for y in ys]
+
+
+BATCH_CASES = [
+    # M, K, d, bits, [(N, C), ...]
+    (1, 4096, 2, 8, [(4096, 256), (1024, 256), (1024, 256)]),      # q, k, v shapes
+    (1, 4096, 2, 8, [(14336, 256), (14336, 256)]),                 # gate, up shapes
+    (1, 256, 2, 8, [(1, 256), (300, 256), (17, 64), (129, 8)]),    # ragged N, mixed C
+    (1, 512, 4, 12, [(100, 4096), (33, 4096), (257, 1000)]),
+    (1, 320, 4, 16, [(64, 65536), (65, 300)]),
+    (1, 256, 2, 8, [(40 + 7 * i, 256) for i in range(11)]),        # more than one launch's worth
+    (3, 256, 2, 8, [(70, 256), (130, 256)]),                       # M > 1: one call per matrix
+    (1, 96, 3, 8, [(20, 7), (9, 5)]),                              # d = 3: general kernel
+]
+
+
+@pytest.mark.parametrize("case", BATCH_CASES)
+def test_batched_matches_single_calls_and_oracle(case):
+    M, K, d, bits, mats = case
+    print(f"[case] batched {case}", flush=True)
+    rng = np.random.default_rng(len(mats) * 1000 + K)
+    probs = [pi.draw_problem(rng, M, K, N, d, C, bits) for N, C in mats]
+    x = probs[0].x
+    got = _batched(x, probs, bits, d)
+    for i, p in enumerate(probs):
+        single = to_np(fasq.pq_gemv(to_dev(x), to_dev(p.idx), bits, d, to_dev(p.codebook)))
+        assert np.array_equal(got[i].view(np.uint16), single.view(np.uint16)), f"matrix {i}"
+        rows = sample_rows(p.N)
+        ref = orc.pq_linear(x, p.idx, bits, d, p.codebook, rows=rows)
+        assert_close(got[i].astype(np.float64)[:, rows], ref, f"batched matrix {i}")
+
+
+def test_batched_layer_groups_full_size():
+    """q/k/v and gate/up of the effective-4-bit layer as grouped launches."""
+    w = pi.workload("llama3_8b_4bit")
+    for group in ((0, 1, 2), (4, 5)):
+        probs = [w.problem(i) for i in group]
+        x = probs[0].x
+        got = _batched(x, probs, probs[0].idx_bits, probs[0].d)
+        for g, p in zip(got, probs):
+            rows = sample_rows(p.N)
+            ref = orc.pq_linear(x, p.idx, p.idx_bits, p.d, p.codebook, rows=rows)
+            assert_close(g.astype(np.float64)[:, rows], ref, f"group {group}")
+
+
+def test_batched_one_hot_bit_exact():
+    """Signed one-hot codebooks with ternary x: every partial sum is an exact
+    integer, so each grouped output equals the oracle bit for bit."""
+    rng = np.random.default_rng(77)
+    K, d = 1024, 2
+    x = pi.ternary_x(rng, 1, K)
+    probs = []
+    for N in (513, 64, 1000):
+        cb = pi.signed_one_hot_codebook(256, d, rng)
+        ids = rng.integers(0, 256, size=(N, K // d))
+        probs.append(pi.PQProblem(M=1, K=K, N=N, d=d, C=256, idx_bits=8, codebook=cb, ids=ids,
+                                  idx=pi.pack_indices(ids, 8), x=x))
+    got = _batched(x, probs, 8, d)
+    for g, p in zip(got, probs):
+        ref = orc.pq_linear(x, p.idx, 8, d, p.codebook)
+        assert np.array_equal(g.astype(np.float64), ref)
