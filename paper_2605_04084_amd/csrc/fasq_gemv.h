@@ -48,13 +48,12 @@ struct GemvArgs {
 };
 
 constexpr int kGemvPipe = 8;      // load units per wave in the software pipeline
-constexpr int kM1EarlyLoads = 2;  // index loads per wave issued before the codebook barrier (M = 1)
-
-// Highest unit whose load has been issued once unit i of the first window has
-// been computed (i = -1: before any): two more per unit, at most L ahead.
-__host__ __device__ constexpr int m1_ramp_hi(int i) {
-  return (kM1EarlyLoads - 1 + 2 * (i + 1)) < (i + kGemvPipe) ? (kM1EarlyLoads - 1 + 2 * (i + 1)) : (i + kGemvPipe);
-}
+// Index loads each single-token wave keeps in flight.  Two per wave (32 KB
+// per CU at 16 waves) already saturate a CU's share of HBM; more only make
+// waves wait at the issue of loads that cannot enter the queue, where they
+// cannot compute the data that has arrived.
+constexpr int kM1Window = 2;
+static_assert(kM1Window <= kGemvPipe, "the window must fit the load slots");
 constexpr int kXWordsPerThread = 8;  // first-round x words (16 B) per thread for M > 1
 
 // MASK: some lanes of the last wave of a row see chunk columns past the end
@@ -341,13 +340,13 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
     }
   }
   // Every wave's codebook and x requests enter the CU's (in-order) memory
-  // queue before any index load, and only kM1EarlyLoads index loads per wave
-  // go out before the staging barrier: the barrier then waits for the small
-  // staging data alone, not for the whole workgroup to get its pipeline
-  // loads accepted by a saturated memory queue.
+  // queue before any index load, and only the first kM1Window index loads of
+  // a wave go out before the staging barrier: the barrier then waits for the
+  // small staging data alone, not for the whole workgroup to get its loads
+  // accepted by a saturated memory queue.
   __syncthreads();
 #pragma unroll
-  for (int i = 0; i < kM1EarlyLoads; ++i) load_unit(i, row0 + (uint32_t)(i / T) * rstride, i % T);
+  for (int i = 0; i < kM1Window; ++i) load_unit(i, row0 + (uint32_t)(i / T) * rstride, i % T);
 
   cb_store<D, MODE>(smem, cb, C, cst);
 #pragma unroll
@@ -412,24 +411,15 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
     }
   };
 
-  // Unit k lives in slot k % L.  A wave computes a unit before it issues more
-  // loads, so data that has arrived is never held up behind a load waiting
-  // for room in the memory queue.  First window: the loads not issued before
-  // the barrier go out two per computed unit until L are in flight.
-#pragma unroll
-  for (int i = 0; i < L; ++i) {
-    if (i < nunits) compute_unit(i, i, i % T);
-#pragma unroll
-    for (int k = m1_ramp_hi(i - 1) + 1; k <= m1_ramp_hi(i); ++k)
-      load_unit(k % L, row0 + (uint32_t)(k / T) * rstride, k % T);
-  }
-  // Steady state: after unit base + i, issue unit base + i + L into its slot.
-  uint32_t rbase = row0 + (uint32_t)(L / T) * rstride;  // offset of local row base / T
-  for (int base = L; base < nunits; base += L, rbase += (uint32_t)(L / T) * rstride) {
+  // Unit k lives in slot k % L, and kM1Window loads stay in flight.  A wave
+  // computes a unit before it issues the next load, so data that has arrived
+  // is never held up behind a load waiting for room in the memory queue.
+  uint32_t rbase = row0;  // offset of local row base / T
+  for (int base = 0; base < nunits; base += L, rbase += (uint32_t)(L / T) * rstride) {
 #pragma unroll
     for (int i = 0; i < L; ++i) {
       if (base + i < nunits) compute_unit(i, base + i, i % T);
-      load_unit(i, rbase + (uint32_t)((i + L) / T) * rstride, i % T);
+      load_unit((i + kM1Window) % L, rbase + (uint32_t)((i + kM1Window) / T) * rstride, (i + kM1Window) % T);
     }
   }
   __syncthreads();
