@@ -49,14 +49,13 @@ hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t
   if ((reinterpret_cast<uintptr_t>(p.x) & 15) || (reinterpret_cast<uintptr_t>(p.codebook) & 15) ||
       (reinterpret_cast<uintptr_t>(p.idx) & 15) || (p.R & 3))
     return hipErrorNotSupported;
-  // per-lane index runs are read as 16/8/4-byte words: they must be aligned so
+  // id runs are copied as 4-byte words
   const int hb = (32 / d) * p.idx_bits / 8;
-  const int align = (hb % 16 == 0) ? 16 : (hb % 8 == 0) ? 8 : 4;
-  if (p.R % align) return hipErrorNotSupported;
+  if (hb % 4) return hipErrorNotSupported;
 
   const int mode = choose_cb_mode(p.C, d);
   const int cb_bytes = (int)cb_lds_bytes(mode, p.C, d);
-  const int lds = cb_bytes + 2 * 128 * kXRowBytes;
+  const int lds = cb_bytes + kGemmStages * (128 * 128 + 128 * 2 * hb);
   if (lds > dev.lds_per_block) return hipErrorNotSupported;
 
   GemmArgs a;

@@ -4,16 +4,22 @@
 //   * A workgroup of 4 waves owns a BM x BN output tile; the waves form a
 //     2 x 2 grid, each wave owning (BM/2) x (BN/2) = FM x FN MFMA tiles of
 //     32 x 32 with fp32 accumulators in registers.
-//   * K is walked in chunks of 64.  The X chunk (BM x 64 fp16) is staged in
-//     LDS (row stride padded to 144 B so that the 16-byte operand reads of one
-//     LDS cycle hit distinct banks), double-buffered, with the next chunk held
-//     in registers while the current one is consumed.
+//   * K is walked in chunks of 64.  Each chunk's X tile (BM x 64 fp16) and
+//     packed-id tile (BN columns) are copied from global memory straight
+//     into LDS (global_load_lds), NS chunks ahead, into a ring of NS LDS
+//     stages: the copies need no registers, so the loads of several chunks
+//     are in flight while one is computed.  X rows are 128 B with their
+//     16-byte granules XOR-swizzled by (row / 2) mod 8, so the MFMA operand
+//     reads of one LDS cycle hit distinct banks.
 //   * W_hat is never written to memory, not even to LDS: each lane decodes
-//     the ids of its own B-operand column straight from the packed index row
-//     and gathers the codewords from the LDS codebook into the MFMA B
-//     registers.  The order of K inside a chunk is permuted identically for
-//     A and B (allowed: the contraction is a sum over K), so that lane half h
-//     reads one contiguous run of 32/d ids per chunk.
+//     the ids of its own B-operand column from the staged id tile and
+//     gathers the codewords from the LDS codebook into the MFMA B registers.
+//     The order of K inside a chunk is permuted identically for A and B
+//     (allowed: the contraction is a sum over K), so that lane half h reads
+//     one contiguous run of 32/d ids per chunk.
+//   * Synchronisation per chunk: an explicit wait for this wave's copies of
+//     the chunk, then one workgroup barrier (every wave's copies are in, and
+//     every wave is done with the stage about to be refilled).
 //   * Epilogue: fp32 -> fp16 once, direct stores.
 #pragma once
 
@@ -24,7 +30,7 @@
 namespace fasq {
 
 constexpr int kGemmKC = 64;          // K per chunk
-constexpr int kXRowBytes = 144;      // padded LDS row of one X chunk (128 B of data)
+constexpr int kGemmStages = 4;       // LDS ring depth (chunks in flight + 1)
 
 struct GemmArgs {
   const half_t* x;
@@ -37,20 +43,47 @@ struct GemmArgs {
   half_t* y;
 };
 
+// Bytes of one packed-id run (one lane half, one chunk) and of one stage.
+template <int BITS, int D>
+__host__ __device__ constexpr int gemm_run_bytes() { return (32 / D) * BITS / 8; }
+template <int BITS, int D, int BM, int BN>
+__host__ __device__ constexpr int gemm_stage_bytes() { return BM * 128 + BN * 2 * gemm_run_bytes<BITS, D>(); }
+
+// Copy 16 (or 4) bytes per lane from global memory into LDS: lane i's data
+// lands at lds + 16 i (4 i).
+__device__ __forceinline__ void copy16_to_lds(const void* src, uint8_t* lds) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+__device__ __forceinline__ void copy4_to_lds(const void* src, uint8_t* lds) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds, 4, 0, 0);
+}
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt out of range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
 template <int BITS, int D, int MODE, int BM, int BN>
 __global__ __launch_bounds__(256) void k_gemm_mfma(GemmArgs a) {
+  constexpr int NS = kGemmStages;
   constexpr int WM = BM / 2, WN = BN / 2;
   constexpr int FM = WM / 32, FN = WN / 32;
-  constexpr int IDS_HALF = 32 / D;                 // ids per lane half per chunk
-  constexpr int HB = IDS_HALF * BITS / 8;          // bytes per lane half per chunk
-  constexpr int HW = HB / 4;                       // dwords per lane half per chunk
+  constexpr int HB = gemm_run_bytes<BITS, D>();    // bytes per lane half per chunk
   constexpr int IPS = 8 / D;                       // ids per k-step per lane
-  constexpr int XPASS = BM * 128 / (256 * 16);     // 16-byte X loads per thread per chunk
+  constexpr int XI = BM / 32;                      // X copy instructions per wave per chunk (8 rows each)
+  constexpr int IW = 2 * HB / 4;                   // id words per column per chunk
+  constexpr int II = BN * IW / 256;                // id copy instructions per wave per chunk
+  constexpr int LPC = XI + II;                     // vector-memory instructions per wave per chunk
+  constexpr int XBYTES = BM * 128;
+  constexpr int SBYTES = gemm_stage_bytes<BITS, D, BM, BN>();
   static_assert(HB % 4 == 0, "index run must be whole dwords");
-  static_assert(XPASS >= 1, "tile too small");
+  static_assert((BN * IW) % 256 == 0, "id tile must split evenly over the workgroup");
+  static_assert(LPC * (NS - 2) < 64, "too many loads in flight for vmcnt");
 
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  uint8_t* xs = smem + a.cb_lds_bytes;  // 2 x [BM][144 B]
+  uint8_t* ring = smem + a.cb_lds_bytes;  // NS stages of [X tile][id tile]
 
   const int tid = threadIdx.x;
   const int wave = tid / kWave, lane = tid % kWave;
@@ -58,73 +91,43 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(GemmArgs a) {
   const int h = lane >> 5, l32 = lane & 31;
   const int64_t m0 = (int64_t)blockIdx.y * BM;
   const int64_t n0 = (int64_t)blockIdx.x * BN;
-  const int64_t nchunks = a.K / kGemmKC;
+  const int nchunks = (int)(a.K / kGemmKC);
 
-  // ---- index pointers for this lane's B columns
-  const uint8_t* irow[FN];
-  bool nval[FN];
+  // ---- copy sources of this lane (rows >= M read row M - 1, columns >= N
+  //      read column 0: they are computed but never stored)
+  const half_t* xsrc[XI];
 #pragma unroll
-  for (int fn = 0; fn < FN; ++fn) {
-    const int64_t n = n0 + wn * WN + fn * 32 + l32;
-    nval[fn] = n < a.N;
-    irow[fn] = a.idx + (nval[fn] ? n : 0) * a.R + h * HB;
+  for (int j = 0; j < XI; ++j) {
+    const int r = wave * (BM / 4) + j * 8 + lane / 8;  // tile row
+    const int g = (lane % 8) ^ ((r >> 1) & 7);         // granule stored in slot lane % 8
+    const int64_t m = m0 + r;
+    xsrc[j] = a.x + (m < a.M ? m : a.M - 1) * a.K + g * 8;
   }
-  auto load_ids = [&](uint32_t (&buf)[FN][HW], int64_t c) {
+  const uint8_t* isrc[II];
 #pragma unroll
-    for (int fn = 0; fn < FN; ++fn) {
-      const uint32_t* p = reinterpret_cast<const uint32_t*>(irow[fn] + c * (2 * HB));
-      if constexpr (HW % 4 == 0) {
-#pragma unroll
-        for (int w = 0; w < HW; w += 4) {
-          const u32x4 v = *reinterpret_cast<const u32x4*>(p + w);
-          buf[fn][w] = v[0]; buf[fn][w + 1] = v[1]; buf[fn][w + 2] = v[2]; buf[fn][w + 3] = v[3];
-        }
-      } else if constexpr (HW % 2 == 0) {
-#pragma unroll
-        for (int w = 0; w < HW; w += 2) {
-          const u32x2 v = *reinterpret_cast<const u32x2*>(p + w);
-          buf[fn][w] = v[0]; buf[fn][w + 1] = v[1];
-        }
-      } else {
-#pragma unroll
-        for (int w = 0; w < HW; ++w) buf[fn][w] = p[w];
-      }
-    }
-  };
-
-  // ---- X chunk loads: thread -> (row, 16-byte column)
-  // rows >= M read row M - 1: they are computed but never stored
-  const half_t* xrow[XPASS];
-#pragma unroll
-  for (int ps = 0; ps < XPASS; ++ps) {
-    const int64_t m = m0 + ps * 32 + tid / 8;
-    xrow[ps] = a.x + (m < a.M ? m : a.M - 1) * a.K + (tid % 8) * 8;
+  for (int j = 0; j < II; ++j) {
+    const int gl = (wave * II + j) * kWave + lane;     // word slot in the id tile
+    const int64_t n = n0 + gl / IW;
+    isrc[j] = a.idx + (n < a.N ? n : 0) * a.R + (gl % IW) * 4;
   }
-  u32x4 xreg[XPASS];
-  auto load_x = [&](int64_t c) {
+  auto issue = [&](int c, int stage) {
+    uint8_t* sb = ring + stage * SBYTES;
 #pragma unroll
-    for (int ps = 0; ps < XPASS; ++ps)
-      xreg[ps] = *reinterpret_cast<const u32x4*>(xrow[ps] + c * kGemmKC);
-  };
-  auto store_x = [&](int buf) {
-    uint8_t* base = xs + buf * (BM * kXRowBytes);
+    for (int j = 0; j < XI; ++j)
+      copy16_to_lds(xsrc[j] + (int64_t)c * kGemmKC, sb + (wave * (BM / 4) + j * 8) * 128);
 #pragma unroll
-    for (int ps = 0; ps < XPASS; ++ps) {
-      const int r = ps * 32 + tid / 8;
-      *reinterpret_cast<u32x4*>(base + r * kXRowBytes + (tid % 8) * 16) = xreg[ps];
-    }
+    for (int j = 0; j < II; ++j)
+      copy4_to_lds(isrc[j] + (int64_t)c * (2 * HB), sb + XBYTES + (wave * II + j) * kWave * 4);
   };
 
-  // The codebook (L2-resident) is staged before the first index / X loads:
-  // the vector L1 returns loads in order, so it would otherwise wait for them.
+  // The codebook (L2-resident) is staged first.
   CbStage cst;
   cb_fetch<D, MODE>(a.cb, a.C, cst);
   cb_store<D, MODE>(smem, a.cb, a.C, cst);
-  uint32_t idsA[FN][HW], idsB[FN][HW];
-  load_ids(idsA, 0);
-  load_x(0);
-  store_x(0);
   __syncthreads();
+
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s) issue(s < nchunks ? s : nchunks - 1, s);
 
   float16_t acc[FM][FN];
 #pragma unroll
@@ -136,8 +139,23 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(GemmArgs a) {
 
   const uint32_t lane_off = repl_lane_off<D>(lane);
 
-  auto compute_chunk = [&](const uint32_t (&ids)[FN][HW], int buf) {
-    const uint8_t* xb = xs + buf * (BM * kXRowBytes);
+  for (int c = 0; c < nchunks; ++c) {
+    const int stage = c % NS;
+    wait_vmcnt<LPC * (NS - 2)>();  // this wave's copies of chunk c are in LDS
+    __builtin_amdgcn_s_barrier();  // everyone's are; stage (c - 1) % NS is free
+    {
+      const int cn = c + NS - 1 < nchunks ? c + NS - 1 : nchunks - 1;
+      issue(cn, (c + NS - 1) % NS);
+    }
+    const uint8_t* xb = ring + stage * SBYTES;
+    const uint8_t* ib = xb + XBYTES;
+    uint32_t ids[FN][HB / 4];
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) {
+      const uint8_t* p = ib + (wn * WN + fn * 32 + l32) * (2 * HB) + h * HB;
+#pragma unroll
+      for (int w = 0; w < HB / 4; ++w) ids[fn][w] = reinterpret_cast<const uint32_t*>(p)[w];
+    }
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       half8_t bop[FN];
@@ -146,36 +164,15 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(GemmArgs a) {
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm) {
         const int r = wm * WM + fm * 32 + l32;
-        const half8_t aop = *reinterpret_cast<const half8_t*>(xb + r * kXRowBytes + (h * 32 + t * 8) * 2);
+        const int slot = (h * 4 + t) ^ ((r >> 1) & 7);
+        const half8_t aop = *reinterpret_cast<const half8_t*>(xb + r * 128 + slot * 16);
 #pragma unroll
         for (int fn = 0; fn < FN; ++fn)
           acc[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x16_f16(aop, bop[fn], acc[fm][fn], 0, 0, 0);
       }
     }
-  };
-
-  // Chunk c lives in one register set / LDS buffer while chunk c + 1 is
-  // loaded into the other.  The next-chunk loads are unconditional (the last
-  // chunk is re-read) so that the number of loads in flight is static.
-  int64_t c = 0;
-  int buf = 0;
-  while (c < nchunks) {
-    int64_t cn = (c + 1) < nchunks ? c + 1 : c;
-    load_ids(idsB, cn);
-    load_x(cn);
-    compute_chunk(idsA, buf);
-    store_x(buf ^ 1);
-    __syncthreads();
-    ++c; buf ^= 1;
-    if (c >= nchunks) break;
-    cn = (c + 1) < nchunks ? c + 1 : c;
-    load_ids(idsA, cn);
-    load_x(cn);
-    compute_chunk(idsB, buf);
-    store_x(buf ^ 1);
-    __syncthreads();
-    ++c; buf ^= 1;
   }
+  wait_vmcnt<0>();  // drain the clamped copies issued past the last chunk
 
   // ---- epilogue: lane l holds rows (i/4)*8 + h*4 + i%4, column l32 of each 32x32 tile
 #pragma unroll
