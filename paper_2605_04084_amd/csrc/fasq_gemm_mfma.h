@@ -1,9 +1,9 @@
 // Prefill GEMM: Y[M x N] = X[M x K] . W_hat^T with W_hat decoded tile by tile.
 //
 // Design (gfx950, wave64, v_mfma_f32_32x32x16_f16):
-//   * A workgroup of 4 waves owns a BM x BN output tile; the waves form a
-//     2 x 2 grid, each wave owning (BM/2) x (BN/2) = FM x FN MFMA tiles of
-//     32 x 32 with fp32 accumulators in registers.
+//   * A workgroup of WGM x WGN waves owns a BM x BN output tile, each wave
+//     owning (BM/WGM) x (BN/WGN) = FM x FN MFMA tiles of 32 x 32 with fp32
+//     accumulators in registers.
 //   * K is walked in chunks of 64.  Each chunk's X tile (BM x 64 fp16) and
 //     packed-id tile (BN columns) are copied from global memory straight
 //     into LDS (global_load_lds), NS chunks ahead, into a ring of NS LDS
@@ -65,21 +65,24 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-template <int BITS, int D, int MODE, int BM, int BN>
-__global__ __launch_bounds__(256) void k_gemm_mfma(GemmArgs a) {
+template <int BITS, int D, int MODE, int BM, int BN, int WGM, int WGN>
+__global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_mfma(GemmArgs a) {
   constexpr int NS = kGemmStages;
-  constexpr int WM = BM / 2, WN = BN / 2;
+  constexpr int WAVES = WGM * WGN;
+  constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int FM = WM / 32, FN = WN / 32;
   constexpr int HB = gemm_run_bytes<BITS, D>();    // bytes per lane half per chunk
   constexpr int IPS = 8 / D;                       // ids per k-step per lane
-  constexpr int XI = BM / 32;                      // X copy instructions per wave per chunk (8 rows each)
+  constexpr int XR = BM / WAVES;                   // X tile rows copied by each wave
+  constexpr int XI = XR / 8;                       // X copy instructions per wave per chunk (8 rows each)
   constexpr int IW = 2 * HB / 4;                   // id words per column per chunk
-  constexpr int II = BN * IW / 256;                // id copy instructions per wave per chunk
+  constexpr int II = BN * IW / (WAVES * kWave);    // id copy instructions per wave per chunk
   constexpr int LPC = XI + II;                     // vector-memory instructions per wave per chunk
   constexpr int XBYTES = BM * 128;
   constexpr int SBYTES = gemm_stage_bytes<BITS, D, BM, BN>();
+  static_assert(WM % 32 == 0 && WN % 32 == 0 && XR % 8 == 0, "tile does not split over the waves");
   static_assert(HB % 4 == 0, "index run must be whole dwords");
-  static_assert((BN * IW) % 256 == 0, "id tile must split evenly over the workgroup");
+  static_assert((BN * IW) % (WAVES * kWave) == 0, "id tile must split evenly over the workgroup");
   static_assert(LPC * (NS - 2) < 64, "too many loads in flight for vmcnt");
 
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
@@ -87,7 +90,7 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(GemmArgs a) {
 
   const int tid = threadIdx.x;
   const int wave = tid / kWave, lane = tid % kWave;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WGN, wn = wave % WGN;
   const int h = lane >> 5, l32 = lane & 31;
   const int64_t m0 = (int64_t)blockIdx.y * BM;
   const int64_t n0 = (int64_t)blockIdx.x * BN;
@@ -98,7 +101,7 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(GemmArgs a) {
   const half_t* xsrc[XI];
 #pragma unroll
   for (int j = 0; j < XI; ++j) {
-    const int r = wave * (BM / 4) + j * 8 + lane / 8;  // tile row
+    const int r = wave * XR + j * 8 + lane / 8;        // tile row
     const int g = (lane % 8) ^ ((r >> 1) & 7);         // granule stored in slot lane % 8
     const int64_t m = m0 + r;
     xsrc[j] = a.x + (m < a.M ? m : a.M - 1) * a.K + g * 8;
@@ -114,7 +117,7 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(GemmArgs a) {
     uint8_t* sb = ring + stage * SBYTES;
 #pragma unroll
     for (int j = 0; j < XI; ++j)
-      copy16_to_lds(xsrc[j] + (int64_t)c * kGemmKC, sb + (wave * (BM / 4) + j * 8) * 128);
+      copy16_to_lds(xsrc[j] + (int64_t)c * kGemmKC, sb + (wave * XR + j * 8) * 128);
 #pragma unroll
     for (int j = 0; j < II; ++j)
       copy4_to_lds(isrc[j] + (int64_t)c * (2 * HB), sb + XBYTES + (wave * II + j) * kWave * 4);

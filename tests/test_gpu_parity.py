@@ -145,6 +145,26 @@ def test_gemm_prefill(M, mat):
                  f"prefill M={M} {w.matrices[mat].name}")
 
 
+WIDE_TILE = [
+    # M, K, N, d, C, bits: enough output tiles for the 128 x 256 GEMM tile, ragged M and N
+    (1030, 256, 16400, 2, 256, 8),
+    (1030, 384, 16400, 4, 4096, 12),
+    (1100, 256, 16500, 4, 65536, 16),
+    (1025, 128, 16390, 8, 256, 8),
+]
+
+
+@pytest.mark.parametrize("case", WIDE_TILE)
+def test_gemm_wide_tiles(case):
+    M, K, N, d, C, bits = case
+    print(f"[case] gemm wide tile {case}", flush=True)
+    rng = np.random.default_rng(sum(case))
+    p = pi.draw_problem(rng, M, K, N, d, C, bits)
+    y = run("gemm", p)
+    rows = np.unique(np.concatenate([sample_rows(N, 96), np.arange(N - 40, N)]))
+    assert_close(y[:, rows], orc.pq_linear(p.x, p.idx, bits, d, p.codebook, rows=rows), f"wide {case}")
+
+
 # ---------------------------------------------------------------------------
 # Ragged and small shapes, every id width and sub-vector length
 # ---------------------------------------------------------------------------
