@@ -68,7 +68,8 @@ hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t
   auto lds_of = [&](int bn) { return cb_bytes + kGemmStages * (128 * 128 + bn * 2 * hb); };
   const int64_t mt = (p.M + 127) / 128;
   int tile = kTile128x128;
-  if (mt * ((p.N + 255) / 256) >= 2 * (int64_t)dev.num_cus && lds_of(256) <= dev.lds_per_block) tile = kTile128x256;
+  if (4 * mt * ((p.N + 255) / 256) >= 3 * (int64_t)dev.num_cus && lds_of(256) <= dev.lds_per_block)
+    tile = kTile128x256;
   const int lds = lds_of(tile == kTile128x256 ? 256 : 128);
   if (lds > dev.lds_per_block) return hipErrorNotSupported;
 
