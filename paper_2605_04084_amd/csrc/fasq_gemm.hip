@@ -17,14 +17,35 @@ hipError_t launch_gemm_variant(const GemmArgs& a, int lds, hipStream_t stream) {
   return hipGetLastError();
 }
 
-// Tile shapes: 128 x 128 on 2 x 2 waves, or 128 x 256 on 2 x 4 waves (half the
-// X re-reads per output, two waves per SIMD) when there are tiles enough.
-enum GemmTile { kTile128x128 = 0, kTile128x256 = 1 };
+// Tile shapes, largest first: 128 x 256 on 2 x 4 waves (half the X re-reads
+// per output, two waves per SIMD), 128 x 128, 64 x 128 and 64 x 64 on 2 x 2
+// waves.  The launcher takes the largest tile whose grid covers at least 3/4
+// of the CUs, else the smallest.
+struct GemmTileShape {
+  int bm, bn;
+};
+constexpr GemmTileShape kGemmTiles[] = {{128, 256}, {128, 128}, {64, 128}, {64, 64}};
+constexpr int kGemmNumTiles = 4;
+
+// Whether tile t splits the id copies evenly over its waves.
+inline bool gemm_tile_ok(int t, int hb) {
+  const int waves = kGemmTiles[t].bn == 256 ? 8 : 4;
+  return (kGemmTiles[t].bn * (2 * hb / 4)) % (waves * kWave) == 0;
+}
 
 template <int BITS, int D, int MODE>
 hipError_t launch_gemm_tile(const GemmArgs& a, int tile, int lds, hipStream_t stream) {
-  if (tile == kTile128x256) return launch_gemm_variant<BITS, D, MODE, 128, 256, 2, 4>(a, lds, stream);
-  return launch_gemm_variant<BITS, D, MODE, 128, 128, 2, 2>(a, lds, stream);
+  constexpr int IW = 2 * gemm_run_bytes<BITS, D>() / 4;
+  switch (tile) {
+    case 0: return launch_gemm_variant<BITS, D, MODE, 128, 256, 2, 4>(a, lds, stream);
+    case 2:
+      if constexpr ((128 * IW) % 256 == 0) return launch_gemm_variant<BITS, D, MODE, 64, 128, 2, 2>(a, lds, stream);
+      else return hipErrorNotSupported;
+    case 3:
+      if constexpr ((64 * IW) % 256 == 0) return launch_gemm_variant<BITS, D, MODE, 64, 64, 2, 2>(a, lds, stream);
+      else return hipErrorNotSupported;
+    default: return launch_gemm_variant<BITS, D, MODE, 128, 128, 2, 2>(a, lds, stream);
+  }
 }
 
 template <int BITS, int D>
@@ -65,13 +86,18 @@ hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t
 
   const int mode = choose_cb_mode(p.C, d);
   const int cb_bytes = (int)cb_lds_bytes(mode, p.C, d);
-  auto lds_of = [&](int bn) { return cb_bytes + kGemmStages * (128 * 128 + bn * 2 * hb); };
-  const int64_t mt = (p.M + 127) / 128;
-  int tile = kTile128x128;
-  if (4 * mt * ((p.N + 255) / 256) >= 3 * (int64_t)dev.num_cus && lds_of(256) <= dev.lds_per_block)
-    tile = kTile128x256;
-  const int lds = lds_of(tile == kTile128x256 ? 256 : 128);
-  if (lds > dev.lds_per_block) return hipErrorNotSupported;
+  auto lds_of = [&](int t) { return cb_bytes + kGemmStages * (kGemmTiles[t].bm * 128 + kGemmTiles[t].bn * 2 * hb); };
+  auto tiles_of = [&](int t) {
+    return ((p.M + kGemmTiles[t].bm - 1) / kGemmTiles[t].bm) * ((p.N + kGemmTiles[t].bn - 1) / kGemmTiles[t].bn);
+  };
+  int tile = -1;
+  for (int t = 0; t < kGemmNumTiles && tile < 0; ++t)
+    if (gemm_tile_ok(t, hb) && lds_of(t) <= dev.lds_per_block && 4 * tiles_of(t) >= 3 * (int64_t)dev.num_cus)
+      tile = t;
+  for (int t = kGemmNumTiles - 1; t >= 0 && tile < 0; --t)
+    if (gemm_tile_ok(t, hb) && lds_of(t) <= dev.lds_per_block) tile = t;
+  if (tile < 0) return hipErrorNotSupported;
+  const int lds = lds_of(tile);
 
   GemmArgs a;
   a.x = static_cast<const half_t*>(p.x);
