@@ -53,7 +53,11 @@ constexpr int kGemvPipe = 8;      // load units per wave in the software pipelin
 // waves wait at the issue of loads that cannot enter the queue, where they
 // cannot compute the data that has arrived.
 constexpr int kM1Window = 2;
-static_assert(kM1Window <= kGemvPipe, "the window must fit the load slots");
+// Index loads a wave issues before the staging barrier (at least the window):
+// the first ones keep the CU's memory queue busy while the codebook and x
+// are staged.
+constexpr int kM1EarlyLoads = 2;
+static_assert(kM1Window <= kM1EarlyLoads && kM1EarlyLoads <= kGemvPipe, "early loads must cover the window");
 constexpr int kXWordsPerThread = 8;  // first-round x words (16 B) per thread for M > 1
 
 // MASK: some lanes of the last wave of a row see chunk columns past the end
@@ -340,13 +344,13 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
     }
   }
   // Every wave's codebook and x requests enter the CU's (in-order) memory
-  // queue before any index load, and only the first kM1Window index loads of
-  // a wave go out before the staging barrier: the barrier then waits for the
-  // small staging data alone, not for the whole workgroup to get its loads
-  // accepted by a saturated memory queue.
+  // queue before any index load, and only the first kM1EarlyLoads index loads
+  // of a wave go out before the staging barrier: the barrier then waits for
+  // the small staging data alone, not for the whole workgroup to get its
+  // loads accepted by a saturated memory queue.
   __syncthreads();
 #pragma unroll
-  for (int i = 0; i < kM1Window; ++i) load_unit(i, row0 + (uint32_t)(i / T) * rstride, i % T);
+  for (int i = 0; i < kM1EarlyLoads; ++i) load_unit(i, row0 + (uint32_t)(i / T) * rstride, i % T);
 
   cb_store<D, MODE>(smem, cb, C, cst);
 #pragma unroll
@@ -414,12 +418,19 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
   // Unit k lives in slot k % L, and kM1Window loads stay in flight.  A wave
   // computes a unit before it issues the next load, so data that has arrived
   // is never held up behind a load waiting for room in the memory queue.
-  uint32_t rbase = row0;  // offset of local row base / T
-  for (int base = 0; base < nunits; base += L, rbase += (uint32_t)(L / T) * rstride) {
+  // First window: units below kM1EarlyLoads are already in flight.
+  constexpr int W = kM1Window;
+#pragma unroll
+  for (int i = 0; i < L; ++i) {
+    if (i < nunits) compute_unit(i, i, i % T);
+    if (i + W >= kM1EarlyLoads) load_unit((i + W) % L, row0 + (uint32_t)((i + W) / T) * rstride, (i + W) % T);
+  }
+  uint32_t rbase = row0 + (uint32_t)(L / T) * rstride;  // offset of local row base / T
+  for (int base = L; base < nunits; base += L, rbase += (uint32_t)(L / T) * rstride) {
 #pragma unroll
     for (int i = 0; i < L; ++i) {
       if (base + i < nunits) compute_unit(i, base + i, i % T);
-      load_unit((i + kM1Window) % L, rbase + (uint32_t)((i + kM1Window) / T) * rstride, (i + kM1Window) % T);
+      load_unit((i + W) % L, rbase + (uint32_t)((i + W) / T) * rstride, (i + W) % T);
     }
   }
   __syncthreads();
