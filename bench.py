@@ -393,6 +393,27 @@ def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None, gro
     return res
 
 
+def dense_gemm_seconds(torch, x, w, reps, short, long):
+    """Per-call time of torch.matmul(x, w) (fp16, rocBLAS/hipBLASLt), timed
+    like the PQ GEMM: differential over back-to-back calls."""
+    y = torch.empty((x.shape[0], w.shape[1]), dtype=torch.float16, device=x.device)
+    stream = torch.cuda.current_stream()
+    torch.matmul(x, w, out=y)
+
+    def batch(count):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(SPACER_CYCLES)
+        e0.record(stream)
+        for _ in range(count):
+            torch.matmul(x, w, out=y)
+        e1.record(stream)
+        e1.synchronize()
+        return e0.elapsed_time(e1) * 1e-3
+
+    times = [(batch(long) - batch(short)) / (long - short) for _ in range(reps)]
+    return max(float(np.median(times)), 1e-7)
+
+
 def prefill(torch, fasq, pi, Ms, reps, short=1, long=4):
     """Prefill GEMM per-launch time, from back-to-back launches (the same
     operands each time: at these sizes the GEMM is bound by the matrix cores,
@@ -406,6 +427,8 @@ def prefill(torch, fasq, pi, Ms, reps, short=1, long=4):
         x_all = torch.from_numpy(base.x).to(dev)
         idx = torch.from_numpy(base.idx).to(dev)
         cb = torch.from_numpy(base.codebook).to(dev)
+        gen = torch.Generator(device=dev).manual_seed(i)
+        w_dense = (torch.randn((spec.K, spec.N), generator=gen, device=dev) * 0.02).to(torch.float16)
         for M in Ms:
             x = x_all[:M].contiguous()
             y = torch.empty((M, spec.N), dtype=torch.float16, device=dev)
@@ -428,11 +451,16 @@ def prefill(torch, fasq, pi, Ms, reps, short=1, long=4):
                 times.append((batch(long) - batch(short)) / (long - short))
             t = max(float(np.median(times)), 1e-7)
             fl = 2.0 * M * spec.N * spec.K
+            # Context, not the product: the vendor library's dense fp16 GEMM on
+            # the same shape, with the weights stored uncompressed (K x N).
+            td = dense_gemm_seconds(torch, x, w_dense, reps, short, long)
             out.append(dict(name=spec.name, M=M, N=spec.N, K=spec.K, us=t * 1e6, tflops=fl / t / 1e12,
                             pct_mfma=100.0 * fl / t / 1e12 / FP16_MFMA_PEAK_TFLOPS,
+                            dense_fp16_tflops=fl / td / 1e12, vs_dense_fp16=td / t,
                             kernel=fasq.plan("gemm", M, spec.K, spec.N, base.idx_bits, base.d, base.C)))
-            log(f"[bench] prefill {spec.name} M={M}: {t * 1e6:.1f} us, {fl / t / 1e12:.1f} TFLOP/s")
-        del x_all, idx, cb
+            log(f"[bench] prefill {spec.name} M={M}: {t * 1e6:.1f} us, {fl / t / 1e12:.1f} TFLOP/s "
+                f"(dense fp16 library GEMM: {fl / td / 1e12:.1f})")
+        del x_all, idx, cb, w_dense
     torch.cuda.empty_cache()
     return out
 

@@ -6,10 +6,11 @@ namespace fasq {
 
 namespace {
 
-template <int BITS, int D, int MODE, int BM, int BN, int WGM, int WGN>
+template <int BITS, int D, int MODE, int BM, int BN, int WGM, int WGN, int WANT>
 hipError_t launch_gemm_variant(const GemmArgs& a, int lds, hipStream_t stream) {
-  auto kern = k_gemm_mfma<BITS, D, MODE, BM, BN, WGM, WGN>;
-  if (plan_record("k_gemm_mfma", {BITS, D, MODE, BM, BN, WGM, WGN})) return hipSuccess;
+  constexpr int NS = gemm_ring_depth(BITS, D, BM, BN, WGM * WGN, WANT);
+  auto kern = k_gemm_mfma<BITS, D, MODE, BM, BN, WGM, WGN, NS>;
+  if (plan_record("k_gemm_mfma", {BITS, D, MODE, BM, BN, WGM, WGN, NS})) return hipSuccess;
   hipError_t e = prepare_kernel(kern);
   if (e != hipSuccess) return e;
   dim3 grid((unsigned)((a.N + BN - 1) / BN), (unsigned)((a.M + BM - 1) / BM));
@@ -19,32 +20,35 @@ hipError_t launch_gemm_variant(const GemmArgs& a, int lds, hipStream_t stream) {
 
 // Tile shapes, largest first: 128 x 256 on 2 x 4 waves (half the X re-reads
 // per output, two waves per SIMD), 128 x 128, 64 x 128 and 64 x 64 on 2 x 2
-// waves.  The launcher takes the largest tile whose grid covers at least 3/4
-// of the CUs, else the smallest.
+// waves, with the LDS ring depth of each.  The launcher takes the largest
+// tile whose grid covers at least 3/4 of the CUs, else the smallest.
 struct GemmTileShape {
-  int bm, bn;
+  int bm, bn, ns;
 };
-constexpr GemmTileShape kGemmTiles[] = {{128, 256}, {128, 128}, {64, 128}, {64, 64}};
+constexpr GemmTileShape kGemmTiles[] = {{128, 256, 4}, {128, 128, 4}, {64, 128, 8}, {64, 64, 8}};
 constexpr int kGemmNumTiles = 4;
+
+inline int gemm_tile_waves(int t) { return kGemmTiles[t].bn == 256 ? 8 : 4; }
 
 // Whether tile t splits the id copies evenly over its waves.
 inline bool gemm_tile_ok(int t, int hb) {
-  const int waves = kGemmTiles[t].bn == 256 ? 8 : 4;
-  return (kGemmTiles[t].bn * (2 * hb / 4)) % (waves * kWave) == 0;
+  return (kGemmTiles[t].bn * (2 * hb / 4)) % (gemm_tile_waves(t) * kWave) == 0;
 }
 
 template <int BITS, int D, int MODE>
 hipError_t launch_gemm_tile(const GemmArgs& a, int tile, int lds, hipStream_t stream) {
   constexpr int IW = 2 * gemm_run_bytes<BITS, D>() / 4;
   switch (tile) {
-    case 0: return launch_gemm_variant<BITS, D, MODE, 128, 256, 2, 4>(a, lds, stream);
+    case 0: return launch_gemm_variant<BITS, D, MODE, 128, 256, 2, 4, kGemmTiles[0].ns>(a, lds, stream);
     case 2:
-      if constexpr ((128 * IW) % 256 == 0) return launch_gemm_variant<BITS, D, MODE, 64, 128, 2, 2>(a, lds, stream);
+      if constexpr ((128 * IW) % 256 == 0)
+        return launch_gemm_variant<BITS, D, MODE, 64, 128, 2, 2, kGemmTiles[2].ns>(a, lds, stream);
       else return hipErrorNotSupported;
     case 3:
-      if constexpr ((64 * IW) % 256 == 0) return launch_gemm_variant<BITS, D, MODE, 64, 64, 2, 2>(a, lds, stream);
+      if constexpr ((64 * IW) % 256 == 0)
+        return launch_gemm_variant<BITS, D, MODE, 64, 64, 2, 2, kGemmTiles[3].ns>(a, lds, stream);
       else return hipErrorNotSupported;
-    default: return launch_gemm_variant<BITS, D, MODE, 128, 128, 2, 2>(a, lds, stream);
+    default: return launch_gemm_variant<BITS, D, MODE, 128, 128, 2, 2, kGemmTiles[1].ns>(a, lds, stream);
   }
 }
 
@@ -86,7 +90,11 @@ hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t
 
   const int mode = choose_cb_mode(p.C, d);
   const int cb_bytes = (int)cb_lds_bytes(mode, p.C, d);
-  auto lds_of = [&](int t) { return cb_bytes + kGemmStages * (kGemmTiles[t].bm * 128 + kGemmTiles[t].bn * 2 * hb); };
+  auto lds_of = [&](int t) {
+    const GemmTileShape& ts = kGemmTiles[t];
+    const int ns = gemm_ring_depth(p.idx_bits, d, ts.bm, ts.bn, gemm_tile_waves(t), ts.ns);
+    return cb_bytes + ns * (ts.bm * 128 + ts.bn * 2 * hb);
+  };
   auto tiles_of = [&](int t) {
     return ((p.M + kGemmTiles[t].bm - 1) / kGemmTiles[t].bm) * ((p.N + kGemmTiles[t].bn - 1) / kGemmTiles[t].bn);
   };

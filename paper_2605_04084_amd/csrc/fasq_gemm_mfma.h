@@ -6,20 +6,25 @@
 //     accumulators in registers.
 //   * K is walked in chunks of 64.  Each chunk's X tile (BM x 64 fp16) and
 //     packed-id tile (BN columns) are copied from global memory straight
-//     into LDS (global_load_lds), NS chunks ahead, into a ring of NS LDS
+//     into LDS (global_load_lds), NS - 1 chunks ahead, into a ring of NS LDS
 //     stages: the copies need no registers, so the loads of several chunks
-//     are in flight while one is computed.  X rows are 128 B with their
-//     16-byte granules XOR-swizzled by (row / 2) mod 8, so the MFMA operand
-//     reads of one LDS cycle hit distinct banks.
+//     are in flight while one is computed.  Small tiles take a deeper ring:
+//     a workgroup that computes a chunk in a few hundred cycles waits on
+//     memory latency unless many chunks are in flight.  X rows are 128 B
+//     with their 16-byte granules XOR-swizzled by (row / 2) mod 8, so the
+//     MFMA operand reads of one LDS cycle hit distinct banks.
 //   * W_hat is never written to memory, not even to LDS: each lane decodes
 //     the ids of its own B-operand column from the staged id tile and
 //     gathers the codewords from the LDS codebook into the MFMA B registers.
 //     The order of K inside a chunk is permuted identically for A and B
 //     (allowed: the contraction is a sum over K), so that lane half h reads
 //     one contiguous run of 32/d ids per chunk.
-//   * Synchronisation per chunk: an explicit wait for this wave's copies of
-//     the chunk, then one workgroup barrier (every wave's copies are in, and
-//     every wave is done with the stage about to be refilled).
+//   * Software pipeline: each wave reads the A and B operands of k-step
+//     t + 2 from LDS while the matrix cores work on step t.
+//   * Synchronisation: one workgroup barrier per chunk, in the middle of it
+//     (after an explicit wait for this wave's copies of the next chunk):
+//     every wave's copies of the next chunk are in, and every wave is done
+//     with the stage about to be refilled.
 //   * Epilogue: fp32 -> fp16 once, direct stores.
 #pragma once
 
@@ -30,7 +35,6 @@
 namespace fasq {
 
 constexpr int kGemmKC = 64;          // K per chunk
-constexpr int kGemmStages = 4;       // LDS ring depth (chunks in flight + 1)
 
 struct GemmArgs {
   const half_t* x;
@@ -49,6 +53,15 @@ __host__ __device__ constexpr int gemm_run_bytes() { return (32 / D) * BITS / 8;
 template <int BITS, int D, int BM, int BN>
 __host__ __device__ constexpr int gemm_stage_bytes() { return BM * 128 + BN * 2 * gemm_run_bytes<BITS, D>(); }
 
+// Ring depth of a tile: the wanted depth, reduced until the copies a wave
+// keeps in flight, (depth - 2) chunks of them, fit the 6-bit vmcnt counter.
+__host__ __device__ constexpr int gemm_ring_depth(int bits, int d, int bm, int bn, int waves, int want) {
+  const int loads = bm / waves / 8 + bn * ((32 / d) * bits / 8 * 2 / 4) / (waves * 64);
+  int ns = want;
+  while (ns > 3 && loads * (ns - 2) >= 64) --ns;
+  return ns;
+}
+
 // Copy 16 (or 4) bytes per lane from global memory into LDS: lane i's data
 // lands at lds + 16 i (4 i).
 __device__ __forceinline__ void copy16_to_lds(const void* src, uint8_t* lds) {
@@ -65,9 +78,8 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-template <int BITS, int D, int MODE, int BM, int BN, int WGM, int WGN>
+template <int BITS, int D, int MODE, int BM, int BN, int WGM, int WGN, int NS>
 __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_mfma(GemmArgs a) {
-  constexpr int NS = kGemmStages;
   constexpr int WAVES = WGM * WGN;
   constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int FM = WM / 32, FN = WN / 32;
@@ -83,7 +95,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_mfma(GemmArgs a) {
   static_assert(WM % 32 == 0 && WN % 32 == 0 && XR % 8 == 0, "tile does not split over the waves");
   static_assert(HB % 4 == 0, "index run must be whole dwords");
   static_assert((BN * IW) % (WAVES * kWave) == 0, "id tile must split evenly over the workgroup");
-  static_assert(LPC * (NS - 2) < 64, "too many loads in flight for vmcnt");
+  static_assert(NS >= 3 && LPC * (NS - 2) < 64, "ring depth out of range for vmcnt");
 
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   uint8_t* ring = smem + a.cb_lds_bytes;  // NS stages of [X tile][id tile]
@@ -142,38 +154,71 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_mfma(GemmArgs a) {
 
   const uint32_t lane_off = repl_lane_off<D>(lane);
 
-  for (int c = 0; c < nchunks; ++c) {
-    const int stage = c % NS;
-    wait_vmcnt<LPC * (NS - 2)>();  // this wave's copies of chunk c are in LDS
-    __builtin_amdgcn_s_barrier();  // everyone's are; stage (c - 1) % NS is free
-    {
-      const int cn = c + NS - 1 < nchunks ? c + NS - 1 : nchunks - 1;
-      issue(cn, (c + NS - 1) % NS);
-    }
-    const uint8_t* xb = ring + stage * SBYTES;
-    const uint8_t* ib = xb + XBYTES;
-    uint32_t ids[FN][HB / 4];
+  // Operands of one k-step: FM A fragments from the X tile, FN B fragments
+  // gathered from the codebook.
+  struct Ops {
+    half8_t a[FM];
+    half8_t b[FN];
+  };
+  auto read_ids = [&](int stage, uint32_t (&ids)[FN][HB / 4]) {
+    const uint8_t* ib = ring + stage * SBYTES + XBYTES;
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn) {
       const uint8_t* p = ib + (wn * WN + fn * 32 + l32) * (2 * HB) + h * HB;
 #pragma unroll
       for (int w = 0; w < HB / 4; ++w) ids[fn][w] = reinterpret_cast<const uint32_t*>(p)[w];
     }
+  };
+  auto read_ops = [&](Ops& o, int stage, const uint32_t (&ids)[FN][HB / 4], int t) {
+    const uint8_t* xb = ring + stage * SBYTES;
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      half8_t bop[FN];
+    for (int fn = 0; fn < FN; ++fn) o.b[fn] = gather8<BITS, D, MODE>(a.cb, lane_off, ids[fn], t * IPS);
 #pragma unroll
-      for (int fn = 0; fn < FN; ++fn) bop[fn] = gather8<BITS, D, MODE>(a.cb, lane_off, ids[fn], t * IPS);
-#pragma unroll
-      for (int fm = 0; fm < FM; ++fm) {
-        const int r = wm * WM + fm * 32 + l32;
-        const int slot = (h * 4 + t) ^ ((r >> 1) & 7);
-        const half8_t aop = *reinterpret_cast<const half8_t*>(xb + r * 128 + slot * 16);
-#pragma unroll
-        for (int fn = 0; fn < FN; ++fn)
-          acc[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x16_f16(aop, bop[fn], acc[fm][fn], 0, 0, 0);
-      }
+    for (int fm = 0; fm < FM; ++fm) {
+      const int r = wm * WM + fm * 32 + l32;
+      const int slot = (h * 4 + t) ^ ((r >> 1) & 7);
+      o.a[fm] = *reinterpret_cast<const half8_t*>(xb + r * 128 + slot * 16);
     }
+  };
+  auto mfma_step = [&](const Ops& o) {
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn)
+        acc[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x16_f16(o.a[fm], o.b[fn], acc[fm][fn], 0, 0, 0);
+  };
+
+  // Software pipeline: the operands of k-step t + 2 are read while the
+  // matrix cores work on step t, across chunk boundaries too (step t's
+  // operands live in o[t % 4]).  The workgroup barrier sits in the middle
+  // of a chunk: at chunk c's third step every wave has finished chunk c - 1
+  // (its stage can be refilled) and, after waiting for its own copies,
+  // chunk c + 1 is in LDS (its ids and first operands can be read).
+  wait_vmcnt<LPC * (NS - 2)>();  // this wave's copies of chunk 0
+  __builtin_amdgcn_s_barrier();  // everyone's
+  uint32_t idc[FN][HB / 4];
+  read_ids(0, idc);
+  Ops o0, o1, o2, o3;
+  read_ops(o0, 0, idc, 0);
+  read_ops(o1, 0, idc, 1);
+  for (int c = 0; c < nchunks; ++c) {
+    const int stage = c % NS;
+    const bool more = c + 1 < nchunks;
+    read_ops(o2, stage, idc, 2);
+    mfma_step(o0);
+    read_ops(o3, stage, idc, 3);
+    mfma_step(o1);
+    if (more) {
+      wait_vmcnt<LPC * (NS - 3)>();  // this wave's copies of chunk c + 1
+      __builtin_amdgcn_s_barrier();  // everyone's; nobody reads chunk c - 1 any more
+      const int cn = c + NS - 1 < nchunks ? c + NS - 1 : nchunks - 1;
+      issue(cn, (c + NS - 1) % NS);
+      read_ids((c + 1) % NS, idc);
+      read_ops(o0, (c + 1) % NS, idc, 0);
+    }
+    mfma_step(o2);
+    if (more) read_ops(o1, (c + 1) % NS, idc, 1);
+    mfma_step(o3);
   }
   wait_vmcnt<0>();  // drain the clamped copies issued past the last chunk
 
