@@ -11,7 +11,10 @@ namespace fasq {
 //   CB_LDS   : LDS, one copy (larger codebooks; gathers may collide).
 //   CB_GLOBAL: global memory (L2 / Infinity Cache resident), for codebooks
 //              larger than the LDS budget.
-enum CbMode { CB_REPL = 0, CB_LDS = 1, CB_GLOBAL = 2 };
+//   CB_SLICE : LDS, one slice of 2^k entries at a time (codebooks larger than
+//              LDS): the kernel makes one pass over its rows per slice, and
+//              an id contributes only in the pass of its own slice.
+enum CbMode { CB_REPL = 0, CB_LDS = 1, CB_GLOBAL = 2, CB_SLICE = 3 };
 
 // One lane's unit of the packed index stream.
 template <int BITS>
@@ -71,6 +74,7 @@ struct Repl {
 };
 
 // LDS bytes a codebook of C entries takes in a given placement.
+// (CB_SLICE: the slice size is chosen by the launcher, not given by C.)
 __host__ __device__ constexpr int64_t cb_lds_bytes(int mode, int64_t C, int d) {
   return mode == CB_REPL ? C * 256 : mode == CB_LDS ? C * d * 2 : 0;
 }
@@ -179,6 +183,41 @@ __device__ __forceinline__ void cb_store(uint8_t* __restrict__ lds, const half_t
   }
 }
 
+// CB_SLICE staging: the `words` 16-byte words of one slice (source `src`)
+// go to LDS from address 0.  The first batch of loads is issued by
+// slice_fetch (as cb_fetch), the rest by slice_store in batches of
+// kCbWordsPerThread loads in flight per thread.
+__device__ __forceinline__ void slice_fetch(const half_t* __restrict__ src, int words, CbStage& st) {
+#pragma unroll
+  for (int k = 0; k < kCbWordsPerThread; ++k) {
+    const int w = threadIdx.x + k * blockDim.x;
+    st.w[k] = reinterpret_cast<const u32x4*>(src)[w < words ? w : words - 1];
+  }
+}
+
+__device__ __forceinline__ void slice_store(uint8_t* __restrict__ lds, const half_t* __restrict__ src, int words,
+                                            const CbStage& st) {
+#pragma unroll
+  for (int k = 0; k < kCbWordsPerThread; ++k) {
+    const int w = threadIdx.x + k * blockDim.x;
+    if (w < words) *reinterpret_cast<u32x4*>(lds + (uint32_t)w * 16) = st.w[k];
+  }
+  for (int base = threadIdx.x + kCbWordsPerThread * blockDim.x; base < words;
+       base += kCbWordsPerThread * blockDim.x) {
+    u32x4 v[kCbWordsPerThread];
+#pragma unroll
+    for (int k = 0; k < kCbWordsPerThread; ++k) {
+      const int w = base + k * blockDim.x;
+      v[k] = reinterpret_cast<const u32x4*>(src)[w < words ? w : words - 1];
+    }
+#pragma unroll
+    for (int k = 0; k < kCbWordsPerThread; ++k) {
+      const int w = base + k * blockDim.x;
+      if (w < words) *reinterpret_cast<u32x4*>(lds + (uint32_t)w * 16) = v[k];
+    }
+  }
+}
+
 // LDS-resident codebooks start at LDS address 0: the kernels that use them
 // declare no static LDS (the launchers check this), so the dynamic segment
 // begins at 0 and an LDS address can be formed as a plain integer.
@@ -204,14 +243,27 @@ __device__ __forceinline__ void read_codeword_lds(uint32_t addr, uint32_t* out) 
   }
 }
 
-// Gather codeword u into `out` (layout as for read_codeword_lds).
+// The codebook slice resident in LDS (CB_SLICE): entries [base, base + mask].
+struct Slice {
+  uint32_t base = 0;
+  uint32_t mask = 0;
+};
+
+// Gather codeword u into `out` (layout as for read_codeword_lds).  In
+// CB_SLICE mode an id outside the resident slice reads nothing and yields
+// a zero codeword.
 template <int D, int MODE>
 __device__ __forceinline__ void gather(const half_t* __restrict__ gcb, uint32_t lane_off, uint32_t u,
-                                       uint32_t* out) {
+                                       uint32_t* out, Slice sl = Slice()) {
   if constexpr (MODE == CB_REPL) {
     read_codeword_lds<D>((u << 8) | lane_off, out);
   } else if constexpr (MODE == CB_LDS) {
     read_codeword_lds<D>(u * (2 * D), out);
+  } else if constexpr (MODE == CB_SLICE) {
+    const uint32_t loc = u - sl.base;
+#pragma unroll
+    for (int k = 0; k < (D + 1) / 2; ++k) out[k] = 0u;
+    if (loc <= sl.mask) read_codeword_lds<D>(loc * (2 * D), out);
   } else {
     const uint8_t* p = reinterpret_cast<const uint8_t*>(gcb) + (size_t)u * (2 * D);
     if constexpr (D == 1) {
@@ -238,12 +290,12 @@ __device__ __forceinline__ uint32_t repl_lane_off(int lane) {
 // offset, byte 1 = the id byte, bytes 2 and 3 = 0.
 template <int BITS, int D, int MODE>
 __device__ __forceinline__ void gather_id(const half_t* __restrict__ gcb, uint32_t lane_off, const uint32_t* w,
-                                          int i, uint32_t* out) {
+                                          int i, uint32_t* out, Slice sl = Slice()) {
   if constexpr (BITS == 8 && MODE == CB_REPL) {
     const uint32_t sel = 0x0C0C0000u | ((4u + (uint32_t)(i & 3)) << 8);
     read_codeword_lds<D>(__builtin_amdgcn_perm(w[i >> 2], lane_off, sel), out);
   } else {
-    gather<D, MODE>(gcb, lane_off, stream_id<BITS>(w, i), out);
+    gather<D, MODE>(gcb, lane_off, stream_id<BITS>(w, i), out, sl);
   }
 }
 
@@ -251,14 +303,14 @@ __device__ __forceinline__ void gather_id(const half_t* __restrict__ gcb, uint32
 // ids first .. first + 8/D - 1 of the lane's chunk w[], gathered and packed.
 template <int BITS, int D, int MODE>
 __device__ __forceinline__ half8_t gather8(const half_t* __restrict__ gcb, uint32_t lane_off, const uint32_t* w,
-                                           int first) {
+                                           int first, Slice sl = Slice()) {
   uint32_t o[4];
   if constexpr (D == 1) {
 #pragma unroll
     for (int e = 0; e < 8; e += 2) {
       uint32_t c0[1], c1[1];
-      gather_id<BITS, D, MODE>(gcb, lane_off, w, first + e, c0);
-      gather_id<BITS, D, MODE>(gcb, lane_off, w, first + e + 1, c1);
+      gather_id<BITS, D, MODE>(gcb, lane_off, w, first + e, c0, sl);
+      gather_id<BITS, D, MODE>(gcb, lane_off, w, first + e + 1, c1, sl);
       o[e / 2] = (c0[0] & 0xFFFFu) | (c1[0] << 16);
     }
   } else {
@@ -266,7 +318,7 @@ __device__ __forceinline__ half8_t gather8(const half_t* __restrict__ gcb, uint3
 #pragma unroll
     for (int e = 0; e < 8 / D; ++e) {
       uint32_t c[CW];
-      gather_id<BITS, D, MODE>(gcb, lane_off, w, first + e, c);
+      gather_id<BITS, D, MODE>(gcb, lane_off, w, first + e, c, sl);
 #pragma unroll
       for (int k = 0; k < CW; ++k) o[e * CW + k] = c[k];
     }

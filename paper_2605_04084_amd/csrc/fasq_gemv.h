@@ -44,6 +44,8 @@ struct GemvArgs {
   int cb_bytes;  // LDS bytes of the codebook (x follows)
   int xs;        // LDS bytes between rows of x
   int x_bytes;   // LDS bytes of x (partials follow)
+  int sl_shift;  // CB_SLICE: log2 of the entries per slice
+  int nsl;       // CB_SLICE: slices (passes over the rows)
   half_t* y;
 };
 
@@ -120,90 +122,117 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
   // workgroup (the only one on its CU) issue their codebook and x loads,
   // meet at a barrier (which does not wait for memory), and only then issue
   // the first index loads: the codebook and x come back first while the
-  // index stream is already in flight.
-  CbStage cst;
-  cb_fetch<D, MODE>(a.cb, a.C, cst);
+  // index stream is already in flight.  CB_SLICE repeats everything from the
+  // codebook staging to the end of the row loop once per slice; x is staged
+  // once.
   constexpr int XWT = MR == 1 ? 2 : kXWordsPerThread;
   const int xw_row = (int)(a.K / 8);        // 16-byte words per row of x
   const int xw_total = xw_row * M;
-  u32x4 xst[XWT];
-#pragma unroll
-  for (int k = 0; k < XWT; ++k) {
-    int w = threadIdx.x + k * blockDim.x;
-    w = w < xw_total ? w : xw_total - 1;
-    xst[k] = reinterpret_cast<const u32x4*>(a.x)[w];
-  }
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < L - 1; ++i) load_unit(i, i, i % T);
-
-  cb_store<D, MODE>(smem, a.cb, a.C, cst);
-#pragma unroll
-  for (int k = 0; k < XWT; ++k) {
-    const int w = threadIdx.x + k * blockDim.x;
-    if (w < xw_total) {
-      const int m = w / xw_row;
-      *reinterpret_cast<u32x4*>(xl + m * a.xs + (w - m * xw_row) * 16) = xst[k];
-    }
-  }
-  for (int w = threadIdx.x + XWT * blockDim.x; w < xw_total; w += blockDim.x) {
-    const int m = w / xw_row;
-    *reinterpret_cast<u32x4*>(xl + m * a.xs + (w - m * xw_row) * 16) = reinterpret_cast<const u32x4*>(a.x)[w];
-  }
-  __syncthreads();
-
   const uint32_t lane_off = repl_lane_off<D>(lane);
   const int mrow = MR == 1 ? 0 : (nl < M ? nl : M - 1);  // x row this lane feeds to the A operand
   const uint8_t* xrow = xl + mrow * a.xs;
-
   // A operands (x) live in registers when they fit, else are read from LDS
   // at every step.
   constexpr bool kXInRegs = !MASK && T * SPC <= 8;
   half8_t xreg[kXInRegs ? T * SPC : 1];
-  if constexpr (kXInRegs) {
-#pragma unroll
-    for (int t = 0; t < T; ++t)
-#pragma unroll
-      for (int s = 0; s < SPC; ++s)
-        xreg[t * SPC + s] = *reinterpret_cast<const half8_t*>(xrow + ccol(t) * (G * D * 2) + s * 16);
-  }
+  const int nsl = MODE == CB_SLICE ? a.nsl : 1;
 
-  float4_t acc0 = {0.f, 0.f, 0.f, 0.f};
-  float4_t acc1 = {0.f, 0.f, 0.f, 0.f};
+  for (int si = 0; si < nsl; ++si) {
+    Slice sl;
+    const half_t* scb = a.cb;
+    int sC = a.C;
+    if constexpr (MODE == CB_SLICE) {
+      sl.base = (uint32_t)si << a.sl_shift;
+      sl.mask = (1u << a.sl_shift) - 1u;
+      scb = a.cb + (size_t)sl.base * D;
+      sC = a.C - (int)sl.base < (1 << a.sl_shift) ? a.C - (int)sl.base : (1 << a.sl_shift);
+      if (si > 0) __syncthreads();  // every wave is done with the previous slice
+    }
+    CbStage cst;
+    if constexpr (MODE == CB_SLICE) slice_fetch(scb, sC * D * 2 / 16, cst);
+    else cb_fetch<D, MODE>(a.cb, a.C, cst);
+    u32x4 xst[XWT];
+    if (si == 0) {
+#pragma unroll
+      for (int k = 0; k < XWT; ++k) {
+        int w = threadIdx.x + k * blockDim.x;
+        w = w < xw_total ? w : xw_total - 1;
+        xst[k] = reinterpret_cast<const u32x4*>(a.x)[w];
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < L - 1; ++i) load_unit(i, i, i % T);
 
-  for (int base = 0; base < nunits; base += L) {
+    if constexpr (MODE == CB_SLICE) slice_store(smem, scb, sC * D * 2 / 16, cst);
+    else cb_store<D, MODE>(smem, a.cb, a.C, cst);
+    if (si == 0) {
 #pragma unroll
-    for (int i = 0; i < L; ++i) {
-      const int u = base + i;
-      const int t = i % T;
-      load_unit((i + L - 1) % L, u + L - 1, (i + L - 1) % T);
-      if (u < nunits) {
-        const uint32_t* w = buf[i];
-        const uint8_t* xa = xrow + ccol(t) * (G * D * 2);
-        const bool cval = !MASK || ccol_raw(t) < CH;
-#pragma unroll
-        for (int s = 0; s < SPC; ++s) {
-          half8_t bop = gather8<BITS, D, MODE>(a.cb, lane_off, w, s * (8 / D));
-          half8_t aop;
-          if constexpr (kXInRegs) aop = xreg[t * SPC + s];
-          else aop = *reinterpret_cast<const half8_t*>(xa + s * 16);
-          if (!cval) {
-            bop = half8_t{};
-            aop = half8_t{};
-          }
-          if (s & 1) acc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc1, 0, 0, 0);
-          else acc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc0, 0, 0, 0);
+      for (int k = 0; k < XWT; ++k) {
+        const int w = threadIdx.x + k * blockDim.x;
+        if (w < xw_total) {
+          const int m = w / xw_row;
+          *reinterpret_cast<u32x4*>(xl + m * a.xs + (w - m * xw_row) * 16) = xst[k];
         }
-        if (t == T - 1) {
-          // lane l holds rows m = 4g .. 4g + 3 of column nl of the 16 x 16 tile
-          const int lrow = ((u / T) * Q + q) * 16 + nl;
+      }
+      for (int w = threadIdx.x + XWT * blockDim.x; w < xw_total; w += blockDim.x) {
+        const int m = w / xw_row;
+        *reinterpret_cast<u32x4*>(xl + m * a.xs + (w - m * xw_row) * 16) = reinterpret_cast<const u32x4*>(a.x)[w];
+      }
+    }
+    __syncthreads();
+
+    if (si == 0) {
+      if constexpr (kXInRegs) {
 #pragma unroll
-          for (int k = 0; k < 4; ++k) {
-            const int m = 4 * g + k;
-            if (m < M) red[(lrow * M + m) * P + p] = acc0[k] + acc1[k];
+        for (int t = 0; t < T; ++t)
+#pragma unroll
+          for (int s = 0; s < SPC; ++s)
+            xreg[t * SPC + s] = *reinterpret_cast<const half8_t*>(xrow + ccol(t) * (G * D * 2) + s * 16);
+      }
+    }
+
+    float4_t acc0 = {0.f, 0.f, 0.f, 0.f};
+    float4_t acc1 = {0.f, 0.f, 0.f, 0.f};
+
+    for (int base = 0; base < nunits; base += L) {
+#pragma unroll
+      for (int i = 0; i < L; ++i) {
+        const int u = base + i;
+        const int t = i % T;
+        load_unit((i + L - 1) % L, u + L - 1, (i + L - 1) % T);
+        if (u < nunits) {
+          const uint32_t* w = buf[i];
+          const uint8_t* xa = xrow + ccol(t) * (G * D * 2);
+          const bool cval = !MASK || ccol_raw(t) < CH;
+#pragma unroll
+          for (int s = 0; s < SPC; ++s) {
+            half8_t bop = gather8<BITS, D, MODE>(a.cb, lane_off, w, s * (8 / D), sl);
+            half8_t aop;
+            if constexpr (kXInRegs) aop = xreg[t * SPC + s];
+            else aop = *reinterpret_cast<const half8_t*>(xa + s * 16);
+            if (!cval) {
+              bop = half8_t{};
+              aop = half8_t{};
+            }
+            if (s & 1) acc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc1, 0, 0, 0);
+            else acc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc0, 0, 0, 0);
           }
-          acc0 = float4_t{0.f, 0.f, 0.f, 0.f};
-          acc1 = float4_t{0.f, 0.f, 0.f, 0.f};
+          if (t == T - 1) {
+            // lane l holds rows m = 4g .. 4g + 3 of column nl of the 16 x 16
+            // tile; slices of a row are summed in slice order by this lane
+            const int lrow = ((u / T) * Q + q) * 16 + nl;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+              const int m = 4 * g + k;
+              if (m < M) {
+                float* r = &red[(lrow * M + m) * P + p];
+                *r = (MODE == CB_SLICE && si > 0) ? *r + (acc0[k] + acc1[k]) : acc0[k] + acc1[k];
+              }
+            }
+            acc0 = float4_t{0.f, 0.f, 0.f, 0.f};
+            acc1 = float4_t{0.f, 0.f, 0.f, 0.f};
+          }
         }
       }
     }
@@ -252,6 +281,7 @@ struct GemvM1Mat {
   int C;
   int wg_begin;
   int wg_count;
+  int nsl;  // CB_SLICE: codebook slices (passes over the rows)
 };
 
 constexpr int kM1MaxMats = 8;  // matrices one single-token launch can take
@@ -265,6 +295,7 @@ struct GemvM1Args {
   int NRW;       // rows per row group
   int cb_bytes;  // LDS bytes of the codebook (x follows)
   int x_bytes;   // LDS bytes of x (partials follow)
+  int sl_shift;  // CB_SLICE: log2 of the entries per slice
   int nmat;
   GemvM1Mat mat[kM1MaxMats];
 };
@@ -327,110 +358,137 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
     buffer_chunk<BITS>(rsrc, roff + (uint32_t)t * (64 * CBY), buf[slot]);
   };
 
-  // ---- prologue (see k_gemv): codebook and x first, then the index stream
-  CbStage cst;
-  cb_fetch<D, MODE>(cb, C, cst);
-  // x in 16-byte words: thread t stages words t and t + blockDim.x; waves
-  // whose words all lie past the end of x issue no load for them.
+  // ---- prologue (see k_gemv): codebook and x first, then the index stream.
+  // CB_SLICE repeats everything from the codebook staging to the end of the
+  // row loop once per slice; x is staged once.
   constexpr int XWT = 2;
   const int xw_total = (int)(a.K / 8);
-  u32x4 xst[XWT];
-#pragma unroll
-  for (int k = 0; k < XWT; ++k) {
-    if (wave * kWave + k * (int)blockDim.x < xw_total) {
-      int w = threadIdx.x + k * blockDim.x;
-      w = w < xw_total ? w : xw_total - 1;
-      xst[k] = reinterpret_cast<const u32x4*>(a.x)[w];
-    }
-  }
-  // Every wave's codebook and x requests enter the CU's (in-order) memory
-  // queue before any index load, and only the first kM1EarlyLoads index loads
-  // of a wave go out before the staging barrier: the barrier then waits for
-  // the small staging data alone, not for the whole workgroup to get its
-  // loads accepted by a saturated memory queue.
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < kM1EarlyLoads; ++i) load_unit(i, row0 + (uint32_t)(i / T) * rstride, i % T);
-
-  cb_store<D, MODE>(smem, cb, C, cst);
-#pragma unroll
-  for (int k = 0; k < XWT; ++k) {
-    const int w = threadIdx.x + k * blockDim.x;
-    if (w < xw_total) reinterpret_cast<u32x4*>(xl)[w] = xst[k];
-  }
-  for (int w = threadIdx.x + XWT * blockDim.x; w < xw_total; w += blockDim.x)
-    reinterpret_cast<u32x4*>(xl)[w] = reinterpret_cast<const u32x4*>(a.x)[w];
-  __syncthreads();
-
   const uint32_t lane_off = repl_lane_off<D>(lane);
   half8_t xreg[kXInRegs ? T * SPC : 1];
-  if constexpr (kXInRegs) {
-#pragma unroll
-    for (int t = 0; t < T; ++t) {
-      const bool ok = !MASK || ccol_raw(t) < CH;
-#pragma unroll
-      for (int s = 0; s < SPC; ++s) {
-        const half8_t v = *reinterpret_cast<const half8_t*>(xl + ccol(t) * (G * D * 2) + s * 16);
-        xreg[t * SPC + s] = ok ? v : half8_t{};
-      }
-    }
-  }
-
   // lane l holds D[4g + i][j]; the diagonal element D[j][j] sits in lane
   // j + 16 * (j / 4), register j % 4
   const bool on_diag = (j >> 2) == g;
   const int diag_reg = j & 3;
+  const int nsl = MODE == CB_SLICE ? a.mat[m].nsl : 1;
 
-  float4_t acc0 = {0.f, 0.f, 0.f, 0.f};
-  float4_t acc1 = {0.f, 0.f, 0.f, 0.f};
-  auto compute_unit = [&](int slot, int u, int t) {
-    const uint32_t* w = buf[slot];
-    const bool cval = !MASK || ccol_raw(t) < CH;
+  for (int si = 0; si < nsl; ++si) {
+    Slice sl;
+    const half_t* scb = cb;
+    int sC = C;
+    if constexpr (MODE == CB_SLICE) {
+      sl.base = (uint32_t)si << a.sl_shift;
+      sl.mask = (1u << a.sl_shift) - 1u;
+      scb = cb + (size_t)sl.base * D;
+      sC = C - (int)sl.base < (1 << a.sl_shift) ? C - (int)sl.base : (1 << a.sl_shift);
+      if (si > 0) __syncthreads();  // every wave is done with the previous slice
+    }
+    CbStage cst;
+    if constexpr (MODE == CB_SLICE) slice_fetch(scb, sC * D * 2 / 16, cst);
+    else cb_fetch<D, MODE>(cb, C, cst);
+    // x in 16-byte words: thread t stages words t and t + blockDim.x; waves
+    // whose words all lie past the end of x issue no load for them.
+    u32x4 xst[XWT];
+    if (si == 0) {
 #pragma unroll
-    for (int s = 0; s < SPC; ++s) {
-      half8_t aop = gather8<BITS, D, MODE>(cb, lane_off, w, s * (8 / D));
-      half8_t bop;
-      if constexpr (kXInRegs) bop = xreg[t * SPC + s];
-      else bop = *reinterpret_cast<const half8_t*>(xl + ccol(t) * (G * D * 2) + s * 16);
-      if (MASK && !cval) {
-        aop = half8_t{};
-        bop = half8_t{};
+      for (int k = 0; k < XWT; ++k) {
+        if (wave * kWave + k * (int)blockDim.x < xw_total) {
+          int w = threadIdx.x + k * blockDim.x;
+          w = w < xw_total ? w : xw_total - 1;
+          xst[k] = reinterpret_cast<const u32x4*>(a.x)[w];
+        }
       }
-      if (s & 1) acc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc1, 0, 0, 0);
-      else acc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc0, 0, 0, 0);
     }
-    if (t == T - 1) {
-      const float4_t acc = acc0 + acc1;
-      float v = diag_reg == 0 ? acc[0] : diag_reg == 1 ? acc[1] : diag_reg == 2 ? acc[2] : acc[3];
-      v = on_diag ? v : 0.f;
-      v = group_sum<16>(v);
-      // the four rows of 16 lanes hold partial sums: combine in a fixed order
-      const float sum = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0)) +
-                        __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16)) +
-                        __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32)) +
-                        __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
-      if (lane == 0) red[((u / T) * Q + q) * P + p] = sum;
-      acc0 = float4_t{0.f, 0.f, 0.f, 0.f};
-      acc1 = float4_t{0.f, 0.f, 0.f, 0.f};
-    }
-  };
-
-  // Unit k lives in slot k % L, and kM1Window loads stay in flight.  A wave
-  // computes a unit before it issues the next load, so data that has arrived
-  // is never held up behind a load waiting for room in the memory queue.
-  // First window: units below kM1EarlyLoads are already in flight.
-  constexpr int W = kM1Window;
+    // Every wave's codebook and x requests enter the CU's (in-order) memory
+    // queue before any index load, and only the first kM1EarlyLoads index
+    // loads of a wave go out before the staging barrier: the barrier then
+    // waits for the small staging data alone, not for the whole workgroup to
+    // get its loads accepted by a saturated memory queue.
+    __syncthreads();
 #pragma unroll
-  for (int i = 0; i < L; ++i) {
-    if (i < nunits) compute_unit(i, i, i % T);
-    if (i + W >= kM1EarlyLoads) load_unit((i + W) % L, row0 + (uint32_t)((i + W) / T) * rstride, (i + W) % T);
-  }
-  uint32_t rbase = row0 + (uint32_t)(L / T) * rstride;  // offset of local row base / T
-  for (int base = L; base < nunits; base += L, rbase += (uint32_t)(L / T) * rstride) {
+    for (int i = 0; i < kM1EarlyLoads; ++i) load_unit(i, row0 + (uint32_t)(i / T) * rstride, i % T);
+
+    if constexpr (MODE == CB_SLICE) slice_store(smem, scb, sC * D * 2 / 16, cst);
+    else cb_store<D, MODE>(smem, cb, C, cst);
+    if (si == 0) {
+#pragma unroll
+      for (int k = 0; k < XWT; ++k) {
+        const int w = threadIdx.x + k * blockDim.x;
+        if (w < xw_total) reinterpret_cast<u32x4*>(xl)[w] = xst[k];
+      }
+      for (int w = threadIdx.x + XWT * blockDim.x; w < xw_total; w += blockDim.x)
+        reinterpret_cast<u32x4*>(xl)[w] = reinterpret_cast<const u32x4*>(a.x)[w];
+    }
+    __syncthreads();
+
+    if (si == 0) {
+      if constexpr (kXInRegs) {
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+          const bool ok = !MASK || ccol_raw(t) < CH;
+#pragma unroll
+          for (int s = 0; s < SPC; ++s) {
+            const half8_t v = *reinterpret_cast<const half8_t*>(xl + ccol(t) * (G * D * 2) + s * 16);
+            xreg[t * SPC + s] = ok ? v : half8_t{};
+          }
+        }
+      }
+    }
+
+    float4_t acc0 = {0.f, 0.f, 0.f, 0.f};
+    float4_t acc1 = {0.f, 0.f, 0.f, 0.f};
+    auto compute_unit = [&](int slot, int u, int t) {
+      const uint32_t* w = buf[slot];
+      const bool cval = !MASK || ccol_raw(t) < CH;
+#pragma unroll
+      for (int s = 0; s < SPC; ++s) {
+        half8_t aop = gather8<BITS, D, MODE>(cb, lane_off, w, s * (8 / D), sl);
+        half8_t bop;
+        if constexpr (kXInRegs) bop = xreg[t * SPC + s];
+        else bop = *reinterpret_cast<const half8_t*>(xl + ccol(t) * (G * D * 2) + s * 16);
+        if (MASK && !cval) {
+          aop = half8_t{};
+          bop = half8_t{};
+        }
+        if (s & 1) acc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc1, 0, 0, 0);
+        else acc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc0, 0, 0, 0);
+      }
+      if (t == T - 1) {
+        const float4_t acc = acc0 + acc1;
+        float v = diag_reg == 0 ? acc[0] : diag_reg == 1 ? acc[1] : diag_reg == 2 ? acc[2] : acc[3];
+        v = on_diag ? v : 0.f;
+        v = group_sum<16>(v);
+        // the four rows of 16 lanes hold partial sums: combine in a fixed order
+        const float sum = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0)) +
+                          __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16)) +
+                          __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32)) +
+                          __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+        // slices of a row are summed in slice order, each by the same lane
+        if (lane == 0) {
+          float* r = &red[((u / T) * Q + q) * P + p];
+          *r = (MODE == CB_SLICE && si > 0) ? *r + sum : sum;
+        }
+        acc0 = float4_t{0.f, 0.f, 0.f, 0.f};
+        acc1 = float4_t{0.f, 0.f, 0.f, 0.f};
+      }
+    };
+
+    // Unit k lives in slot k % L, and kM1Window loads stay in flight.  A
+    // wave computes a unit before it issues the next load, so data that has
+    // arrived is never held up behind a load waiting for room in the memory
+    // queue.  First window: units below kM1EarlyLoads are already in flight.
+    constexpr int W = kM1Window;
 #pragma unroll
     for (int i = 0; i < L; ++i) {
-      if (base + i < nunits) compute_unit(i, base + i, i % T);
-      load_unit((i + W) % L, rbase + (uint32_t)((i + W) / T) * rstride, (i + W) % T);
+      if (i < nunits) compute_unit(i, i, i % T);
+      if (i + W >= kM1EarlyLoads) load_unit((i + W) % L, row0 + (uint32_t)((i + W) / T) * rstride, (i + W) % T);
+    }
+    uint32_t rbase = row0 + (uint32_t)(L / T) * rstride;  // offset of local row base / T
+    for (int base = L; base < nunits; base += L, rbase += (uint32_t)(L / T) * rstride) {
+#pragma unroll
+      for (int i = 0; i < L; ++i) {
+        if (base + i < nunits) compute_unit(i, base + i, i % T);
+        load_unit((i + W) % L, rbase + (uint32_t)((i + W) / T) * rstride, (i + W) % T);
+      }
     }
   }
   __syncthreads();

@@ -9,6 +9,8 @@
 namespace fasq {
 
 constexpr int kLdsCodebookBudget = 64 * 1024;  // bytes of LDS a codebook may take
+constexpr int kSliceReserve = 8 * 1024;        // LDS kept for row partials beside a codebook slice
+constexpr int kMinSliceBytes = 32 * 1024;      // smaller slices: gather from global memory instead
 static_assert(kM1MaxMats == kMaxBatchLaunch, "grouped launches and their kernel disagree on the group size");
 
 // Once per device and kernel: check that the kernel declares no static LDS
@@ -69,6 +71,9 @@ hipError_t launch_gemv_mode(const GemvArgs& a, int mode, int T, bool mask, int t
   switch (mode) {
     case CB_REPL: return launch_gemv_t<BITS, MR, D, CB_REPL>(a, T, mask, threads, blocks, lds, stream);
     case CB_LDS: return launch_gemv_t<BITS, MR, D, CB_LDS>(a, T, mask, threads, blocks, lds, stream);
+    case CB_SLICE:  // only 16-bit ids address codebooks larger than LDS
+      if constexpr (BITS == 16) return launch_gemv_t<BITS, MR, D, CB_SLICE>(a, T, mask, threads, blocks, lds, stream);
+      else return hipErrorNotSupported;
     default: return launch_gemv_t<BITS, MR, D, CB_GLOBAL>(a, T, mask, threads, blocks, lds, stream);
   }
 }
@@ -102,10 +107,21 @@ hipError_t launch_gemv_bits(const Problem& p, const DeviceInfo& dev, hipStream_t
   const bool mask = (int64_t)P * T * 4 != CH;  // the last wave sees columns past the row end
   const int threads = P * Q * kWave;
 
-  const int mode = choose_cb_mode(p.C, d);
-  const int cb_bytes = (int)cb_lds_bytes(mode, p.C, d);
+  int mode = choose_cb_mode(p.C, d);
   const int xs = (int)(p.M == 1 ? p.K * 2 : p.K * 2 + 16);
   const int64_t x_bytes = p.M * (int64_t)xs;
+  // A codebook too large for the LDS budget still goes to LDS when all of it
+  // fits beside x and the partials of two row groups (one slice, one pass).
+  // More passes do not pay here: each pass costs as much as the whole
+  // gather-from-L2 kernel at M >= 4.
+  int sl_shift = 0;
+  if (mode == CB_GLOBAL && (p.C * d * 2) % 16 == 0) {
+    const int64_t red_min = 2 * (int64_t)Q * 16 * p.M * P * 4;
+    const int64_t room = dev.lds_per_block - x_bytes - (red_min > kSliceReserve ? red_min : kSliceReserve);
+    while (sl_shift < 16 && (int64_t(2) << sl_shift) * d * 2 <= room) ++sl_shift;
+    if ((int64_t(1) << sl_shift) * d * 2 >= kMinSliceBytes && (int64_t(1) << sl_shift) >= p.C) mode = CB_SLICE;
+  }
+  const int cb_bytes = mode == CB_SLICE ? (int)((int64_t(1) << sl_shift) * d * 2) : (int)cb_lds_bytes(mode, p.C, d);
   const int64_t avail = dev.lds_per_block - cb_bytes - x_bytes;
 
   // Row tiles of 16 are dealt round-robin to at most one workgroup per CU;
@@ -139,6 +155,8 @@ hipError_t launch_gemv_bits(const Problem& p, const DeviceInfo& dev, hipStream_t
   a.cb_bytes = cb_bytes;
   a.xs = xs;
   a.x_bytes = (int)x_bytes;
+  a.sl_shift = sl_shift;
+  a.nsl = mode == CB_SLICE ? (int)((p.C + (int64_t(1) << sl_shift) - 1) >> sl_shift) : 1;
   a.y = static_cast<half_t*>(p.y);
   switch (d) {
     case 1: return launch_gemv_mode<BITS, MR, 1>(a, mode, T, mask, threads, (int)nwg, lds, stream);
@@ -180,6 +198,9 @@ hipError_t launch_gemv_m1_mode(const GemvM1Args& a, int mode, int T, bool mask, 
   switch (mode) {
     case CB_REPL: return launch_gemv_m1_t<BITS, D, CB_REPL>(a, T, mask, threads, blocks, lds, stream);
     case CB_LDS: return launch_gemv_m1_t<BITS, D, CB_LDS>(a, T, mask, threads, blocks, lds, stream);
+    case CB_SLICE:  // only 16-bit ids address codebooks larger than LDS
+      if constexpr (BITS == 16) return launch_gemv_m1_t<BITS, D, CB_SLICE>(a, T, mask, threads, blocks, lds, stream);
+      else return hipErrorNotSupported;
     default: return launch_gemv_m1_t<BITS, D, CB_GLOBAL>(a, T, mask, threads, blocks, lds, stream);
   }
 }
@@ -235,12 +256,20 @@ hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& d
   const bool mask = (int64_t)P * T * 64 != CH;
 
   // One codebook placement for the launch: the largest codebook decides it.
-  const int mode = choose_cb_mode(maxC, d);
+  // A codebook too large for LDS is staged slice by slice (one pass over the
+  // rows per slice) when its slices fit beside x and the row partials.
+  int mode = choose_cb_mode(maxC, d);
+  const int64_t x_bytes = (p.K * 2 + 15) / 16 * 16;
+  int sl_shift = 0;
+  if (mode == CB_GLOBAL && (maxC * d * 2) % 16 == 0) {
+    const int64_t room = dev.lds_per_block - x_bytes - kSliceReserve;
+    while (sl_shift < 16 && (int64_t(2) << sl_shift) * d * 2 <= room) ++sl_shift;
+    if ((int64_t(1) << sl_shift) * d * 2 >= kMinSliceBytes) mode = CB_SLICE;
+  }
   if (mode != CB_GLOBAL)  // every codebook must be whole 16-byte words to be staged
     for (int i = 0; i < count; ++i)
       if ((ps[i].C * d * 2) % 16 != 0) return hipErrorNotSupported;
-  const int cb_bytes = (int)cb_lds_bytes(mode, maxC, d);
-  const int64_t x_bytes = (p.K * 2 + 15) / 16 * 16;
+  const int cb_bytes = mode == CB_SLICE ? (int)((int64_t(1) << sl_shift) * d * 2) : (int)cb_lds_bytes(mode, maxC, d);
   const int64_t avail = dev.lds_per_block - cb_bytes - x_bytes;
 
   // Q row groups per workgroup: enough workgroups to cover every CU for
@@ -303,6 +332,7 @@ hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& d
   a.NRW = (int)nrw;
   a.cb_bytes = cb_bytes;
   a.x_bytes = (int)x_bytes;
+  a.sl_shift = sl_shift;
   a.nmat = count;
   int64_t begin = 0;
   for (int i = 0; i < count; ++i) {
@@ -314,6 +344,7 @@ hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& d
     mt.C = (int)ps[i].C;
     mt.wg_begin = (int)begin;
     mt.wg_count = (int)wgs[i];
+    mt.nsl = mode == CB_SLICE ? (int)((ps[i].C + (int64_t(1) << sl_shift) - 1) >> sl_shift) : 1;
     begin += wgs[i];
   }
   switch (d) {

@@ -377,3 +377,51 @@ def test_batched_one_hot_bit_exact():
     for g, p in zip(got, probs):
         ref = orc.pq_linear(x, p.idx, 8, d, p.codebook)
         assert np.array_equal(g.astype(np.float64), ref)
+
+
+# ---------------------------------------------------------------------------
+# Codebooks larger than LDS, staged slice by slice (one pass per slice)
+# ---------------------------------------------------------------------------
+
+SLICED = [
+    # M, K, N, d, C, bits: the decode kernels take the codebook in LDS slices
+    (1, 4096, 300, 4, 40000, 16),    # 3 slices of 16384 entries, the last one partial
+    (1, 2048, 100, 2, 65536, 16),    # 2 slices of 32768
+    (1, 1024, 200, 8, 65536, 16),    # 8 slices of 8192
+    (1, 4096, 64, 1, 65536, 16),     # 1 slice: the whole 128 KB codebook
+    (1, 12288, 70, 4, 65536, 16),    # wide x beside the slice
+    (2, 2048, 100, 1, 65536, 16),    # several tokens: one slice beside x and the partials
+    (4, 1024, 64, 1, 60000, 16),
+]
+
+
+@pytest.mark.parametrize("case", SLICED)
+def test_sliced_codebook(case):
+    M, K, N, d, C, bits = case
+    print(f"[case] gemv sliced codebook {case}", flush=True)
+    assert ", 3, " in fasq.plan("gemv", M, K, N, bits, d, C)  # CB_SLICE
+    rng = np.random.default_rng(sum(case))
+    p = pi.draw_problem(rng, M, K, N, d, C, bits)
+    assert_close(run("gemv", p), orc.pq_linear(p.x, p.idx, bits, d, p.codebook), f"sliced {case}")
+
+
+@pytest.mark.parametrize("case", SLICED)
+def test_sliced_codebook_boundaries_bit_exact(case):
+    """Ids on both sides of every slice boundary, and the last id, with
+    signed one-hot codewords: exact integers, so bit-exact."""
+    M, K, N, d, C, bits = case
+    print(f"[case] gemv sliced boundaries {case}", flush=True)
+    rng = np.random.default_rng(5 + sum(case))
+    cb = pi.signed_one_hot_codebook(C, d, rng)
+    edges = []
+    for shift in (13, 14, 15, 16):
+        for b in range(1 << shift, C, 1 << shift):
+            edges += [b - 1, b]
+    edges = np.unique(np.array(edges + [0, C - 1]))
+    ids = rng.choice(edges, size=(N, K // d))
+    x = pi.ternary_x(rng, M, K)
+    idx = pi.pack_indices(ids, bits)
+    ref = orc.pq_linear(x, idx, bits, d, cb)
+    assert np.abs(ref).max() <= 2048
+    y = to_np(fasq.pq_gemv(to_dev(x), to_dev(idx), bits, d, to_dev(cb))).astype(np.float64)
+    assert np.array_equal(y, ref)
