@@ -98,8 +98,10 @@ class MatrixSet:
     matrix, a group of one is one fasq_pq_gemv call.
     """
 
-    def __init__(self, torch, fasq, problems, names, groups=None, min_copies=1, rotation_bytes=ROTATION_BYTES):
+    def __init__(self, torch, fasq, problems, names, groups=None, min_copies=1, rotation_bytes=ROTATION_BYTES,
+                 regime="gemv"):
         self.torch, self.fasq = torch, fasq
+        self.regime = regime
         self.problems, self.names = problems, names
         self.groups = groups if groups is not None else [[i] for i in range(len(problems))]
         self.bytes = [gemv_bytes(p.M, p.K, p.N, p.d, p.C, p.idx_bits) for p in problems]
@@ -133,7 +135,7 @@ class MatrixSet:
 
     def group_kernel(self, g):
         p = self.problems[self.groups[g][0]]
-        return self.fasq.plan("gemv", p.M, p.K, p.N, p.idx_bits, p.d, p.C)
+        return self.fasq.plan(self.regime, p.M, p.K, p.N, p.idx_bits, p.d, p.C)
 
     def launch(self, c, g, stream):
         members = self.groups[g]
@@ -141,8 +143,9 @@ class MatrixSet:
         p0, x = self.problems[members[0]], s[members[0]]["x"].data_ptr()
         if len(members) == 1:
             t = s[members[0]]
-            st = self.fasq.gemv_raw(x, p0.M, p0.K, p0.N, t["idx"].data_ptr(), p0.idx_bits, p0.d,
-                                    t["cb"].data_ptr(), p0.C, t["y"].data_ptr(), stream)
+            fn = self.fasq.gemm_raw if self.regime == "gemm" else self.fasq.gemv_raw
+            st = fn(x, p0.M, p0.K, p0.N, t["idx"].data_ptr(), p0.idx_bits, p0.d,
+                    t["cb"].data_ptr(), p0.C, t["y"].data_ptr(), stream)
         else:
             st = self.fasq.gemv_batched_raw(
                 x, p0.M, p0.K, [s[i]["idx"].data_ptr() for i in members], [self.problems[i].N for i in members],
@@ -393,6 +396,96 @@ def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None, gro
     return res
 
 
+# ---------------------------------------------------------------------------
+# Sensitivity sweeps on one 4096 x 4096 layer (the paper's Fig. sensitivity):
+# codebook size, sub-vector length, batch size (GEMV against GEMM: the
+# dispatch crossover of fasq_pq_linear) and prefill length.  Every launch
+# reads cold copies, as in the decode timing.
+# ---------------------------------------------------------------------------
+
+SENS_N = SENS_K = 4096
+
+
+def time_single(torch, fasq, p, regime, steps=10):
+    """Median per-launch seconds of one PQ problem (cold rotated copies)."""
+    ms = MatrixSet(torch, fasq, [p], ["m"], min_copies=TIMING_COPIES, regime=regime)
+    for c in range(ms.copies):
+        ms.launch_all(c, torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    t = max(float(np.median(ms.time_kernels(steps)[0])), 1e-7)
+    kernel = ms.group_kernel(0)
+    del ms
+    return t, kernel
+
+
+def time_dense(torch, M, K, N, steps=10, short=2, long=10):
+    """Median per-call seconds of torch.matmul on fp16 x [M x K] and W [K x N]
+    (uncompressed weights), over rotated cold copies of W."""
+    dev = torch.device("cuda:0")
+    copies = max(short + long, math.ceil(ROTATION_BYTES / (K * N * 2)) + 1)
+    ws = [(torch.randn((K, N), device=dev) * 0.02).to(torch.float16) for _ in range(copies)]
+    x = torch.randn((M, K), device=dev).to(torch.float16)
+    y = torch.empty((M, N), dtype=torch.float16, device=dev)
+    stream = torch.cuda.current_stream()
+    for w in ws:
+        torch.matmul(x, w, out=y)
+
+    def batch(first, count):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(SPACER_CYCLES)
+        e0.record(stream)
+        for j in range(count):
+            torch.matmul(x, ws[first + j], out=y)
+        e1.record(stream)
+        e1.synchronize()
+        return e0.elapsed_time(e1) * 1e-3
+
+    per = [(batch(0, long) - batch(long, short)) / (long - short) for _ in range(steps)]
+    del ws
+    torch.cuda.empty_cache()
+    return max(float(np.median(per)), 1e-7)
+
+
+def sensitivity(torch, fasq, pi):
+    out = dict(shape=f"{SENS_N}x{SENS_K}", codebook_size=[], subvector=[], batch=[], prefill=[])
+    rng = np.random.default_rng(2026)
+
+    def gemv_row(M, d, C, bits, regime="gemv"):
+        p = pi.draw_problem(rng, M, SENS_K, SENS_N, d, C, bits)
+        t, kern = time_single(torch, fasq, p, regime)
+        b = gemv_bytes(M, SENS_K, SENS_N, d, C, bits)
+        return dict(M=M, d=d, C=C, idx_bits=bits, regime=regime, us=t * 1e6, gbs=b / t / 1e9,
+                    tflops=2.0 * M * SENS_N * SENS_K / t / 1e12, kernel=kern)
+
+    dense1 = time_dense(torch, 1, SENS_K, SENS_N)
+    out["dense_fp16_gemv_us"] = dense1 * 1e6
+    log(f"[bench] sensitivity: dense fp16 GEMV (torch.matmul, M=1) {dense1 * 1e6:.2f} us")
+    for C in (16, 32, 64, 128, 256):
+        r = gemv_row(1, 2, C, 8)
+        out["codebook_size"].append(r)
+        log(f"[bench] sensitivity C={C:4d} d=2: {r['us']:.2f} us ({r['gbs']:.0f} GB/s) {r['kernel']}")
+    for d in (1, 2, 4, 8):
+        r = gemv_row(1, d, 256, 8)
+        out["subvector"].append(r)
+        log(f"[bench] sensitivity d={d} C=256: {r['us']:.2f} us ({r['gbs']:.0f} GB/s) {r['kernel']}")
+    for M in (1, 2, 4, 8, 16, 32, 64, 128):
+        row = dict(M=M, dense_us=time_dense(torch, M, SENS_K, SENS_N) * 1e6)
+        if M <= 16:
+            row["gemv_us"] = gemv_row(M, 2, 256, 8)["us"]
+        row["gemm_us"] = gemv_row(M, 2, 256, 8, regime="gemm")["us"]
+        out["batch"].append(row)
+        log(f"[bench] sensitivity batch M={M:3d}: gemv {row.get('gemv_us', float('nan')):8.2f} us, "
+            f"gemm {row['gemm_us']:8.2f} us, dense fp16 {row['dense_us']:8.2f} us")
+    for L in (32, 64, 128, 256, 512, 1024, 2048):
+        r = gemv_row(L, 2, 256, 8, regime="gemm")
+        r["dense_us"] = time_dense(torch, L, SENS_K, SENS_N) * 1e6
+        out["prefill"].append(r)
+        log(f"[bench] sensitivity prefill L={L:5d}: {r['us']:8.2f} us ({r['tflops']:.0f} TFLOP/s), "
+            f"dense fp16 {r['dense_us']:8.2f} us")
+    torch.cuda.empty_cache()
+    return out
+
+
 def dense_gemm_seconds(torch, x, w, reps, short, long):
     """Per-call time of torch.matmul(x, w) (fp16, rocBLAS/hipBLASLt), timed
     like the PQ GEMM: differential over back-to-back calls."""
@@ -512,6 +605,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-extra", action="store_true", help="only the effective-4-bit decode layer")
     ap.add_argument("--per-matrix", action="store_true", help="add the 4-bit layer with one launch per matrix")
+    ap.add_argument("--sensitivity", action="store_true",
+                    help="add the codebook-size, sub-vector, batch and prefill-length sweeps on one 4096x4096 layer")
     ap.add_argument("--out", default=None, help="also write the JSON record to this file")
     ap.add_argument("--pmc-pass", metavar="MANIFEST", default=None,
                     help="run the short launch sequence for a rocprofv3 --pmc pass and write its manifest")
@@ -581,6 +676,9 @@ def main():
             log(f"[bench] qwen M={M}: kernel sum {r5['us_per_layer_kernel_sum']:.2f} us/layer "
                 f"({r5['gbs_kernel_sum']:.1f} GB/s); x36 layers {36 * r5['us_per_layer_kernel_sum'] / 1e3:.3f} ms")
             extra[f"qwen3_8b_M{M}"] = r5
+
+    if args.sensitivity:
+        extra["sensitivity"] = sensitivity(torch, fasq, pi)
 
     cpu = None
     if not args.no_cpu:

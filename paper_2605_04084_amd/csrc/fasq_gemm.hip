@@ -6,27 +6,34 @@ namespace fasq {
 
 namespace {
 
-template <int BITS, int D, int MODE, int BM, int BN, int WGM, int WGN, int WANT>
+template <int BITS, int D, int MODE, int BM, int BN, int WGM, int WGN, int WANT, int KG>
 hipError_t launch_gemm_variant(const GemmArgs& a, int lds, hipStream_t stream) {
   constexpr int NS = gemm_ring_depth(BITS, D, BM, BN, WGM * WGN, WANT);
-  auto kern = k_gemm_mfma<BITS, D, MODE, BM, BN, WGM, WGN, NS>;
-  if (plan_record("k_gemm_mfma", {BITS, D, MODE, BM, BN, WGM, WGN, NS})) return hipSuccess;
+  auto kern = k_gemm_mfma<BITS, D, MODE, BM, BN, WGM, WGN, NS, KG>;
+  if (plan_record("k_gemm_mfma", {BITS, D, MODE, BM, BN, WGM, WGN, NS, KG})) return hipSuccess;
   hipError_t e = prepare_kernel(kern);
   if (e != hipSuccess) return e;
   dim3 grid((unsigned)((a.N + BN - 1) / BN), (unsigned)((a.M + BM - 1) / BM));
-  hipLaunchKernelGGL(kern, grid, dim3(WGM * WGN * kWave), lds, stream, a);
+  hipLaunchKernelGGL(kern, grid, dim3(WGM * WGN * KG * kWave), lds, stream, a);
   return hipGetLastError();
 }
 
 // Tile shapes, largest first: 128 x 256 on 2 x 4 waves (half the X re-reads
 // per output, two waves per SIMD), 128 x 128, 64 x 128 and 64 x 64 on 2 x 2
 // waves, with the LDS ring depth of each.  The launcher takes the largest
-// tile whose grid covers at least 3/4 of the CUs, else the smallest.
+// tile whose grid covers at least 3/4 of the CUs, else the smallest.  The
+// 64-row tiles (small grids) also split K over KG groups of waves inside the
+// workgroup, with a shallower ring per group.
 struct GemmTileShape {
   int bm, bn, ns;
 };
 constexpr GemmTileShape kGemmTiles[] = {{128, 256, 4}, {128, 128, 4}, {64, 128, 8}, {64, 64, 8}};
 constexpr int kGemmNumTiles = 4;
+// K groups tried for the 64-row tiles, in order.  Two groups (two waves per
+// SIMD) with the replicated codebook measured best; four groups only fit
+// with one codebook copy, whose bank conflicts cost more than they gain.
+constexpr int kGemmSplitGroups[] = {2, 1};
+inline int gemm_group_ring(int kg, int ns) { return kg == 1 ? ns : kg == 2 ? 4 : 3; }
 
 inline int gemm_tile_waves(int t) { return kGemmTiles[t].bn == 256 ? 8 : 4; }
 
@@ -35,41 +42,49 @@ inline bool gemm_tile_ok(int t, int hb) {
   return (kGemmTiles[t].bn * (2 * hb / 4)) % (gemm_tile_waves(t) * kWave) == 0;
 }
 
+template <int BITS, int D, int MODE, int BM, int BN, int NS1>
+hipError_t launch_gemm_groups(const GemmArgs& a, int kg, int lds, hipStream_t stream) {
+  switch (kg) {
+    case 2: return launch_gemm_variant<BITS, D, MODE, BM, BN, 2, 2, 4, 2>(a, lds, stream);
+    default: return launch_gemm_variant<BITS, D, MODE, BM, BN, 2, 2, NS1, 1>(a, lds, stream);
+  }
+}
+
 template <int BITS, int D, int MODE>
-hipError_t launch_gemm_tile(const GemmArgs& a, int tile, int lds, hipStream_t stream) {
+hipError_t launch_gemm_tile(const GemmArgs& a, int tile, int kg, int lds, hipStream_t stream) {
   constexpr int IW = 2 * gemm_run_bytes<BITS, D>() / 4;
   switch (tile) {
-    case 0: return launch_gemm_variant<BITS, D, MODE, 128, 256, 2, 4, kGemmTiles[0].ns>(a, lds, stream);
+    case 0: return launch_gemm_variant<BITS, D, MODE, 128, 256, 2, 4, kGemmTiles[0].ns, 1>(a, lds, stream);
     case 2:
       if constexpr ((128 * IW) % 256 == 0)
-        return launch_gemm_variant<BITS, D, MODE, 64, 128, 2, 2, kGemmTiles[2].ns>(a, lds, stream);
+        return launch_gemm_groups<BITS, D, MODE, 64, 128, kGemmTiles[2].ns>(a, kg, lds, stream);
       else return hipErrorNotSupported;
     case 3:
       if constexpr ((64 * IW) % 256 == 0)
-        return launch_gemm_variant<BITS, D, MODE, 64, 64, 2, 2, kGemmTiles[3].ns>(a, lds, stream);
+        return launch_gemm_groups<BITS, D, MODE, 64, 64, kGemmTiles[3].ns>(a, kg, lds, stream);
       else return hipErrorNotSupported;
-    default: return launch_gemm_variant<BITS, D, MODE, 128, 128, 2, 2, kGemmTiles[1].ns>(a, lds, stream);
+    default: return launch_gemm_variant<BITS, D, MODE, 128, 128, 2, 2, kGemmTiles[1].ns, 1>(a, lds, stream);
   }
 }
 
 template <int BITS, int D>
-hipError_t launch_gemm_mode(const GemmArgs& a, int mode, int tile, int lds, hipStream_t stream) {
+hipError_t launch_gemm_mode(const GemmArgs& a, int mode, int tile, int kg, int lds, hipStream_t stream) {
   switch (mode) {
-    case CB_REPL: return launch_gemm_tile<BITS, D, CB_REPL>(a, tile, lds, stream);
-    case CB_LDS: return launch_gemm_tile<BITS, D, CB_LDS>(a, tile, lds, stream);
-    default: return launch_gemm_tile<BITS, D, CB_GLOBAL>(a, tile, lds, stream);
+    case CB_REPL: return launch_gemm_tile<BITS, D, CB_REPL>(a, tile, kg, lds, stream);
+    case CB_LDS: return launch_gemm_tile<BITS, D, CB_LDS>(a, tile, kg, lds, stream);
+    default: return launch_gemm_tile<BITS, D, CB_GLOBAL>(a, tile, kg, lds, stream);
   }
 }
 
 template <int BITS>
-hipError_t launch_gemm_bits(const GemmArgs& a, int d, int mode, int tile, int lds, hipStream_t stream) {
+hipError_t launch_gemm_bits(const GemmArgs& a, int d, int mode, int tile, int kg, int lds, hipStream_t stream) {
   switch (d) {
-    case 1: return launch_gemm_mode<BITS, 1>(a, mode, tile, lds, stream);
-    case 2: return launch_gemm_mode<BITS, 2>(a, mode, tile, lds, stream);
-    case 4: return launch_gemm_mode<BITS, 4>(a, mode, tile, lds, stream);
+    case 1: return launch_gemm_mode<BITS, 1>(a, mode, tile, kg, lds, stream);
+    case 2: return launch_gemm_mode<BITS, 2>(a, mode, tile, kg, lds, stream);
+    case 4: return launch_gemm_mode<BITS, 4>(a, mode, tile, kg, lds, stream);
     default:
       if constexpr (BITS == 12) return hipErrorNotSupported;  // 4 ids = 6 bytes: not dword aligned
-      else return launch_gemm_mode<BITS, 8>(a, mode, tile, lds, stream);
+      else return launch_gemm_mode<BITS, 8>(a, mode, tile, kg, lds, stream);
   }
 }
 
@@ -88,24 +103,40 @@ hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t
   const int hb = (32 / d) * p.idx_bits / 8;
   if (hb % 4) return hipErrorNotSupported;
 
-  const int mode = choose_cb_mode(p.C, d);
-  const int cb_bytes = (int)cb_lds_bytes(mode, p.C, d);
-  auto lds_of = [&](int t) {
+  int mode = choose_cb_mode(p.C, d);
+  auto lds_of = [&](int t, int kg, int m) {
     const GemmTileShape& ts = kGemmTiles[t];
-    const int ns = gemm_ring_depth(p.idx_bits, d, ts.bm, ts.bn, gemm_tile_waves(t), ts.ns);
-    return cb_bytes + ns * (ts.bm * 128 + ts.bn * 2 * hb);
+    const int ns = gemm_ring_depth(p.idx_bits, d, ts.bm, ts.bn, gemm_tile_waves(t), gemm_group_ring(kg, ts.ns));
+    const int64_t lds = cb_lds_bytes(m, p.C, d) + (int64_t)kg * ns * (ts.bm * 128 + ts.bn * 2 * hb);
+    const int64_t dump = (int64_t)(kg - 1) * ts.bm * ts.bn * 4;  // accumulators of groups 1 .. kg-1
+    return lds > dump ? lds : dump;
   };
   auto tiles_of = [&](int t) {
     return ((p.M + kGemmTiles[t].bm - 1) / kGemmTiles[t].bm) * ((p.N + kGemmTiles[t].bn - 1) / kGemmTiles[t].bn);
   };
   int tile = -1;
   for (int t = 0; t < kGemmNumTiles && tile < 0; ++t)
-    if (gemm_tile_ok(t, hb) && lds_of(t) <= dev.lds_per_block && 4 * tiles_of(t) >= 3 * (int64_t)dev.num_cus)
+    if (gemm_tile_ok(t, hb) && lds_of(t, 1, mode) <= dev.lds_per_block &&
+        4 * tiles_of(t) >= 3 * (int64_t)dev.num_cus)
       tile = t;
   for (int t = kGemmNumTiles - 1; t >= 0 && tile < 0; --t)
-    if (gemm_tile_ok(t, hb) && lds_of(t) <= dev.lds_per_block) tile = t;
+    if (gemm_tile_ok(t, hb) && lds_of(t, 1, mode) <= dev.lds_per_block) tile = t;
   if (tile < 0) return hipErrorNotSupported;
-  const int lds = lds_of(tile);
+  // K groups for the 64-row tiles: the first count in kGemmSplitGroups that
+  // fits, with the replicated codebook or, failing that, one copy.
+  int kg = 1;
+  if (kGemmTiles[tile].bm == 64) {
+    bool done = false;
+    for (int g : kGemmSplitGroups) {
+      for (int m : {mode, (int)CB_LDS}) {
+        if (m == CB_LDS && mode != CB_REPL && mode != CB_LDS) continue;
+        if (lds_of(tile, g, m) <= dev.lds_per_block) { kg = g; mode = m; done = true; break; }
+      }
+      if (done) break;
+    }
+  }
+  const int lds = (int)lds_of(tile, kg, mode);
+  const int cb_bytes = (int)cb_lds_bytes(mode, p.C, d);
 
   GemmArgs a;
   a.x = static_cast<const half_t*>(p.x);
@@ -119,9 +150,9 @@ hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t
   a.cb_lds_bytes = cb_bytes;
   a.y = static_cast<half_t*>(p.y);
   switch (p.idx_bits) {
-    case 8: return launch_gemm_bits<8>(a, d, mode, tile, lds, stream);
-    case 12: return launch_gemm_bits<12>(a, d, mode, tile, lds, stream);
-    default: return launch_gemm_bits<16>(a, d, mode, tile, lds, stream);
+    case 8: return launch_gemm_bits<8>(a, d, mode, tile, kg, lds, stream);
+    case 12: return launch_gemm_bits<12>(a, d, mode, tile, kg, lds, stream);
+    default: return launch_gemm_bits<16>(a, d, mode, tile, kg, lds, stream);
   }
 }
 

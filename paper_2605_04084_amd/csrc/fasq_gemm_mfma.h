@@ -78,9 +78,14 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-template <int BITS, int D, int MODE, int BM, int BN, int WGM, int WGN, int NS>
-__global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_mfma(GemmArgs a) {
-  constexpr int WAVES = WGM * WGN;
+// KG > 1 splits K inside the workgroup: KG groups of WGM x WGN waves, each
+// with its own ring, take the chunks c = KG * it + kg (group kg, iteration
+// it) of the same output tile, and their accumulators are summed through LDS
+// in group order at the end.  Small grids use it to keep several waves per
+// SIMD busy.
+template <int BITS, int D, int MODE, int BM, int BN, int WGM, int WGN, int NS, int KG>
+__global__ __launch_bounds__(WGM * WGN * KG * 64) void k_gemm_mfma(GemmArgs a) {
+  constexpr int WAVES = WGM * WGN;                 // waves per K group
   constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int FM = WM / 32, FN = WN / 32;
   constexpr int HB = gemm_run_bytes<BITS, D>();    // bytes per lane half per chunk
@@ -98,15 +103,22 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_mfma(GemmArgs a) {
   static_assert(NS >= 3 && LPC * (NS - 2) < 64, "ring depth out of range for vmcnt");
 
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  uint8_t* ring = smem + a.cb_lds_bytes;  // NS stages of [X tile][id tile]
 
   const int tid = threadIdx.x;
-  const int wave = tid / kWave, lane = tid % kWave;
+  // K group and wave index as wave-uniform (scalar) values: a branch on them
+  // is a real jump.  (MFMA ignores the execution mask, so a group's skipped
+  // chunk must not become a masked branch.)
+  const int kg = __builtin_amdgcn_readfirstlane(tid / (WAVES * kWave));
+  const int wave = __builtin_amdgcn_readfirstlane((tid / kWave) % WAVES), lane = tid % kWave;
   const int wm = wave / WGN, wn = wave % WGN;
   const int h = lane >> 5, l32 = lane & 31;
   const int64_t m0 = (int64_t)blockIdx.y * BM;
   const int64_t n0 = (int64_t)blockIdx.x * BN;
   const int nchunks = (int)(a.K / kGemmKC);
+  const int niter = (nchunks + KG - 1) / KG;       // chunks per group (the last ones may lie past K)
+  uint8_t* ring = smem + a.cb_lds_bytes + kg * (NS * SBYTES);  // NS stages of [X tile][id tile]
+  // data chunk of iteration it, clamped into K for the copies
+  auto chunk_of = [&](int it) { const int c = it * KG + kg; return c < nchunks ? c : nchunks - 1; };
 
   // ---- copy sources of this lane (rows >= M read row M - 1, columns >= N
   //      read column 0: they are computed but never stored)
@@ -142,7 +154,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_mfma(GemmArgs a) {
   __syncthreads();
 
 #pragma unroll
-  for (int s = 0; s < NS - 1; ++s) issue(s < nchunks ? s : nchunks - 1, s);
+  for (int s = 0; s < NS - 1; ++s) issue(chunk_of(s), s);
 
   float16_t acc[FM][FN];
 #pragma unroll
@@ -180,7 +192,8 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_mfma(GemmArgs a) {
       o.a[fm] = *reinterpret_cast<const half8_t*>(xb + r * 128 + slot * 16);
     }
   };
-  auto mfma_step = [&](const Ops& o) {
+  auto mfma_step = [&](const Ops& o, bool valid) {
+    if (KG > 1 && !valid) return;  // a group's last chunk past K
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
@@ -201,26 +214,60 @@ __global__ __launch_bounds__(WGM * WGN * 64) void k_gemm_mfma(GemmArgs a) {
   Ops o0, o1, o2, o3;
   read_ops(o0, 0, idc, 0);
   read_ops(o1, 0, idc, 1);
-  for (int c = 0; c < nchunks; ++c) {
+  for (int c = 0; c < niter; ++c) {
     const int stage = c % NS;
-    const bool more = c + 1 < nchunks;
+    const bool more = c + 1 < niter;
+    const bool valid = c * KG + kg < nchunks;
     read_ops(o2, stage, idc, 2);
-    mfma_step(o0);
+    mfma_step(o0, valid);
     read_ops(o3, stage, idc, 3);
-    mfma_step(o1);
+    mfma_step(o1, valid);
     if (more) {
       wait_vmcnt<LPC * (NS - 3)>();  // this wave's copies of chunk c + 1
       __builtin_amdgcn_s_barrier();  // everyone's; nobody reads chunk c - 1 any more
-      const int cn = c + NS - 1 < nchunks ? c + NS - 1 : nchunks - 1;
-      issue(cn, (c + NS - 1) % NS);
+      issue(chunk_of(c + NS - 1 < niter ? c + NS - 1 : niter - 1), (c + NS - 1) % NS);
       read_ids((c + 1) % NS, idc);
       read_ops(o0, (c + 1) % NS, idc, 0);
     }
-    mfma_step(o2);
+    mfma_step(o2, valid);
     if (more) read_ops(o1, (c + 1) % NS, idc, 1);
-    mfma_step(o3);
+    mfma_step(o3, valid);
   }
   wait_vmcnt<0>();  // drain the clamped copies issued past the last chunk
+
+  if constexpr (KG > 1) {
+    // Groups 1 .. KG-1 leave their accumulators in LDS (16-byte vectors,
+    // lanes contiguous), group 0 adds them in group order.
+    float4_t* dump = reinterpret_cast<float4_t*>(smem);
+    auto slot = [&](int g, int fm, int fn, int i4) {
+      return ((((g - 1) * WAVES + wave) * FM + fm) * FN + fn) * 4 * kWave + i4 * kWave + lane;
+    };
+    __syncthreads();  // every group is done with its ring and the codebook
+    if (kg > 0) {
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn)
+#pragma unroll
+          for (int i4 = 0; i4 < 4; ++i4)
+            dump[slot(kg, fm, fn, i4)] = float4_t{acc[fm][fn][4 * i4], acc[fm][fn][4 * i4 + 1],
+                                                  acc[fm][fn][4 * i4 + 2], acc[fm][fn][4 * i4 + 3]};
+    }
+    __syncthreads();
+    if (kg > 0) return;
+    for (int g = 1; g < KG; ++g) {
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn)
+#pragma unroll
+          for (int i4 = 0; i4 < 4; ++i4) {
+            const float4_t v = dump[slot(g, fm, fn, i4)];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) acc[fm][fn][4 * i4 + k] += v[k];
+          }
+    }
+  }
 
   // ---- epilogue: lane l holds rows (i/4)*8 + h*4 + i%4, column l32 of each 32x32 tile
 #pragma unroll

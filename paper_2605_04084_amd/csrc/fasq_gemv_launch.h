@@ -110,6 +110,11 @@ hipError_t launch_gemv_bits(const Problem& p, const DeviceInfo& dev, hipStream_t
   int mode = choose_cb_mode(p.C, d);
   const int xs = (int)(p.M == 1 ? p.K * 2 : p.K * 2 + 16);
   const int64_t x_bytes = p.M * (int64_t)xs;
+  // The replicated table (up to 64 KB) gives way to one copy when it leaves
+  // too little room beside x for one row group's partials.
+  if (mode == CB_REPL &&
+      cb_lds_bytes(CB_REPL, p.C, d) + x_bytes + (int64_t)Q * 16 * p.M * P * 4 > dev.lds_per_block)
+    mode = CB_LDS;
   // A codebook too large for the LDS budget still goes to LDS when all of it
   // fits beside x and the partials of two row groups (one slice, one pass).
   // More passes do not pay here: each pass costs as much as the whole

@@ -190,6 +190,7 @@ RAGGED = [
     (64, 128, 64, 8, 256, 8),
     (130, 256, 257, 4, 4096, 12),
     (33, 64, 50, 1, 256, 8),
+    (16, 4096, 200, 2, 256, 8),         # 16 rows of x leave no room for the replicated table
 ]
 
 
@@ -424,4 +425,43 @@ def test_sliced_codebook_boundaries_bit_exact(case):
     ref = orc.pq_linear(x, idx, bits, d, cb)
     assert np.abs(ref).max() <= 2048
     y = to_np(fasq.pq_gemv(to_dev(x), to_dev(idx), bits, d, to_dev(cb))).astype(np.float64)
+    assert np.array_equal(y, ref)
+
+
+def test_wide_x_takes_the_decode_kernel_with_one_codebook_copy():
+    """M = 16 at K = 4096 keeps the decode kernel: the codebook drops to one
+    LDS copy (mode 1) to make room for x."""
+    assert fasq.plan("gemv", 16, 4096, 4096, 8, 2, 256).startswith("k_gemv<8, 2, ")
+    assert ", 1, 16, " in fasq.plan("gemv", 16, 4096, 4096, 8, 2, 256)
+
+
+# ---------------------------------------------------------------------------
+# Prefill GEMM with K split over two groups of waves inside the workgroup
+# ---------------------------------------------------------------------------
+
+K_GROUPS = [
+    # M, K, N, d, C, bits: small grids (64-row tiles, two K groups); an odd
+    # number of 64-wide K chunks leaves the second group one chunk short
+    (8, 192, 64, 2, 256, 8),
+    (40, 320, 100, 4, 256, 8),
+    (64, 4096 + 64, 130, 4, 4096, 12),
+    (100, 1088, 70, 4, 65536, 16),
+]
+
+
+@pytest.mark.parametrize("case", K_GROUPS)
+def test_gemm_k_groups_one_hot_bit_exact(case):
+    """Exact small-integer results: a chunk summed twice or dropped by a
+    group would show as an exact mismatch."""
+    M, K, N, d, C, bits = case
+    print(f"[case] gemm k groups {case}", flush=True)
+    assert fasq.plan("gemm", M, K, N, bits, d, C).endswith(", 2>")
+    rng = np.random.default_rng(11 + sum(case))
+    cb = pi.signed_one_hot_codebook(C, d, rng)
+    ids = rng.integers(0, C, size=(N, K // d))
+    x = pi.ternary_x(rng, M, K)
+    idx = pi.pack_indices(ids, bits)
+    ref = orc.pq_linear(x, idx, bits, d, cb)
+    assert np.abs(ref).max() <= 2048
+    y = to_np(fasq.pq_gemm(to_dev(x), to_dev(idx), bits, d, to_dev(cb))).astype(np.float64)
     assert np.array_equal(y, ref)
