@@ -66,7 +66,10 @@ typedef enum {
 /*
  * Decode regime (FASQ Sec. 4.1, the batch-1 GEMV of the decode phase):
  * y[M x N] = x[M x K] . W_hat^T.  Tuned for M <= 16 (M = 1 is token-by-token
- * decode); any M >= 1 is accepted and computed correctly.
+ * decode); any M >= 1 is accepted and computed correctly.  This is also the
+ * batch-adaptive entry point the paper leaves to future work (Sec. 4.4,
+ * batch size): rows of x beyond 16, or operands the decode kernels cannot
+ * hold on chip, go to the prefill kernel of fasq_pq_gemm.
  *
  *   x, M, K     activations, fp16 [M x K]
  *   N           output features (rows of the index table)

@@ -290,3 +290,30 @@ def scaled_signed_one_hot_codebook(C: int, d: int, rng: np.random.Generator) -> 
 def ternary_x(rng: np.random.Generator, M: int, K: int) -> np.ndarray:
     """Activations drawn uniformly from {-1, 0, 1}, fp16."""
     return rng.integers(-1, 2, size=(M, K)).astype(np.float16)
+
+
+# ---------------------------------------------------------------------------
+# Encoder inputs: a dense fp16 weight matrix and the starting codebook.  The
+# starting points are random numbers the encoder would otherwise draw, so both
+# the CPU oracle and the GPU encoder receive them as inputs.
+# ---------------------------------------------------------------------------
+
+def draw_weights(rng: np.random.Generator, N: int, K: int, std: float = 0.02) -> np.ndarray:
+    """Dense weights ``N x K`` from N(0, std), rounded to fp16 (a stand-in for a
+    trained layer, whose weights are not available)."""
+    return (rng.standard_normal((N, K)) * std).astype(np.float16)
+
+
+def init_point_ids(rng: np.random.Generator, n_points: int, C: int) -> np.ndarray:
+    """``C`` distinct sub-vector indices in ``[0, n_points)`` (sorted): where
+    k-means starts."""
+    if C > n_points:
+        raise ValueError("more codewords than sub-vectors")
+    return np.sort(rng.choice(n_points, size=C, replace=False)).astype(np.int64)
+
+
+def subvectors_at(w: np.ndarray, d: int, point_ids: np.ndarray) -> np.ndarray:
+    """Sub-vectors ``point_ids`` of ``w`` (point ``n * (K / d) + s`` is
+    ``w[n, s*d:(s+1)*d]``), as an fp16 ``[len(point_ids), d]`` array (a copy)."""
+    N, K = w.shape
+    return np.ascontiguousarray(w.reshape(N * (K // d), d)[point_ids])
