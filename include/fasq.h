@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define FASQ_ABI_VERSION 2
+#define FASQ_ABI_VERSION 3
 
 typedef enum {
   FASQ_OK = 0,
@@ -125,6 +125,48 @@ fasq_status fasq_pq_gemm(const void* x, int64_t M, int64_t K, int64_t N,
                          const void* idx, int idx_bits, int d,
                          const void* codebook, int64_t C,
                          void* y, hipStream_t stream);
+
+/*
+ * Calibration-free PQ encoding of one weight matrix (FASQ Sec. 3.1.1, Alg. 1):
+ * Lloyd's k-means over the N * K / d sub-vectors of w, with one codebook of C
+ * codewords shared by every subspace (the format the matmul entry points
+ * consume).  No calibration data: only the weights.
+ *
+ *   w              fp16 [N x K], row-major; sub-vector p = n * (K / d) + s is
+ *                  w[n, s*d : (s+1)*d]; finite, |w| < 128 (unchecked)
+ *   d, C, idx_bits sub-vector length (1 <= d <= 16), codewords, id width
+ *   init_codebook  fp16 [C x d], the starting codewords (for example C
+ *                  distinct sub-vectors of w chosen at random); may be the
+ *                  same buffer as `codebook`
+ *   iters          Lloyd iterations (assignment, then update), >= 0
+ *   codebook       out: fp16 [C x d], the codewords after `iters` updates
+ *   idx            out: N rows of fasq_idx_row_bytes(K, d, idx_bits) bytes,
+ *                  the nearest codeword of every sub-vector under the final
+ *                  codebook, in the packed format of fasq_pq_gemv
+ *   workspace      device scratch of at least
+ *                  fasq_pq_encode_workspace_bytes(N, K, d, C) bytes, 8-byte
+ *                  aligned; its contents are overwritten
+ *
+ * Arithmetic (the paper leaves it open): squared distances in fp32, summed
+ * over the d components in order without fused multiply-add, the lowest index
+ * winning a tie; cluster sums formed exactly (every fp16 value is a multiple
+ * of 2^-24), the mean divided out in fp64 and rounded to fp16 (nearest, ties
+ * to even); an empty cluster keeps its codeword.  The result does not depend
+ * on scheduling: repeated calls give identical bits.
+ *
+ * Asynchronous on `stream`; the caller owns every buffer.  Returns
+ * FASQ_ERR_INVALID_ARG (sizes; d does not divide K; idx_bits not in
+ * {8, 12, 16}; C outside [1, 2^idx_bits]; iters < 0; a NULL or misaligned
+ * pointer; a workspace that is too small), FASQ_ERR_UNSUPPORTED (d > 16) or
+ * FASQ_ERR_HIP.
+ */
+fasq_status fasq_pq_encode(const void* w, int64_t N, int64_t K, int d, int64_t C, int idx_bits,
+                           const void* init_codebook, int iters, void* codebook, void* idx,
+                           void* workspace, int64_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes fasq_pq_encode needs for these sizes; -1 if they are invalid
+ * (N, K < 1; d does not divide K; C outside [1, 65536]). */
+int64_t fasq_pq_encode_workspace_bytes(int64_t N, int64_t K, int d, int64_t C);
 
 /*
  * Decode W_hat explicitly (the reconstruction the paper's reconstruction-free

@@ -58,13 +58,14 @@ def points_of(w: np.ndarray, d: int) -> np.ndarray:
     return w.reshape(N * (K // d), d)
 
 
-def assign(points: np.ndarray, codebook: np.ndarray, block: int = 1 << 16) -> np.ndarray:
+def assign(points: np.ndarray, codebook: np.ndarray) -> np.ndarray:
     """Nearest codeword of every point (fp32 squared distance, lowest index on
     ties), as uint32 ``[P]``."""
     pts = np.asarray(points).astype(np.float32)
     cb = np.asarray(codebook).astype(np.float32)
     P, d = pts.shape
     C = cb.shape[0]
+    block = max(1, (1 << 24) // C)  # points per block: bounds the [block, C] distance table
     out = np.empty(P, dtype=np.uint32)
     for b0 in range(0, P, block):
         p = pts[b0:b0 + block]

@@ -8,6 +8,8 @@ there is no fallback.
 Operation (FASQ, Sec. 3.1.2, Eq. lut-accumulate): ``y = x . W_hat^T`` where
 ``W_hat[n, s*d + i] = codebook[u(n, s), i]`` and ``u(n, s)`` are packed ids
 (8, 12 or 16 bits, one least-significant-bit-first stream per output row).
+The encoder (Sec. 3.1.1, Alg. 1) produces the codebook and the ids from dense
+weights by k-means.
 """
 
 from __future__ import annotations
@@ -32,6 +34,9 @@ __all__ = [
     "pq_gemm",
     "pq_reconstruct",
     "pq_gemv_batched",
+    "pq_encode",
+    "encode_raw",
+    "encode_workspace_bytes",
     "gemv_raw",
     "gemv_batched_raw",
     "gemm_raw",
@@ -46,7 +51,7 @@ __all__ = [
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfasq.so")
 
-ABI_VERSION = 2  # FASQ_ABI_VERSION of include/fasq.h
+ABI_VERSION = 3  # FASQ_ABI_VERSION of include/fasq.h
 
 FASQ_OK = 0
 FASQ_ERR_INVALID_ARG = 1
@@ -63,6 +68,8 @@ EXPORTED_SYMBOLS = (
     "fasq_last_error",
     "fasq_abi_version",
     "fasq_pq_plan",
+    "fasq_pq_encode",
+    "fasq_pq_encode_workspace_bytes",
 )
 
 
@@ -117,6 +124,11 @@ def lib() -> ctypes.CDLL:
         L.fasq_abi_version.restype = _c_int
         L.fasq_pq_plan.argtypes = [_c_int, _c_i64, _c_i64, _c_i64, _c_int, _c_int, _c_i64]
         L.fasq_pq_plan.restype = ctypes.c_char_p
+        L.fasq_pq_encode.argtypes = [_c_vp, _c_i64, _c_i64, _c_int, _c_i64, _c_int, _c_vp, _c_int, _c_vp, _c_vp,
+                                     _c_vp, _c_i64, _c_vp]
+        L.fasq_pq_encode.restype = _c_int
+        L.fasq_pq_encode_workspace_bytes.argtypes = [_c_i64, _c_i64, _c_int, _c_i64]
+        L.fasq_pq_encode_workspace_bytes.restype = _c_i64
         _lib = L
         return L
 
@@ -307,3 +319,45 @@ def pq_reconstruct(idx, K: int, idx_bits: int, d: int, codebook, out=None):
         _check(lib().fasq_pq_reconstruct(idx.data_ptr(), N, K, idx_bits, d, codebook.data_ptr(), C,
                                          out.data_ptr(), _stream_handle(idx)))
     return out
+
+
+def encode_workspace_bytes(N: int, K: int, d: int, C: int) -> int:
+    return lib().fasq_pq_encode_workspace_bytes(N, K, d, C)
+
+
+def encode_raw(w, N, K, d, C, idx_bits, init_codebook, iters, codebook, idx, workspace, workspace_bytes,
+               stream=0) -> int:
+    return lib().fasq_pq_encode(w, N, K, d, C, idx_bits, init_codebook, iters, codebook, idx, workspace,
+                                workspace_bytes, stream)
+
+
+def pq_encode(w, d: int, idx_bits: int, init_codebook, iters: int, workspace=None):
+    """k-means PQ encoding of dense fp16 weights ``w`` [N x K] with the
+    starting codebook ``init_codebook`` (fp16 [C x d]); see ``fasq_pq_encode``.
+    Returns ``(codebook, idx)``: fp16 [C x d] and uint8 [N x R] device tensors."""
+    torch = _torch()
+    _require(w, "w", torch.float16, 2)
+    _require(init_codebook, "init_codebook", torch.float16, 2)
+    N, K = w.shape
+    C, dd = init_codebook.shape
+    if dd != d:
+        raise ValueError(f"init_codebook is [C x {dd}] but d = {d}")
+    R = idx_row_bytes(K, d, idx_bits)
+    if R < 0:
+        raise ValueError("invalid (K, d, idx_bits)")
+    need = encode_workspace_bytes(N, K, d, C)
+    if need < 0:
+        raise ValueError("invalid encoder sizes")
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=w.device)
+    elif not (workspace.is_cuda and workspace.is_contiguous() and workspace.numel() * workspace.element_size() >= need):
+        raise ValueError(f"workspace must be a contiguous device tensor of at least {need} bytes")
+    if init_codebook.device != w.device or workspace.device != w.device:
+        raise ValueError("all tensors must be on one device")
+    codebook = torch.empty((C, d), dtype=torch.float16, device=w.device)
+    idx = torch.empty((N, R), dtype=torch.uint8, device=w.device)
+    with torch.cuda.device(w.device):
+        _check(encode_raw(w.data_ptr(), N, K, d, C, idx_bits, init_codebook.data_ptr(), iters, codebook.data_ptr(),
+                          idx.data_ptr(), workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                          _stream_handle(w)))
+    return codebook, idx

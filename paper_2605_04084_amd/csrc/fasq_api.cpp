@@ -250,6 +250,55 @@ const char* fasq_last_error(void) { return fasq::t_last_error.c_str(); }
 
 int fasq_abi_version(void) { return FASQ_ABI_VERSION; }
 
+int64_t fasq_pq_encode_workspace_bytes(int64_t N, int64_t K, int d, int64_t C) {
+  if (N < 1 || K < 1 || d < 1 || K % d != 0 || C < 1 || C > (int64_t(1) << 16)) return -1;
+  if (N > (int64_t(1) << 40) / K) return -1;
+  return fasq::encode_workspace_bytes(N, K, d, C);
+}
+
+fasq_status fasq_pq_encode(const void* w, int64_t N, int64_t K, int d, int64_t C, int idx_bits,
+                           const void* init_codebook, int iters, void* codebook, void* idx, void* workspace,
+                           int64_t workspace_bytes, hipStream_t stream) {
+  using fasq::fail;
+  if (N < 1 || K < 1) return fail(FASQ_ERR_INVALID_ARG, "N and K must be >= 1");
+  if (d < 1) return fail(FASQ_ERR_INVALID_ARG, "d must be >= 1");
+  if (K % d != 0) return fail(FASQ_ERR_INVALID_ARG, "K must be a multiple of d");
+  if (idx_bits != 8 && idx_bits != 12 && idx_bits != 16)
+    return fail(FASQ_ERR_INVALID_ARG, "idx_bits must be 8, 12 or 16");
+  if (C < 1 || C > (int64_t(1) << idx_bits)) return fail(FASQ_ERR_INVALID_ARG, "C must lie in [1, 2^idx_bits]");
+  if (iters < 0) return fail(FASQ_ERR_INVALID_ARG, "iters must be >= 0");
+  if (w == nullptr || init_codebook == nullptr || codebook == nullptr || idx == nullptr || workspace == nullptr)
+    return fail(FASQ_ERR_INVALID_ARG, "a buffer pointer is NULL");
+  if (N > (int64_t(1) << 40) / K) return fail(FASQ_ERR_INVALID_ARG, "problem too large");
+  if ((reinterpret_cast<uintptr_t>(w) | reinterpret_cast<uintptr_t>(init_codebook) |
+       reinterpret_cast<uintptr_t>(codebook)) & 1)
+    return fail(FASQ_ERR_INVALID_ARG, "fp16 buffers must be 2-byte aligned");
+  if (reinterpret_cast<uintptr_t>(workspace) & 7) return fail(FASQ_ERR_INVALID_ARG, "workspace must be 8-byte aligned");
+  if (workspace_bytes < fasq::encode_workspace_bytes(N, K, d, C))
+    return fail(FASQ_ERR_INVALID_ARG, "workspace smaller than fasq_pq_encode_workspace_bytes()");
+  if (d > 16) return fail(FASQ_ERR_UNSUPPORTED, "the encoder handles d <= 16");
+  fasq::DeviceInfo dev;
+  hipError_t e = fasq::device_info(&dev);
+  if (e != hipSuccess) return fasq::hip_fail("querying the current device", e);
+  fasq::EncodeProblem ep;
+  ep.w = w;
+  ep.N = N;
+  ep.K = K;
+  ep.d = d;
+  ep.C = C;
+  ep.idx_bits = idx_bits;
+  ep.R = (K / d * idx_bits + 7) / 8;
+  ep.init = init_codebook;
+  ep.iters = iters;
+  ep.codebook = codebook;
+  ep.idx = idx;
+  ep.workspace = workspace;
+  e = fasq::launch_encode(ep, dev, stream);
+  if (e != hipSuccess) return fasq::hip_fail("kernel launch", e);
+  fasq::t_last_error.clear();
+  return FASQ_OK;
+}
+
 const char* fasq_pq_plan(int regime, int64_t M, int64_t K, int64_t N, int idx_bits, int d, int64_t C) {
   // Placeholder, suitably aligned, never dereferenced: nothing is launched.
   const void* fake = reinterpret_cast<const void*>(uintptr_t(1) << 20);

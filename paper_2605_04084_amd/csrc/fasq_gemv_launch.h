@@ -13,28 +13,6 @@ constexpr int kSliceReserve = 8 * 1024;        // LDS kept for row partials besi
 constexpr int kMinSliceBytes = 32 * 1024;      // smaller slices: gather from global memory instead
 static_assert(kM1MaxMats == kMaxBatchLaunch, "grouped launches and their kernel disagree on the group size");
 
-// Once per device and kernel: check that the kernel declares no static LDS
-// (its LDS-resident codebook is addressed from LDS address 0) and raise its
-// dynamic-LDS limit to the 160 KB a gfx950 CU offers.  One bit per device
-// ordinal; ordinals >= 64 repeat the set-up on every call.
-template <typename K>
-hipError_t prepare_kernel(K kernel) {
-  static std::atomic<uint64_t> done{0};
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return e;
-  const uint64_t bit = dev < 64 ? (uint64_t(1) << dev) : 0;
-  if (bit && (done.load(std::memory_order_acquire) & bit)) return hipSuccess;
-  hipFuncAttributes attr;
-  e = hipFuncGetAttributes(&attr, reinterpret_cast<const void*>(kernel));
-  if (e != hipSuccess) return e;
-  if (attr.sharedSizeBytes != 0) return hipErrorInvalidDeviceFunction;
-  e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
-                          160 * 1024);
-  if (e == hipSuccess && bit) done.fetch_or(bit, std::memory_order_acq_rel);
-  return e;
-}
-
 // Codebook placement for a call: replicated in LDS when the replicated table
 // fits the budget, one copy in LDS when that fits, else global memory.
 inline int choose_cb_mode(int64_t C, int d) {

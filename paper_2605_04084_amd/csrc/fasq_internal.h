@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
 #include <initializer_list>
 
 namespace fasq {
@@ -46,6 +47,45 @@ constexpr int kMaxBatchLaunch = 8;  // matrices per grouped launch
 
 // Tuned MFMA prefill kernel.  hipErrorNotSupported when no variant applies.
 hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
+
+// Once per device and kernel: check that the kernel declares no static LDS
+// (its LDS-resident codebook is addressed from LDS address 0) and raise its
+// dynamic-LDS limit to the 160 KB a gfx950 CU offers.  One bit per device
+// ordinal; ordinals >= 64 repeat the set-up on every call.
+template <typename K>
+hipError_t prepare_kernel(K kernel) {
+  static std::atomic<uint64_t> done{0};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const uint64_t bit = dev < 64 ? (uint64_t(1) << dev) : 0;
+  if (bit && (done.load(std::memory_order_acquire) & bit)) return hipSuccess;
+  hipFuncAttributes attr;
+  e = hipFuncGetAttributes(&attr, reinterpret_cast<const void*>(kernel));
+  if (e != hipSuccess) return e;
+  if (attr.sharedSizeBytes != 0) return hipErrorInvalidDeviceFunction;
+  e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                          160 * 1024);
+  if (e == hipSuccess && bit) done.fetch_or(bit, std::memory_order_acq_rel);
+  return e;
+}
+
+// Calibration-free encoding of one weight matrix (validated arguments).
+struct EncodeProblem {
+  const void* w;  // fp16 [N x K]
+  int64_t N, K;
+  int d;
+  int64_t C;
+  int idx_bits;
+  int64_t R;             // bytes per packed id row
+  const void* init;      // fp16 [C x d]
+  int iters;
+  void* codebook;        // fp16 [C x d] out
+  void* idx;             // packed ids out
+  void* workspace;
+};
+int64_t encode_workspace_bytes(int64_t N, int64_t K, int d, int64_t C);
+hipError_t launch_encode(const EncodeProblem& e, const DeviceInfo& dev, hipStream_t stream);
 
 // Planning mode (per thread): while active, launchers record the name of the
 // kernel instantiation they would launch instead of launching it.

@@ -145,3 +145,42 @@ def test_batched_null_arrays_rejected(L):
 def test_batched_binding_checks_lengths(L):
     with pytest.raises(ValueError):
         fasq.gemv_batched_raw(DUMMY, 1, 16, [DUMMY], [4, 4], [DUMMY], [16], [DUMMY], 8, 2)
+
+
+# ---------------------------------------------------------------------------
+# Encoder entry points: validation before any HIP call
+# ---------------------------------------------------------------------------
+
+def test_encode_workspace_bytes(L):
+    # [C x d] int64 sums and [C] int64 counts (256-byte aligned), then one uint32 id per sub-vector
+    assert fasq.encode_workspace_bytes(4, 16, 2, 256) == 256 * 3 * 8 + 4 * 8 * 4
+    assert fasq.encode_workspace_bytes(4, 16, 3, 4) == -1
+    assert fasq.encode_workspace_bytes(0, 16, 2, 4) == -1
+    assert fasq.encode_workspace_bytes(4, 16, 2, 70000) == -1
+
+
+@pytest.mark.parametrize("args,why,status", [
+    (dict(N=0), "N and K", 1),
+    (dict(d=0), "d must", 1),
+    (dict(K=10, d=4), "multiple of d", 1),
+    (dict(idx_bits=9), "idx_bits", 1),
+    (dict(C=257), "C must", 1),
+    (dict(iters=-1), "iters", 1),
+    (dict(w=0), "NULL", 1),
+    (dict(init=0), "NULL", 1),
+    (dict(cb=0), "NULL", 1),
+    (dict(idx=0), "NULL", 1),
+    (dict(ws=0), "NULL", 1),
+    (dict(w=DUMMY + 1), "aligned", 1),
+    (dict(ws=DUMMY + 4), "aligned", 1),
+    (dict(ws_bytes=16), "workspace smaller", 1),
+    (dict(K=34, d=17, ws_bytes=1 << 20), "d <= 16", 2),
+])
+def test_encode_invalid_arguments_rejected_without_launch(L, args, why, status):
+    a = dict(w=DUMMY, N=4, K=16, d=2, C=256, idx_bits=8, init=DUMMY, iters=2, cb=DUMMY, idx=DUMMY, ws=DUMMY,
+             ws_bytes=1 << 20)
+    a.update(args)
+    st = fasq.encode_raw(a["w"], a["N"], a["K"], a["d"], a["C"], a["idx_bits"], a["init"], a["iters"], a["cb"],
+                         a["idx"], a["ws"], a["ws_bytes"], 0)
+    assert st == status
+    assert why in fasq.last_error()

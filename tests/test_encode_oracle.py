@@ -177,7 +177,7 @@ def test_rejects_out_of_range_weights():
 # Planted mistakes: a broken oracle must fail the pins above
 # ---------------------------------------------------------------------------
 
-def _ties_to_highest(points, codebook, block=1 << 16):
+def _ties_to_highest(points, codebook):
     pts = np.asarray(points).astype(np.float32)
     cb = np.asarray(codebook).astype(np.float32)
     acc = np.zeros((pts.shape[0], cb.shape[0]), np.float32)
