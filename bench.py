@@ -486,6 +486,47 @@ def sensitivity(torch, fasq, pi):
     return out
 
 
+def encode_timing(torch, fasq, pi, N=4096, K=4096, d=2, C=256, bits=8):
+    """The k-means encoder (fasq_pq_encode) on one dense 4096 x 4096 fp16
+    matrix: seconds per Lloyd iteration, from the difference between 10 and 2
+    iterations; and the CPU oracle's rate on a 256-row sample."""
+    from oracle import pq_encode as enc
+
+    rng = np.random.default_rng(2027)
+    w_h = pi.draw_weights(rng, N, K)
+    init_h = pi.subvectors_at(w_h, d, pi.init_point_ids(rng, N * K // d, C))
+    dev = torch.device("cuda:0")
+    w, init = torch.from_numpy(w_h).to(dev), torch.from_numpy(init_h).to(dev)
+    ws = torch.empty(fasq.encode_workspace_bytes(N, K, d, C), dtype=torch.uint8, device=dev)
+    fasq.pq_encode(w, d, bits, init, 1, workspace=ws)
+    torch.cuda.synchronize()
+
+    def run(iters):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fasq.pq_encode(w, d, bits, init, iters, workspace=ws)
+        e1.record()
+        e1.synchronize()
+        return e0.elapsed_time(e1) * 1e-3
+
+    per = float(np.median([(run(10) - run(2)) / 8 for _ in range(3)]))
+    total = run(10)
+    P = N * K // d
+    rows = 256
+    t0 = time.perf_counter()
+    enc.kmeans_encode(w_h[:rows], d, init_h, 2)
+    cpu = time.perf_counter() - t0
+    out = dict(shape=f"{N}x{K}", d=d, C=C, idx_bits=bits, points=P, s_per_iteration=per, s_10_iterations=total,
+               distance_evals_per_s=P * C / per,
+               cpu_oracle=dict(rows=rows, iterations=2, seconds=cpu,
+                               points_iterations_per_s=rows * (K // d) * 3 / cpu))
+    log(f"[bench] encode {N}x{K} d={d} C={C}: {per * 1e3:.3f} ms per Lloyd iteration, {total * 1e3:.2f} ms for 10 "
+        f"({P * C / per / 1e12:.2f} T distance evaluations/s); CPU oracle {rows} rows x 2 iterations: {cpu:.2f} s")
+    del w, init, ws
+    torch.cuda.empty_cache()
+    return out
+
+
 def dense_gemm_seconds(torch, x, w, reps, short, long):
     """Per-call time of torch.matmul(x, w) (fp16, rocBLAS/hipBLASLt), timed
     like the PQ GEMM: differential over back-to-back calls."""
@@ -605,6 +646,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-extra", action="store_true", help="only the effective-4-bit decode layer")
     ap.add_argument("--per-matrix", action="store_true", help="add the 4-bit layer with one launch per matrix")
+    ap.add_argument("--encode", action="store_true", help="add the k-means encoder timing on one 4096x4096 matrix")
     ap.add_argument("--sensitivity", action="store_true",
                     help="add the codebook-size, sub-vector, batch and prefill-length sweeps on one 4096x4096 layer")
     ap.add_argument("--out", default=None, help="also write the JSON record to this file")
@@ -679,6 +721,8 @@ def main():
 
     if args.sensitivity:
         extra["sensitivity"] = sensitivity(torch, fasq, pi)
+    if args.encode:
+        extra["encode"] = encode_timing(torch, fasq, pi)
 
     cpu = None
     if not args.no_cpu:
