@@ -127,6 +127,36 @@ fasq_status fasq_pq_gemm(const void* x, int64_t M, int64_t K, int64_t N,
                          void* y, hipStream_t stream);
 
 /*
+ * Decode regime with the paper's general codebook layout (FASQ Sec. 3.1.1:
+ * T_cluster is [N_ss x K_s x SZ_ss], one codebook per subspace; Eq.
+ * lut-accumulate):
+ *
+ *   y[m, n] = sum_s dot(x[m, s*d : (s+1)*d], codebook[s * cb_stride + u(n, s) * d .. + d])
+ *
+ *   cb_stride  0: one codebook [C x d] shared by every subspace (exactly
+ *              fasq_pq_gemv); C * d: one codebook per subspace, the S = K / d
+ *              books back to back, fp16 [S x C x d].  Other values are invalid.
+ *   workspace  device scratch of at least fasq_pq_gemv_ex_workspace_bytes()
+ *              bytes (4-byte aligned; NULL when that is 0), for the fp32
+ *              partial sums of the K split; contents are overwritten
+ *
+ * Other arguments, layouts and errors as fasq_pq_gemv.  With per-subspace
+ * books and M = 1 the tuned kernel splits K over workgroups whose books fit
+ * in LDS and adds the partials in a fixed order (deterministic); other shapes,
+ * or a workspace that is too small, take the general kernel.
+ */
+fasq_status fasq_pq_gemv_ex(const void* x, int64_t M, int64_t K, int64_t N,
+                            const void* idx, int idx_bits, int d,
+                            const void* codebook, int64_t C, int64_t cb_stride,
+                            void* y, void* workspace, int64_t workspace_bytes,
+                            hipStream_t stream);
+
+/* Workspace bytes the tuned per-subspace kernel of fasq_pq_gemv_ex needs on
+ * the current device (0 when no workspace is used), -1 for invalid sizes. */
+int64_t fasq_pq_gemv_ex_workspace_bytes(int64_t M, int64_t K, int64_t N, int idx_bits, int d,
+                                        int64_t C, int64_t cb_stride);
+
+/*
  * Calibration-free PQ encoding of one weight matrix (FASQ Sec. 3.1.1, Alg. 1):
  * Lloyd's k-means over the N * K / d sub-vectors of w, with one codebook of C
  * codewords shared by every subspace (the format the matmul entry points

@@ -35,6 +35,9 @@ __all__ = [
     "pq_reconstruct",
     "pq_gemv_batched",
     "pq_encode",
+    "pq_gemv_ex",
+    "gemv_ex_raw",
+    "gemv_ex_workspace_bytes",
     "encode_raw",
     "encode_workspace_bytes",
     "gemv_raw",
@@ -70,6 +73,8 @@ EXPORTED_SYMBOLS = (
     "fasq_pq_plan",
     "fasq_pq_encode",
     "fasq_pq_encode_workspace_bytes",
+    "fasq_pq_gemv_ex",
+    "fasq_pq_gemv_ex_workspace_bytes",
 )
 
 
@@ -129,6 +134,11 @@ def lib() -> ctypes.CDLL:
         L.fasq_pq_encode.restype = _c_int
         L.fasq_pq_encode_workspace_bytes.argtypes = [_c_i64, _c_i64, _c_int, _c_i64]
         L.fasq_pq_encode_workspace_bytes.restype = _c_i64
+        L.fasq_pq_gemv_ex.argtypes = [_c_vp, _c_i64, _c_i64, _c_i64, _c_vp, _c_int, _c_int, _c_vp, _c_i64, _c_i64,
+                                      _c_vp, _c_vp, _c_i64, _c_vp]
+        L.fasq_pq_gemv_ex.restype = _c_int
+        L.fasq_pq_gemv_ex_workspace_bytes.argtypes = [_c_i64, _c_i64, _c_i64, _c_int, _c_int, _c_i64, _c_i64]
+        L.fasq_pq_gemv_ex_workspace_bytes.restype = _c_i64
         _lib = L
         return L
 
@@ -361,3 +371,58 @@ def pq_encode(w, d: int, idx_bits: int, init_codebook, iters: int, workspace=Non
                           idx.data_ptr(), workspace.data_ptr(), workspace.numel() * workspace.element_size(),
                           _stream_handle(w)))
     return codebook, idx
+
+
+def gemv_ex_workspace_bytes(M: int, K: int, N: int, idx_bits: int, d: int, C: int, cb_stride: int) -> int:
+    return lib().fasq_pq_gemv_ex_workspace_bytes(M, K, N, idx_bits, d, C, cb_stride)
+
+
+def gemv_ex_raw(x, M, K, N, idx, idx_bits, d, codebook, C, cb_stride, y, workspace, workspace_bytes, stream=0) -> int:
+    return lib().fasq_pq_gemv_ex(x, M, K, N, idx, idx_bits, d, codebook, C, cb_stride, y, workspace,
+                                 workspace_bytes, stream)
+
+
+def pq_gemv_ex(x, idx, idx_bits: int, d: int, codebook, out=None, workspace=None):
+    """Decode-regime ``y = x . W_hat^T`` with per-subspace codebooks
+    (``codebook`` fp16 [S x C x d]) or one shared codebook ([C x d]); see
+    ``fasq_pq_gemv_ex``."""
+    torch = _torch()
+    _require(x, "x", torch.float16, 2)
+    _require(idx, "idx", torch.uint8, 2)
+    if not isinstance(codebook, torch.Tensor) or codebook.dim() not in (2, 3):
+        raise ValueError("codebook must be [C x d] or [S x C x d]")
+    _require(codebook, "codebook", torch.float16, codebook.dim())
+    M, K = x.shape
+    N, R = idx.shape
+    if codebook.shape[-1] != d:
+        raise ValueError(f"codebook entries have {codebook.shape[-1]} values but d = {d}")
+    C = codebook.shape[-2]
+    if codebook.dim() == 3:
+        if codebook.shape[0] != K // d:
+            raise ValueError(f"per-subspace codebook has {codebook.shape[0]} books, expected K / d = {K // d}")
+        stride = C * d
+    else:
+        stride = 0
+    want = idx_row_bytes(K, d, idx_bits)
+    if want < 0 or R != want:
+        raise ValueError(f"idx rows are {R} bytes, expected {want}")
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float16, device=x.device)
+    else:
+        _require(out, "out", torch.float16, 2)
+        if tuple(out.shape) != (M, N):
+            raise ValueError("out must be [M x N]")
+    need = gemv_ex_workspace_bytes(M, K, N, idx_bits, d, C, stride)
+    if need < 0:
+        raise ValueError("invalid sizes")
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
+    ws_ptr = workspace.data_ptr() if workspace is not None else 0
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    for t in (idx, codebook, out):
+        if t.device != x.device:
+            raise ValueError("all tensors must be on one device")
+    with torch.cuda.device(x.device):
+        _check(gemv_ex_raw(x.data_ptr(), M, K, N, idx.data_ptr(), idx_bits, d, codebook.data_ptr(), C, stride,
+                           out.data_ptr(), ws_ptr, ws_bytes, _stream_handle(x)))
+    return out

@@ -250,6 +250,40 @@ const char* fasq_last_error(void) { return fasq::t_last_error.c_str(); }
 
 int fasq_abi_version(void) { return FASQ_ABI_VERSION; }
 
+int64_t fasq_pq_gemv_ex_workspace_bytes(int64_t M, int64_t K, int64_t N, int idx_bits, int d, int64_t C,
+                                        int64_t cb_stride) {
+  const void* fake = reinterpret_cast<const void*>(uintptr_t(1) << 20);
+  if (fasq::validate(M, K, N, idx_bits, d, C, fake, fake, fake, fake, true) != FASQ_OK) return -1;
+  if (cb_stride != 0 && cb_stride != C * d) return -1;
+  Problem p = fasq::make_problem(fake, M, K, N, fake, idx_bits, d, fake, C, const_cast<void*>(fake));
+  p.cb_stride = cb_stride;
+  fasq::DeviceInfo dev;
+  if (fasq::device_info(&dev) != hipSuccess) return -1;
+  return fasq::gemv_sub_workspace_bytes(p, dev);
+}
+
+fasq_status fasq_pq_gemv_ex(const void* x, int64_t M, int64_t K, int64_t N, const void* idx, int idx_bits, int d,
+                            const void* codebook, int64_t C, int64_t cb_stride, void* y, void* workspace,
+                            int64_t workspace_bytes, hipStream_t stream) {
+  fasq_status s = fasq::validate(M, K, N, idx_bits, d, C, x, idx, codebook, y, true);
+  if (s != FASQ_OK) return s;
+  if (cb_stride != 0 && cb_stride != C * d)
+    return fasq::fail(FASQ_ERR_INVALID_ARG, "cb_stride must be 0 (one shared codebook) or C * d (one per subspace)");
+  if (workspace_bytes < 0) return fasq::fail(FASQ_ERR_INVALID_ARG, "workspace_bytes must be >= 0");
+  Problem p = fasq::make_problem(x, M, K, N, idx, idx_bits, d, codebook, C, y);
+  if (cb_stride == 0) return fasq::run(p, fasq::Regime::kGemv, stream);
+  p.cb_stride = cb_stride;
+  fasq::DeviceInfo dev;
+  hipError_t e = fasq::device_info(&dev);
+  if (e != hipSuccess) return fasq::hip_fail("querying the current device", e);
+  e = hipErrorNotSupported;
+  if (!fasq::force_generic()) e = fasq::launch_gemv_sub(p, workspace, workspace_bytes, dev, stream);
+  if (e == hipErrorNotSupported) e = fasq::launch_generic(p, stream);
+  if (e != hipSuccess) return fasq::hip_fail("kernel launch", e);
+  fasq::t_last_error.clear();
+  return FASQ_OK;
+}
+
 int64_t fasq_pq_encode_workspace_bytes(int64_t N, int64_t K, int d, int64_t C) {
   if (N < 1 || K < 1 || d < 1 || K % d != 0 || C < 1 || C > (int64_t(1) << 16)) return -1;
   if (N > (int64_t(1) << 40) / K) return -1;

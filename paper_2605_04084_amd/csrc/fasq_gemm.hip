@@ -92,6 +92,7 @@ hipError_t launch_gemm_bits(const GemmArgs& a, int d, int mode, int tile, int kg
 
 hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t stream) {
   const int d = p.d;
+  if (p.cb_stride != 0) return hipErrorNotSupported;
   if (!(d == 1 || d == 2 || d == 4 || d == 8)) return hipErrorNotSupported;
   if (p.idx_bits == 12 && d == 8) return hipErrorNotSupported;
   if (p.K % kGemmKC) return hipErrorNotSupported;

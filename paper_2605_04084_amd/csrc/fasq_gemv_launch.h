@@ -64,6 +64,7 @@ hipError_t launch_gemv_bits(const Problem& p, const DeviceInfo& dev, hipStream_t
   constexpr int CBY = Chunk<BITS>::DW * 4;
   const int d = p.d;
   if (MR == 1 ? p.M != 1 : (p.M < 2 || p.M > 16)) return hipErrorNotSupported;
+  if (p.cb_stride != 0) return hipErrorNotSupported;
   if (!(d == 1 || d == 2 || d == 4 || d == 8)) return hipErrorNotSupported;
   if (p.S % G || p.K % 8) return hipErrorNotSupported;
   const int64_t CH = p.S / G;
@@ -210,6 +211,7 @@ hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& d
   for (int i = 0; i < count; ++i) {
     const Problem& pi = ps[i];
     if (pi.M != 1 || pi.K != p.K || pi.d != d || pi.idx_bits != p.idx_bits || pi.x != p.x) return hipErrorNotSupported;
+    if (pi.cb_stride != 0) return hipErrorNotSupported;
     if (pi.N * pi.R >= (int64_t(1) << 32)) return hipErrorNotSupported;
     if ((reinterpret_cast<uintptr_t>(pi.idx) & (CBY == 16 ? 15 : 3)) || (reinterpret_cast<uintptr_t>(pi.codebook) & 15))
       return hipErrorNotSupported;

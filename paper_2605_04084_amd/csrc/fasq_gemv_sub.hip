@@ -1,0 +1,274 @@
+// Decode GEMV with one codebook per subspace (FASQ Sec. 3.1.1, Eq.
+// lut-accumulate with its per-subspace tables; Sec. 4.1 splits the subspaces
+// over blocks the same way), one token (M = 1).
+//
+//   y[n] = sum_s dot(x[s*d : (s+1)*d], codebook_s[u(n, s)])
+//
+// The books of all subspaces (S x C x d fp16, 2 MB for a 4096-wide layer at
+// d = 2, C = 256) do not fit in LDS, so K is split over workgroups: workgroup
+// (row block rb, segment ks) stages the books of the NCH * G subspaces of its
+// segment (up to 144 KB) into LDS once, then streams the id segments of its
+// rows.  Lane l of a wave-wide load holds chunk l % NCH (G ids, 16 or 12
+// bytes) of row l / NCH of the segment, so one load reads 64 / NCH rows of
+// NCH * 16 contiguous bytes.  The lane gathers each codeword from the book of
+// its subspace and accumulates the dot products with x in fp32; the NCH lanes
+// of a row sum their partials (DPP), and the row's fp32 partial for this
+// segment goes to the workspace.  A second kernel adds the segments of every
+// row in segment order and rounds to fp16 once: deterministic, no atomics.
+#include "fasq_codebook.h"
+#include "fasq_device.h"
+#include "fasq_internal.h"
+
+namespace fasq {
+
+namespace {
+
+constexpr int kSubThreads = 1024;               // 16 waves
+constexpr int kSubBookBytes = 144 * 1024;       // LDS for the books of one segment
+constexpr int kSubMaxNch = 16;                  // chunks per row segment (lanes per row)
+
+struct SubArgs {
+  const half_t* x;
+  int64_t N;
+  const uint8_t* idx;
+  int64_t R;          // bytes per id row
+  int64_t CH;         // chunks per row
+  const half_t* cb;   // [S x C x d]
+  int C;
+  int KS;             // segments
+  int64_t rows_per_block;
+  float* ws;          // [KS x N] fp32 partials
+};
+
+// Codeword of book b (LDS byte address base + (b * C + u) * 2D) dotted with
+// the D x values at xv, added to acc.
+template <int D>
+__device__ __forceinline__ float dot_codeword(uint32_t addr, const uint32_t* xv, float acc) {
+  if constexpr (D == 1) {
+    const half_t c = __builtin_bit_cast(half_t, *lds_at<uint16_t>(addr));
+    const half_t xh = __builtin_bit_cast(half_t, (uint16_t)(xv[0] & 0xFFFF));
+    return __builtin_fmaf(static_cast<float>(xh), static_cast<float>(c), acc);
+  } else {
+    uint32_t c[D / 2];
+    read_codeword_lds<D>(addr, c);
+#pragma unroll
+    for (int k = 0; k < D / 2; ++k) acc = dot2(xv[k], c[k], acc);
+    return acc;
+  }
+}
+
+template <int BITS, int D, int NCH>
+__global__ __launch_bounds__(kSubThreads) void k_gemv_sub(SubArgs a) {
+  constexpr int G = Chunk<BITS>::G;
+  constexpr int DW = Chunk<BITS>::DW;
+  constexpr int CBY = DW * 4;
+  constexpr int RPL = kWave / NCH;             // rows per wave-wide load
+  constexpr int XW = D == 1 ? 1 : D / 2;       // dwords of x per id (D == 1: the low half)
+  static_assert(kWave % NCH == 0 && NCH <= kSubMaxNch, "NCH must divide the wave");
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+
+  const int ks = (int)(blockIdx.x % a.KS);
+  const int64_t rb = blockIdx.x / a.KS;
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int waves = blockDim.x / kWave;
+  const int c = lane % NCH;                     // chunk of the lane within the segment
+  const int rl = lane / NCH;                    // row of the lane within a load
+  const int64_t ch = (int64_t)ks * NCH + c;     // chunk within the row
+  const bool cval = ch < a.CH;
+  const int nbooks = (int)((a.CH - (int64_t)ks * NCH < NCH ? a.CH - (int64_t)ks * NCH : NCH) * G);
+
+  // rows of this workgroup: [r0, r1); wave-wide loads j = wave, wave + waves, ...
+  const int64_t r0 = rb * a.rows_per_block;
+  const int64_t r1 = r0 + a.rows_per_block < a.N ? r0 + a.rows_per_block : a.N;
+  const int nloads = (int)((r1 - r0 + RPL - 1) / RPL);
+  const int mine = nloads > wave ? (nloads - wave + waves - 1) / waves : 0;
+
+  const __amdgpu_buffer_rsrc_t rsrc = idx_rsrc(a.idx, (uint32_t)(a.N * a.R));
+  auto offset_of = [&](int k) {  // k-th load of this wave; rows past N read zeros
+    const int64_t row = r0 + (int64_t)(wave + k * waves) * RPL + rl;
+    return (uint32_t)(row * a.R + (cval ? ch : 0) * CBY);
+  };
+  uint32_t buf0[DW], buf1[DW];
+  if (mine > 0) buffer_chunk<BITS>(rsrc, offset_of(0), buf0);
+  if (mine > 1) buffer_chunk<BITS>(rsrc, offset_of(1), buf1);
+
+  // books of the segment -> LDS (16-byte words, consecutive threads)
+  {
+    const int words = nbooks * a.C * D * 2 / 16;
+    const u32x4* src = reinterpret_cast<const u32x4*>(a.cb + ((int64_t)ks * NCH * G) * a.C * D);
+    for (int base = threadIdx.x; base < words; base += 8 * blockDim.x) {
+      u32x4 v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int w = base + k * blockDim.x;
+        v[k] = src[w < words ? w : words - 1];
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int w = base + k * blockDim.x;
+        if (w < words) *reinterpret_cast<u32x4*>(smem + (uint32_t)w * 16) = v[k];
+      }
+    }
+  }
+  // x of the lane's chunk: G * D halves
+  uint32_t xv[G][XW];
+  {
+    const uint16_t* xs = reinterpret_cast<const uint16_t*>(a.x) + (cval ? ch : 0) * G * D;
+#pragma unroll
+    for (int i = 0; i < G; ++i) {
+#pragma unroll
+      for (int k = 0; k < XW; ++k) {
+        const uint32_t lo = xs[i * D + 2 * k];
+        const uint32_t hi = D == 1 ? 0u : (uint32_t)xs[i * D + 2 * k + 1];
+        xv[i][k] = cval ? (lo | (hi << 16)) : 0u;  // a chunk past the row contributes 0
+      }
+    }
+  }
+  __syncthreads();
+
+  const uint32_t book0 = (uint32_t)c * G;  // first book of the lane's chunk
+  auto compute = [&](const uint32_t* w, int k) {
+    float acc = 0.f;
+    if (cval) {  // a chunk past the row end (last segment) has no staged books
+#pragma unroll
+      for (int i = 0; i < G; ++i)
+        acc = dot_codeword<D>(((book0 + i) * (uint32_t)a.C + stream_id<BITS>(w, i)) * (2 * D), xv[i], acc);
+    }
+    acc = group_sum<NCH>(acc);
+    const int64_t row = r0 + (int64_t)(wave + k * waves) * RPL + rl;
+    if (c == 0 && row < r1) a.ws[(int64_t)ks * a.N + row] = acc;
+  };
+  for (int k = 0; k < mine; k += 2) {
+    compute(buf0, k);
+    if (k + 2 < mine) buffer_chunk<BITS>(rsrc, offset_of(k + 2), buf0);
+    if (k + 1 < mine) {
+      compute(buf1, k + 1);
+      if (k + 3 < mine) buffer_chunk<BITS>(rsrc, offset_of(k + 3), buf1);
+    }
+  }
+}
+
+// y[n] = fp16(sum over segments, in segment order, of ws[ks][n])
+__global__ void k_sub_reduce(const float* __restrict__ ws, int64_t N, int KS, half_t* __restrict__ y) {
+  for (int64_t n = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; n < N; n += (int64_t)gridDim.x * blockDim.x) {
+    float s = 0.f;
+    for (int k = 0; k < KS; ++k) s += ws[(int64_t)k * N + n];
+    y[n] = static_cast<half_t>(s);
+  }
+}
+
+// The split of a call: chunks per segment (NCH), segments (KS) and row
+// blocks; false when the tuned kernel does not apply.
+struct SubPlan {
+  int nch = 0, ks = 0;
+  int64_t rb = 0, rows = 0;
+};
+
+bool sub_plan(const Problem& p, const DeviceInfo& dev, SubPlan* out) {
+  if (p.M != 1 || p.cb_stride != p.C * p.d) return false;
+  const int d = p.d;
+  if (!(d == 1 || d == 2 || d == 4 || d == 8)) return false;
+  const int G = p.idx_bits == 8 ? 16 : 8;
+  const int CBY = p.idx_bits == 12 ? 12 : 16;
+  if (p.S % G || p.R != p.S / G * CBY) return false;
+  if ((p.C * d * 2) % 16) return false;
+  if ((reinterpret_cast<uintptr_t>(p.idx) & 3) || (reinterpret_cast<uintptr_t>(p.codebook) & 15) ||
+      (reinterpret_cast<uintptr_t>(p.x) & 3))
+    return false;
+  if ((p.N + kWave) * p.R >= (int64_t(1) << 32)) return false;  // loads read up to one load past N
+  const int64_t per_chunk = (int64_t)G * p.C * d * 2;  // book bytes per chunk of ids
+  int nch = kSubMaxNch;
+  while (nch > 1 && nch * per_chunk > kSubBookBytes) nch /= 2;
+  if (per_chunk > kSubBookBytes) return false;
+  const int64_t CH = p.S / G;
+  const int64_t ks = (CH + nch - 1) / nch;
+  // row blocks: about one workgroup per CU in all, each with whole loads
+  int64_t rb = (dev.num_cus + ks - 1) / ks;
+  const int64_t rpl = kWave / nch;
+  if (rb > (p.N + rpl - 1) / rpl) rb = (p.N + rpl - 1) / rpl;
+  if (rb < 1) rb = 1;
+  int64_t rows = (p.N + rb - 1) / rb;
+  rows = (rows + rpl - 1) / rpl * rpl;
+  rb = (p.N + rows - 1) / rows;
+  if (rb * ks > 0x7fffffff) return false;
+  out->nch = nch;
+  out->ks = (int)ks;
+  out->rb = rb;
+  out->rows = rows;
+  return true;
+}
+
+template <int BITS, int D, int NCH>
+hipError_t launch_sub(const SubArgs& a, int blocks, int lds, hipStream_t stream) {
+  auto kern = k_gemv_sub<BITS, D, NCH>;
+  if (plan_record("k_gemv_sub", {BITS, D, NCH})) return hipSuccess;
+  hipError_t e = prepare_kernel(kern);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3(blocks), dim3(kSubThreads), lds, stream, a);
+  return hipGetLastError();
+}
+
+template <int BITS, int D>
+hipError_t launch_sub_nch(const SubArgs& a, int nch, int blocks, int lds, hipStream_t stream) {
+  switch (nch) {
+    case 16: return launch_sub<BITS, D, 16>(a, blocks, lds, stream);
+    case 8: return launch_sub<BITS, D, 8>(a, blocks, lds, stream);
+    case 4: return launch_sub<BITS, D, 4>(a, blocks, lds, stream);
+    case 2: return launch_sub<BITS, D, 2>(a, blocks, lds, stream);
+    default: return launch_sub<BITS, D, 1>(a, blocks, lds, stream);
+  }
+}
+
+template <int BITS>
+hipError_t launch_sub_d(const SubArgs& a, int d, int nch, int blocks, int lds, hipStream_t stream) {
+  switch (d) {
+    case 1: return launch_sub_nch<BITS, 1>(a, nch, blocks, lds, stream);
+    case 2: return launch_sub_nch<BITS, 2>(a, nch, blocks, lds, stream);
+    case 4: return launch_sub_nch<BITS, 4>(a, nch, blocks, lds, stream);
+    default: return launch_sub_nch<BITS, 8>(a, nch, blocks, lds, stream);
+  }
+}
+
+}  // namespace
+
+int64_t gemv_sub_workspace_bytes(const Problem& p, const DeviceInfo& dev) {
+  SubPlan sp;
+  if (!sub_plan(p, dev, &sp)) return 0;
+  return (int64_t)sp.ks * p.N * 4;
+}
+
+hipError_t launch_gemv_sub(const Problem& p, void* workspace, int64_t workspace_bytes, const DeviceInfo& dev,
+                           hipStream_t stream) {
+  SubPlan sp;
+  if (!sub_plan(p, dev, &sp)) return hipErrorNotSupported;
+  if (workspace == nullptr || workspace_bytes < (int64_t)sp.ks * p.N * 4 ||
+      (reinterpret_cast<uintptr_t>(workspace) & 3))
+    return hipErrorNotSupported;
+  const int G = p.idx_bits == 8 ? 16 : 8;
+  SubArgs a;
+  a.x = static_cast<const half_t*>(p.x);
+  a.N = p.N;
+  a.idx = static_cast<const uint8_t*>(p.idx);
+  a.R = p.R;
+  a.CH = p.S / G;
+  a.cb = static_cast<const half_t*>(p.codebook);
+  a.C = (int)p.C;
+  a.KS = sp.ks;
+  a.rows_per_block = sp.rows;
+  a.ws = static_cast<float*>(workspace);
+  const int lds = (int)((int64_t)sp.nch * G * p.C * p.d * 2);
+  const int blocks = (int)(sp.rb * sp.ks);
+  hipError_t e;
+  switch (p.idx_bits) {
+    case 8: e = launch_sub_d<8>(a, p.d, sp.nch, blocks, lds, stream); break;
+    case 12: e = launch_sub_d<12>(a, p.d, sp.nch, blocks, lds, stream); break;
+    default: e = launch_sub_d<16>(a, p.d, sp.nch, blocks, lds, stream); break;
+  }
+  if (e != hipSuccess || plan().active) return e;
+  const int64_t rblocks = (p.N + 255) / 256;
+  hipLaunchKernelGGL(k_sub_reduce, dim3((unsigned)(rblocks < 65536 ? rblocks : 65536)), dim3(256), 0, stream,
+                     static_cast<const float*>(workspace), p.N, sp.ks, static_cast<half_t*>(p.y));
+  return hipGetLastError();
+}
+
+}  // namespace fasq

@@ -13,7 +13,7 @@ namespace fasq {
 template <int BITS>
 __global__ __launch_bounds__(256) void k_reconstruct(const uint8_t* __restrict__ idx, int64_t N, int64_t S,
                                                      int64_t R, int d, const uint16_t* __restrict__ cb,
-                                                     uint16_t* __restrict__ w) {
+                                                     int64_t cbs, uint16_t* __restrict__ w) {
   const int64_t total = N * S;
   const int64_t K = S * d;
   for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total;
@@ -21,13 +21,14 @@ __global__ __launch_bounds__(256) void k_reconstruct(const uint8_t* __restrict__
     const int64_t n = t / S;
     const int64_t s = t - n * S;
     const uint32_t u = load_id_bytes<BITS>(idx + n * R, s, R);
-    const uint16_t* src = cb + (int64_t)u * d;
+    const uint16_t* src = cb + s * cbs + (int64_t)u * d;
     uint16_t* dst = w + n * K + s * d;
     for (int i = 0; i < d; ++i) dst[i] = src[i];
   }
 }
 
-// y[m, n] = sum_s dot(x[m, s*d:(s+1)*d], codebook[u(n, s)]), fp32 accumulation.
+// y[m, n] = sum_s dot(x[m, s*d:(s+1)*d], codebook[u(n, s)]), fp32 accumulation
+// (codebook s of subspace s at cb + s * cbs when the books are per subspace).
 // One wave per output row n; lanes stride over the S sub-vectors; MB rows of
 // x are accumulated at a time.  Codewords are read from global memory.
 constexpr int kGenericMB = 8;
@@ -35,7 +36,7 @@ constexpr int kGenericMB = 8;
 template <int BITS>
 __global__ __launch_bounds__(256) void k_pq_generic(const half_t* __restrict__ x, int64_t M, int64_t K,
                                                     int64_t N, const uint8_t* __restrict__ idx, int64_t R,
-                                                    int d, const half_t* __restrict__ cb,
+                                                    int d, const half_t* __restrict__ cb, int64_t cbs,
                                                     half_t* __restrict__ y) {
   const int lane = threadIdx.x & (kWave - 1);
   const int64_t waves = (int64_t)gridDim.x * (blockDim.x / kWave);
@@ -49,7 +50,7 @@ __global__ __launch_bounds__(256) void k_pq_generic(const half_t* __restrict__ x
       for (int j = 0; j < kGenericMB; ++j) acc[j] = 0.f;
       for (int64_t s = lane; s < S; s += kWave) {
         const uint32_t u = load_id_bytes<BITS>(row, s, R);
-        const half_t* c = cb + (int64_t)u * d;
+        const half_t* c = cb + s * cbs + (int64_t)u * d;
         for (int i = 0; i < d; ++i) {
           const float cv = static_cast<float>(c[i]);
           const half_t* xp = x + m0 * K + s * d + i;
@@ -83,9 +84,9 @@ hipError_t launch_reconstruct(const Problem& p, void* w, hipStream_t stream) {
   const uint16_t* cb = static_cast<const uint16_t*>(p.codebook);
   uint16_t* out = static_cast<uint16_t*>(w);
   switch (p.idx_bits) {
-    case 8: hipLaunchKernelGGL(k_reconstruct<8>, dim3(blocks), dim3(256), 0, stream, idx, p.N, S, p.R, p.d, cb, out); break;
-    case 12: hipLaunchKernelGGL(k_reconstruct<12>, dim3(blocks), dim3(256), 0, stream, idx, p.N, S, p.R, p.d, cb, out); break;
-    default: hipLaunchKernelGGL(k_reconstruct<16>, dim3(blocks), dim3(256), 0, stream, idx, p.N, S, p.R, p.d, cb, out); break;
+    case 8: hipLaunchKernelGGL(k_reconstruct<8>, dim3(blocks), dim3(256), 0, stream, idx, p.N, S, p.R, p.d, cb, p.cb_stride, out); break;
+    case 12: hipLaunchKernelGGL(k_reconstruct<12>, dim3(blocks), dim3(256), 0, stream, idx, p.N, S, p.R, p.d, cb, p.cb_stride, out); break;
+    default: hipLaunchKernelGGL(k_reconstruct<16>, dim3(blocks), dim3(256), 0, stream, idx, p.N, S, p.R, p.d, cb, p.cb_stride, out); break;
   }
   return hipGetLastError();
 }
@@ -98,9 +99,9 @@ hipError_t launch_generic(const Problem& p, hipStream_t stream) {
   const half_t* cb = static_cast<const half_t*>(p.codebook);
   half_t* y = static_cast<half_t*>(p.y);
   switch (p.idx_bits) {
-    case 8: hipLaunchKernelGGL(k_pq_generic<8>, dim3(blocks), dim3(256), 0, stream, x, p.M, p.K, p.N, idx, p.R, p.d, cb, y); break;
-    case 12: hipLaunchKernelGGL(k_pq_generic<12>, dim3(blocks), dim3(256), 0, stream, x, p.M, p.K, p.N, idx, p.R, p.d, cb, y); break;
-    default: hipLaunchKernelGGL(k_pq_generic<16>, dim3(blocks), dim3(256), 0, stream, x, p.M, p.K, p.N, idx, p.R, p.d, cb, y); break;
+    case 8: hipLaunchKernelGGL(k_pq_generic<8>, dim3(blocks), dim3(256), 0, stream, x, p.M, p.K, p.N, idx, p.R, p.d, cb, p.cb_stride, y); break;
+    case 12: hipLaunchKernelGGL(k_pq_generic<12>, dim3(blocks), dim3(256), 0, stream, x, p.M, p.K, p.N, idx, p.R, p.d, cb, p.cb_stride, y); break;
+    default: hipLaunchKernelGGL(k_pq_generic<16>, dim3(blocks), dim3(256), 0, stream, x, p.M, p.K, p.N, idx, p.R, p.d, cb, p.cb_stride, y); break;
   }
   return hipGetLastError();
 }

@@ -21,6 +21,7 @@ struct Problem {
   void* y;
   int64_t S;  // sub-vectors per row, K / d
   int64_t R;  // bytes per packed index row
+  int64_t cb_stride = 0;  // 0: one shared codebook; C * d: codebook s of subspace s at codebook + s * C * d
 };
 
 // Properties of the current device, read once per device and cached.
@@ -47,6 +48,13 @@ constexpr int kMaxBatchLaunch = 8;  // matrices per grouped launch
 
 // Tuned MFMA prefill kernel.  hipErrorNotSupported when no variant applies.
 hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
+
+// Per-subspace codebooks, one token: K split over workgroups whose codebooks
+// fit in LDS, fp32 partials in `workspace`, then a fixed-order sum.
+// hipErrorNotSupported when the tuned kernel does not apply.
+int64_t gemv_sub_workspace_bytes(const Problem& p, const DeviceInfo& dev);
+hipError_t launch_gemv_sub(const Problem& p, void* workspace, int64_t workspace_bytes, const DeviceInfo& dev,
+                           hipStream_t stream);
 
 // Once per device and kernel: check that the kernel declares no static LDS
 // (its LDS-resident codebook is addressed from LDS address 0) and raise its
