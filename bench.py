@@ -135,6 +135,8 @@ class MatrixSet:
 
     def group_kernel(self, g):
         p = self.problems[self.groups[g][0]]
+        if self.regime == "lut":
+            return "k_gemm_lut"
         return self.fasq.plan(self.regime, p.M, p.K, p.N, p.idx_bits, p.d, p.C)
 
     def launch(self, c, g, stream):
@@ -143,7 +145,7 @@ class MatrixSet:
         p0, x = self.problems[members[0]], s[members[0]]["x"].data_ptr()
         if len(members) == 1:
             t = s[members[0]]
-            fn = self.fasq.gemm_raw if self.regime == "gemm" else self.fasq.gemv_raw
+            fn = dict(gemm=self.fasq.gemm_raw, lut=self.fasq.gemm_lut_raw).get(self.regime, self.fasq.gemv_raw)
             st = fn(x, p0.M, p0.K, p0.N, t["idx"].data_ptr(), p0.idx_bits, p0.d,
                     t["cb"].data_ptr(), p0.C, t["y"].data_ptr(), stream)
         else:
@@ -529,9 +531,11 @@ def sensitivity(torch, fasq, pi):
     for L in (32, 64, 128, 256, 512, 1024, 2048):
         r = gemv_row(L, 2, 256, 8, regime="gemm")
         r["dense_us"] = time_dense(torch, L, SENS_K, SENS_N) * 1e6
+        if L in (32, 128, 512, 2048):  # the paper's lookup-table GEMM design (Alg. 3), for comparison
+            r["lut_us"] = gemv_row(L, 2, 256, 8, regime="lut")["us"]
         out["prefill"].append(r)
         log(f"[bench] sensitivity prefill L={L:5d}: {r['us']:8.2f} us ({r['tflops']:.0f} TFLOP/s), "
-            f"dense fp16 {r['dense_us']:8.2f} us")
+            f"dense fp16 {r['dense_us']:8.2f} us" + (f", lookup-table GEMM {r['lut_us']:9.2f} us" if "lut_us" in r else ""))
     torch.cuda.empty_cache()
     return out
 

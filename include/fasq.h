@@ -127,6 +127,19 @@ fasq_status fasq_pq_gemm(const void* x, int64_t M, int64_t K, int64_t N,
                          void* y, hipStream_t stream);
 
 /*
+ * The paper's own prefill kernel design (FASQ Sec. 4.2, Alg. 3), kept for
+ * comparison with fasq_pq_gemm: per token and subspace a lookup table of the
+ * C dot products x_s . codebook[k] is built in LDS (fp32), and every output
+ * feature adds up its table entries.  No matrix cores.  Same arguments,
+ * layouts and errors as fasq_pq_gemm, plus FASQ_ERR_UNSUPPORTED when d is not
+ * in {1, 2, 4, 8} or C > 2048 (the tables would not fit in LDS).
+ */
+fasq_status fasq_pq_gemm_lut(const void* x, int64_t M, int64_t K, int64_t N,
+                             const void* idx, int idx_bits, int d,
+                             const void* codebook, int64_t C,
+                             void* y, hipStream_t stream);
+
+/*
  * Decode regime with the paper's general codebook layout (FASQ Sec. 3.1.1:
  * T_cluster is [N_ss x K_s x SZ_ss], one codebook per subspace; Eq.
  * lut-accumulate):

@@ -36,6 +36,8 @@ __all__ = [
     "pq_gemv_batched",
     "pq_encode",
     "pq_gemv_ex",
+    "pq_gemm_lut",
+    "gemm_lut_raw",
     "gemv_ex_raw",
     "gemv_ex_workspace_bytes",
     "encode_raw",
@@ -75,6 +77,7 @@ EXPORTED_SYMBOLS = (
     "fasq_pq_encode_workspace_bytes",
     "fasq_pq_gemv_ex",
     "fasq_pq_gemv_ex_workspace_bytes",
+    "fasq_pq_gemm_lut",
 )
 
 
@@ -108,7 +111,7 @@ def lib() -> ctypes.CDLL:
             raise LibraryNotBuilt(f"{LIB_PATH} is missing; build it with __graft_entry__.build()")
         L = ctypes.CDLL(LIB_PATH)
         mm = [_c_vp, _c_i64, _c_i64, _c_i64, _c_vp, _c_int, _c_int, _c_vp, _c_i64, _c_vp, _c_vp]
-        for name in ("fasq_pq_gemv", "fasq_pq_gemm"):
+        for name in ("fasq_pq_gemv", "fasq_pq_gemm", "fasq_pq_gemm_lut"):
             f = getattr(L, name)
             f.argtypes = mm
             f.restype = _c_int
@@ -268,6 +271,16 @@ def pq_gemv(x, idx, idx_bits: int, d: int, codebook, out=None):
 def pq_gemm(x, idx, idx_bits: int, d: int, codebook, out=None):
     """Prefill-regime ``y = x . W_hat^T`` (MFMA path); see ``fasq_pq_gemm``."""
     return _matmul(lib().fasq_pq_gemm, x, idx, idx_bits, d, codebook, out)
+
+
+def pq_gemm_lut(x, idx, idx_bits: int, d: int, codebook, out=None):
+    """``y = x . W_hat^T`` with the paper's lookup-table GEMM design (for
+    comparison); see ``fasq_pq_gemm_lut``."""
+    return _matmul(lib().fasq_pq_gemm_lut, x, idx, idx_bits, d, codebook, out)
+
+
+def gemm_lut_raw(x, M, K, N, idx, idx_bits, d, codebook, C, y, stream=0) -> int:
+    return lib().fasq_pq_gemm_lut(x, M, K, N, idx, idx_bits, d, codebook, C, y, stream)
 
 
 def pq_gemv_batched(x, idxs, idx_bits: int, d: int, codebooks, outs=None):

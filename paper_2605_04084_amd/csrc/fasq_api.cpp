@@ -219,6 +219,18 @@ fasq_status fasq_pq_gemm(const void* x, int64_t M, int64_t K, int64_t N, const v
   return fasq::run(fasq::make_problem(x, M, K, N, idx, idx_bits, d, codebook, C, y), fasq::Regime::kGemm, stream);
 }
 
+fasq_status fasq_pq_gemm_lut(const void* x, int64_t M, int64_t K, int64_t N, const void* idx, int idx_bits, int d,
+                             const void* codebook, int64_t C, void* y, hipStream_t stream) {
+  fasq_status s = fasq::validate(M, K, N, idx_bits, d, C, x, idx, codebook, y, true);
+  if (s != FASQ_OK) return s;
+  hipError_t e = fasq::launch_gemm_lut(fasq::make_problem(x, M, K, N, idx, idx_bits, d, codebook, C, y), stream);
+  if (e == hipErrorNotSupported)
+    return fasq::fail(FASQ_ERR_UNSUPPORTED, "the lookup-table GEMM needs d in {1, 2, 4, 8} and C <= 2048");
+  if (e != hipSuccess) return fasq::hip_fail("kernel launch", e);
+  fasq::t_last_error.clear();
+  return FASQ_OK;
+}
+
 fasq_status fasq_pq_reconstruct(const void* idx, int64_t N, int64_t K, int idx_bits, int d, const void* codebook,
                                 int64_t C, void* w, hipStream_t stream) {
   fasq_status s = fasq::validate(1, K, N, idx_bits, d, C, nullptr, idx, codebook, w, false);

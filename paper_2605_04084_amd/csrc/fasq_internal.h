@@ -49,6 +49,10 @@ constexpr int kMaxBatchLaunch = 8;  // matrices per grouped launch
 // Tuned MFMA prefill kernel.  hipErrorNotSupported when no variant applies.
 hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
 
+// The paper's lookup-table GEMM (Alg. 3), kept for comparison with the MFMA
+// GEMM.  hipErrorNotSupported when its tables do not fit in LDS.
+hipError_t launch_gemm_lut(const Problem& p, hipStream_t stream);
+
 // Per-subspace codebooks, one token: K split over workgroups whose codebooks
 // fit in LDS, fp32 partials in `workspace`, then a fixed-order sum.
 // hipErrorNotSupported when the tuned kernel does not apply.

@@ -465,3 +465,50 @@ def test_gemm_k_groups_one_hot_bit_exact(case):
     assert np.abs(ref).max() <= 2048
     y = to_np(fasq.pq_gemm(to_dev(x), to_dev(idx), bits, d, to_dev(cb))).astype(np.float64)
     assert np.array_equal(y, ref)
+
+
+# ---------------------------------------------------------------------------
+# The paper's lookup-table GEMM (Alg. 3), kept for comparison
+# ---------------------------------------------------------------------------
+
+LUT_CASES = [
+    # M, K, N, d, C, bits
+    (5, 256, 300, 2, 256, 8),      # ragged tokens and features
+    (128, 512, 256, 4, 256, 8),
+    (9, 320, 77, 1, 64, 8),
+    (16, 512, 130, 8, 256, 16),
+    (12, 384, 90, 4, 2048, 12),    # one subspace per table batch
+    (3, 36, 20, 4, 9, 12),         # odd 12-bit rows, batch past the last subspace
+]
+
+
+@pytest.mark.parametrize("case", LUT_CASES)
+def test_lut_gemm_matches_oracle(case):
+    M, K, N, d, C, bits = case
+    print(f"[case] lut gemm {case}", flush=True)
+    rng = np.random.default_rng(31 + sum(case))
+    p = pi.draw_problem(rng, M, K, N, d, C, bits)
+    y = to_np(fasq.pq_gemm_lut(to_dev(p.x), to_dev(p.idx), bits, d, to_dev(p.codebook))).astype(np.float64)
+    assert_close(y, orc.pq_linear(p.x, p.idx, bits, d, p.codebook), f"lut {case}")
+
+
+def test_lut_gemm_one_hot_is_bit_exact():
+    M, K, N, d, C, bits = 20, 1024, 200, 2, 256, 8
+    rng = np.random.default_rng(41)
+    cb = pi.signed_one_hot_codebook(C, d, rng)
+    ids = rng.integers(0, C, size=(N, K // d))
+    x = pi.ternary_x(rng, M, K)
+    idx = pi.pack_indices(ids, bits)
+    ref = orc.pq_linear(x, idx, bits, d, cb)
+    y = to_np(fasq.pq_gemm_lut(to_dev(x), to_dev(idx), bits, d, to_dev(cb))).astype(np.float64)
+    assert np.array_equal(y, ref)
+
+
+def test_lut_gemm_rejects_tables_larger_than_lds():
+    x = torch.zeros((2, 64), dtype=torch.float16, device="cuda:0")
+    idx = torch.zeros((4, 64 * 12 // 8 // 4), dtype=torch.uint8, device="cuda:0")
+    cb = torch.zeros((4096, 4), dtype=torch.float16, device="cuda:0")
+    y = torch.empty((2, 4), dtype=torch.float16, device="cuda:0")
+    st = fasq.gemm_lut_raw(x.data_ptr(), 2, 64, 4, idx.data_ptr(), 12, 4, cb.data_ptr(), 4096, y.data_ptr(), 0)
+    assert st == fasq.FASQ_ERR_UNSUPPORTED
+    assert "C <= 2048" in fasq.last_error()
