@@ -436,7 +436,7 @@ def time_per_subspace(torch, fasq, pi, rng, d=2, C=256, bits=8, steps=10, short=
     ws_bytes = fasq.gemv_ex_workspace_bytes(1, SENS_K, SENS_N, bits, d, C, C * d)
     base = [torch.from_numpy(a).to(dev) for a in (x, idx, books)]
     sets = [[t.clone() for t in base] + [torch.empty((1, SENS_N), dtype=torch.float16, device=dev),
-                                         torch.empty(max(ws_bytes, 4), dtype=torch.uint8, device=dev)]
+                                         torch.zeros(max(ws_bytes, 4), dtype=torch.uint8, device=dev)]
             for _ in range(copies)]
     stream = torch.cuda.current_stream()
 
@@ -537,6 +537,44 @@ def sensitivity(torch, fasq, pi):
         log(f"[bench] sensitivity prefill L={L:5d}: {r['us']:8.2f} us ({r['tflops']:.0f} TFLOP/s), "
             f"dense fp16 {r['dense_us']:8.2f} us" + (f", lookup-table GEMM {r['lut_us']:9.2f} us" if "lut_us" in r else ""))
     torch.cuda.empty_cache()
+    return out
+
+
+def tiny_latency(torch, fasq, pi, reps=200):
+    """The tiny workload (M = 1, 128 x 256, d = 4, C = 256): a latency case.
+    GPU: per-call time of back-to-back launches on the same (hot) operands;
+    CPU: the fp64 oracle, median of 5."""
+    from oracle import pq_oracle as orc
+
+    p = pi.workload("tiny").problem(0)
+    dev = torch.device("cuda:0")
+    x, idx, cb = (torch.from_numpy(a).to(dev) for a in (p.x, p.idx, p.codebook))
+    y = torch.empty((p.M, p.N), dtype=torch.float16, device=dev)
+    stream = torch.cuda.current_stream()
+    args = (x.data_ptr(), p.M, p.K, p.N, idx.data_ptr(), p.idx_bits, p.d, cb.data_ptr(), p.C, y.data_ptr(),
+            stream.cuda_stream)
+    assert fasq.gemv_raw(*args) == 0, fasq.last_error()
+
+    def batch(count):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(SPACER_CYCLES)
+        e0.record(stream)
+        for _ in range(count):
+            fasq.gemv_raw(*args)
+        e1.record(stream)
+        e1.synchronize()
+        return e0.elapsed_time(e1) * 1e-3
+
+    t = float(np.median([(batch(20) - batch(4)) / 16 for _ in range(reps // 20)]))
+    cpu = []
+    for _ in range(5):
+        t0 = time.perf_counter()
+        orc.pq_linear(p.x, p.idx, p.idx_bits, p.d, p.codebook)
+        cpu.append(time.perf_counter() - t0)
+    out = dict(shape="128x256", M=1, d=4, C=256, idx_bits=8, us=t * 1e6,
+               kernel=fasq.plan("gemv", p.M, p.K, p.N, p.idx_bits, p.d, p.C), cpu_oracle_ms=float(np.median(cpu)) * 1e3)
+    log(f"[bench] tiny 128x256 d=4: {t * 1e6:.2f} us per call on the GPU ({out['kernel']}); "
+        f"CPU oracle {out['cpu_oracle_ms']:.3f} ms")
     return out
 
 
@@ -762,6 +800,7 @@ def main():
         report_layer("3bit", r3)
         extra["llama3_8b_3bit"] = r3
         extra["prefill"] = prefill(torch, fasq, pi, (128, 512, 2048), 10)
+        extra["tiny"] = tiny_latency(torch, fasq, pi)
     if args.per_matrix:
         r1 = decode_layer(torch, fasq, pi, "llama3_8b_4bit", max(10, args.steps // 2), 3, grouped=False)
         report_layer("4bit, one launch per matrix", r1)

@@ -11,6 +11,7 @@ namespace fasq {
 constexpr int kLdsCodebookBudget = 64 * 1024;  // bytes of LDS a codebook may take
 constexpr int kSliceReserve = 8 * 1024;        // LDS kept for row partials beside a codebook slice
 constexpr int kMinSliceBytes = 32 * 1024;      // smaller slices: gather from global memory instead
+constexpr int kReplMinIdsPerEntry = 16;        // replicate the codebook only above this many ids per workgroup and entry
 static_assert(kM1MaxMats == kMaxBatchLaunch, "grouped launches and their kernel disagree on the group size");
 
 // Codebook placement for a call: replicated in LDS when the replicated table
@@ -87,6 +88,7 @@ hipError_t launch_gemv_bits(const Problem& p, const DeviceInfo& dev, hipStream_t
   const int threads = P * Q * kWave;
 
   int mode = choose_cb_mode(p.C, d);
+  if (mode == CB_REPL && (p.N + dev.num_cus - 1) / dev.num_cus * p.S < kReplMinIdsPerEntry * p.C) mode = CB_LDS;
   const int xs = (int)(p.M == 1 ? p.K * 2 : p.K * 2 + 16);
   const int64_t x_bytes = p.M * (int64_t)xs;
   // The replicated table (up to 64 KB) gives way to one copy when it leaves
@@ -244,6 +246,10 @@ hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& d
   // A codebook too large for LDS is staged slice by slice (one pass over the
   // rows per slice) when its slices fit beside x and the row partials.
   int mode = choose_cb_mode(maxC, d);
+  // The replicated table costs each workgroup C * 256 bytes of LDS writes; a
+  // workgroup with few ids to gather is faster with one copy.
+  if (mode == CB_REPL && (total_rows + dev.num_cus - 1) / dev.num_cus * p.S < kReplMinIdsPerEntry * maxC)
+    mode = CB_LDS;
   const int64_t x_bytes = (p.K * 2 + 15) / 16 * 16;
   int sl_shift = 0;
   if (mode == CB_GLOBAL && (maxC * d * 2) % 16 == 0) {

@@ -191,6 +191,8 @@ RAGGED = [
     (130, 256, 257, 4, 4096, 12),
     (33, 64, 50, 1, 256, 8),
     (16, 4096, 200, 2, 256, 8),         # 16 rows of x leave no room for the replicated table
+    (1, 320, 20000, 4, 256, 8),         # enough rows per workgroup for the replicated table, masked tail
+    (1, 1024, 9000, 1, 256, 8),
 ]
 
 
@@ -512,3 +514,11 @@ def test_lut_gemm_rejects_tables_larger_than_lds():
     st = fasq.gemm_lut_raw(x.data_ptr(), 2, 64, 4, idx.data_ptr(), 12, 4, cb.data_ptr(), 4096, y.data_ptr(), 0)
     assert st == fasq.FASQ_ERR_UNSUPPORTED
     assert "C <= 2048" in fasq.last_error()
+
+
+def test_codebook_placement_follows_the_work_per_workgroup():
+    """Few ids per workgroup: one LDS copy of the codebook (mode 1); many: the
+    replicated table (mode 0)."""
+    assert fasq.plan("gemv", 1, 256, 128, 8, 4, 256) == "k_gemv_m1<8, 4, 1, 1, 1>"
+    assert fasq.plan("gemv", 1, 4096, 4096, 8, 2, 256) == "k_gemv_m1<8, 2, 2, 0, 0>"
+    assert fasq.plan("gemv", 1, 320, 20000, 8, 4, 256).startswith("k_gemv_m1<8, 4, 1, 0, ")

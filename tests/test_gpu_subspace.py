@@ -61,6 +61,7 @@ def test_per_subspace_books_match_oracle(case):
 
 
 def test_tuned_path_is_taken_for_one_token():
+    # fp32 partials of 16 segments
     assert fasq.gemv_ex_workspace_bytes(1, 4096, 4096, 8, 2, 256, 512) == 16 * 4096 * 4
     assert fasq.gemv_ex_workspace_bytes(3, 4096, 4096, 8, 2, 256, 512) == 0
     assert fasq.gemv_ex_workspace_bytes(1, 4096, 4096, 8, 2, 256, 0) == 0
@@ -108,6 +109,18 @@ def test_small_workspace_takes_the_general_kernel():
                           ws.data_ptr(), 64, torch.cuda.current_stream().cuda_stream)
     assert st == 0, fasq.last_error()
     assert_close(to_np(y).astype(np.float64), reference(x, books, idx, 8), "general kernel")
+
+
+def test_one_workspace_serves_consecutive_calls_of_different_shapes():
+    """One workspace serves calls of different shapes back to back."""
+    rng = np.random.default_rng(12)
+    need = max(fasq.gemv_ex_workspace_bytes(1, K, N, 8, 2, 256, 512) for K, N in ((4096, 700), (2048, 3000)))
+    ws = torch.zeros(need, dtype=torch.uint8, device="cuda:0")
+    for rep in range(3):
+        for K, N in ((4096, 700), (2048, 3000)):
+            x, books, ids, idx = draw(rng, 1, K, N, 2, 256, 8)
+            y = fasq.pq_gemv_ex(to_dev(x), to_dev(idx), 8, 2, to_dev(books), workspace=ws)
+            assert_close(to_np(y).astype(np.float64), reference(x, books, idx, 8), f"reuse {rep} {K}x{N}")
 
 
 def test_paper_layer_4096_2_256_sampled():
