@@ -306,7 +306,9 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
   constexpr int DW = Chunk<BITS>::DW;
   constexpr int CBY = DW * 4;
   constexpr int SPC = G * D / 8;     // MFMA steps per chunk
-  constexpr int L = kGemvPipe;
+  // load slots: the sliced-codebook kernel keeps fewer (its extra state would
+  // otherwise spill), the others a full pipeline's worth
+  constexpr int L = MODE == CB_SLICE ? (T > 4 ? T : 4) : kGemvPipe;
   static_assert(L % T == 0, "pipeline depth must be a multiple of T");
   constexpr bool kXInRegs = T * SPC <= 8;
 
