@@ -137,7 +137,8 @@ class MatrixSet:
         p = self.problems[self.groups[g][0]]
         if self.regime == "lut":
             return "k_gemm_lut"
-        return self.fasq.plan(self.regime, p.M, p.K, p.N, p.idx_bits, p.d, p.C)
+        regime = "gemv_batched" if self.regime == "gemv" and len(self.groups[g]) > 1 else self.regime
+        return self.fasq.plan(regime, p.M, p.K, p.N, p.idx_bits, p.d, p.C)
 
     def launch(self, c, g, stream):
         members = self.groups[g]

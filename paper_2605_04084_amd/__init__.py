@@ -159,8 +159,11 @@ def idx_row_bytes(K: int, d: int, idx_bits: int) -> int:
 
 
 def plan(regime: str, M: int, K: int, N: int, idx_bits: int, d: int, C: int) -> str:
-    """Kernel instantiation a call would launch ("gemv" or "gemm" regime)."""
-    return lib().fasq_pq_plan(1 if regime == "gemm" else 0, M, K, N, idx_bits, d, C).decode()
+    """Kernel instantiation a call would launch: regime "gemv", "gemm", or
+    "gemv_batched" (a grouped decode launch over several matrices of these
+    sizes)."""
+    code = {"gemv": 0, "gemm": 1, "gemv_batched": 2}[regime]
+    return lib().fasq_pq_plan(code, M, K, N, idx_bits, d, C).decode()
 
 
 def status_string(status: int) -> str:

@@ -354,7 +354,17 @@ const char* fasq_pq_plan(int regime, int64_t M, int64_t K, int64_t N, int idx_bi
   pl.active = true;
   pl.name[0] = 0;
   Problem p = fasq::make_problem(fake, M, K, N, fake, idx_bits, d, fake, C, const_cast<void*>(fake));
-  s = fasq::run(p, regime == 1 ? fasq::Regime::kGemm : fasq::Regime::kGemv, nullptr);
+  if (regime == 2) {  // a grouped decode launch: two matrices of these sizes
+    Problem ps[2] = {p, p};
+    fasq::DeviceInfo dev;
+    hipError_t e = fasq::device_info(&dev);
+    if (e == hipSuccess && M == 1 && !fasq::force_generic()) e = fasq::launch_gemv_m1_group(ps, 2, dev, nullptr);
+    else e = hipErrorNotSupported;
+    s = e == hipSuccess ? FASQ_OK : e == hipErrorNotSupported ? fasq::run(p, fasq::Regime::kGemv, nullptr)
+                                                             : FASQ_ERR_HIP;
+  } else {
+    s = fasq::run(p, regime == 1 ? fasq::Regime::kGemm : fasq::Regime::kGemv, nullptr);
+  }
   pl.active = false;
   if (s != FASQ_OK) return "";
   return pl.name;

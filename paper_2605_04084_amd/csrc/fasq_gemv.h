@@ -284,7 +284,7 @@ struct GemvM1Mat {
   int nsl;  // CB_SLICE: codebook slices (passes over the rows)
 };
 
-constexpr int kM1MaxMats = 8;  // matrices one single-token launch can take
+constexpr int kM1MaxMats = 4;  // matrices one single-token launch can take
 
 struct GemvM1Args {
   const half_t* x;  // shared by every matrix of the launch
@@ -296,11 +296,12 @@ struct GemvM1Args {
   int cb_bytes;  // LDS bytes of the codebook (x follows)
   int x_bytes;   // LDS bytes of x (partials follow)
   int sl_shift;  // CB_SLICE: log2 of the entries per slice
-  int nmat;
   GemvM1Mat mat[kM1MaxMats];
 };
 
-template <int BITS, int D, int T, int MODE, bool MASK>
+// NM: matrix slots the workgroups choose from (1 for a single matrix,
+// kM1MaxMats for a grouped launch).
+template <int BITS, int D, int T, int MODE, bool MASK, int NM>
 __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
   constexpr int G = Chunk<BITS>::G;
   constexpr int DW = Chunk<BITS>::DW;
@@ -314,18 +315,24 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
 
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
-  // the matrix of this workgroup, and the workgroup's place among its own
+  // The matrix of this workgroup, and the workgroup's place among its own.
+  // Unused slots have wg_begin = INT_MAX and are never chosen, so all the
+  // range tests load at once; a single-matrix launch reads slot 0 directly,
+  // in the same batch of scalar loads as the other arguments.
   int m = 0;
 #pragma unroll
-  for (int i = 1; i < kM1MaxMats; ++i)
-    if (i < a.nmat && (int)blockIdx.x >= a.mat[i].wg_begin) m = i;
+  for (int i = 1; i < NM; ++i)
+    if ((int)blockIdx.x >= a.mat[i].wg_begin) m = i;
   const uint8_t* __restrict__ idx = a.mat[m].idx;
   const half_t* __restrict__ cb = a.mat[m].cb;
   half_t* __restrict__ y = a.mat[m].y;
   const int64_t N = a.mat[m].N;
   const int C = a.mat[m].C;
-  const uint32_t wg = (uint32_t)blockIdx.x - (uint32_t)a.mat[m].wg_begin;
-  const uint32_t nwg = (uint32_t)a.mat[m].wg_count;
+  const int wg_begin = a.mat[m].wg_begin;
+  const int wg_count = a.mat[m].wg_count;
+  const int mat_nsl = a.mat[m].nsl;
+  const uint32_t wg = (uint32_t)blockIdx.x - (uint32_t)wg_begin;
+  const uint32_t nwg = (uint32_t)wg_count;
 
   uint8_t* xl = smem + a.cb_bytes;
   float* red = reinterpret_cast<float*>(smem + a.cb_bytes + a.x_bytes);  // [Q * NRW][P]
@@ -371,7 +378,7 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
   // j + 16 * (j / 4), register j % 4
   const bool on_diag = (j >> 2) == g;
   const int diag_reg = j & 3;
-  const int nsl = MODE == CB_SLICE ? a.mat[m].nsl : 1;
+  const int nsl = MODE == CB_SLICE ? mat_nsl : 1;
 
   for (int si = 0; si < nsl; ++si) {
     Slice sl;

@@ -159,8 +159,10 @@ namespace fasq {
 template <int BITS, int D, int T, int MODE>
 hipError_t launch_gemv_m1_variant(const GemvM1Args& a, bool mask, int threads, int blocks, int lds,
                                   hipStream_t stream) {
-  auto kern = mask ? k_gemv_m1<BITS, D, T, MODE, true> : k_gemv_m1<BITS, D, T, MODE, false>;
-  if (plan_record("k_gemv_m1", {BITS, D, T, MODE, mask ? 1 : 0})) return hipSuccess;
+  const bool one = a.mat[1].wg_begin == 0x7fffffff;  // a single matrix
+  auto kern = mask ? (one ? k_gemv_m1<BITS, D, T, MODE, true, 1> : k_gemv_m1<BITS, D, T, MODE, true, kM1MaxMats>)
+                   : (one ? k_gemv_m1<BITS, D, T, MODE, false, 1> : k_gemv_m1<BITS, D, T, MODE, false, kM1MaxMats>);
+  if (plan_record("k_gemv_m1", {BITS, D, T, MODE, mask ? 1 : 0, one ? 1 : kM1MaxMats})) return hipSuccess;
   hipError_t e = prepare_kernel(kern);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, dim3(blocks), dim3(threads), lds, stream, a);
@@ -324,7 +326,7 @@ hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& d
   a.cb_bytes = cb_bytes;
   a.x_bytes = (int)x_bytes;
   a.sl_shift = sl_shift;
-  a.nmat = count;
+  for (int i = count; i < kM1MaxMats; ++i) a.mat[i].wg_begin = 0x7fffffff;  // never selected
   int64_t begin = 0;
   for (int i = 0; i < count; ++i) {
     GemvM1Mat& mt = a.mat[i];

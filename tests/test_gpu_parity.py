@@ -519,6 +519,8 @@ def test_lut_gemm_rejects_tables_larger_than_lds():
 def test_codebook_placement_follows_the_work_per_workgroup():
     """Few ids per workgroup: one LDS copy of the codebook (mode 1); many: the
     replicated table (mode 0)."""
-    assert fasq.plan("gemv", 1, 256, 128, 8, 4, 256) == "k_gemv_m1<8, 4, 1, 1, 1>"
-    assert fasq.plan("gemv", 1, 4096, 4096, 8, 2, 256) == "k_gemv_m1<8, 2, 2, 0, 0>"
+    assert fasq.plan("gemv", 1, 256, 128, 8, 4, 256) == "k_gemv_m1<8, 4, 1, 1, 1, 1>"
+    assert fasq.plan("gemv", 1, 4096, 4096, 8, 2, 256) == "k_gemv_m1<8, 2, 2, 0, 0, 1>"
+    assert fasq.plan("gemv_batched", 1, 4096, 4096, 8, 2, 256) == "k_gemv_m1<8, 2, 2, 0, 0, 4>"
+    assert fasq.plan("gemv_batched", 4, 4096, 4096, 8, 2, 256).startswith("k_gemv<")
     assert fasq.plan("gemv", 1, 320, 20000, 8, 4, 256).startswith("k_gemv_m1<8, 4, 1, 0, ")
