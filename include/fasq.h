@@ -99,7 +99,7 @@ fasq_status fasq_pq_gemv(const void* x, int64_t M, int64_t K, int64_t N,
  * with W_hat_i given by idx[i] (N[i] rows of fasq_idx_row_bytes(K, d,
  * idx_bits) bytes) and codebook[i] (fp16 [C[i] x d]).  x, M, K, idx_bits and d
  * are shared; every array holds `count` entries and lives in HOST memory,
- * while the buffers it points to are device memory.  For M = 1 up to four
+ * while the buffers it points to are device memory.  For M = 1 up to eight
  * matrices run in one launch; otherwise, or when the grouped kernel does not
  * apply, the matrices are computed one call after another.  Every y[i] is
  * bit-for-bit what fasq_pq_gemv would write for matrix i alone.
@@ -244,7 +244,7 @@ int fasq_abi_version(void);
  * Diagnostic: the name of the kernel instantiation that fasq_pq_gemv
  * (regime 0), fasq_pq_gemm (regime 1) or fasq_pq_gemv_batched over two or
  * more matrices of these sizes (regime 2) would launch with 16-byte-aligned
- * buffers, e.g. "k_gemv_m1<8, 2, 2, 0, 0, 1>" (template arguments in
+ * buffers, e.g. "k_gemv_m1<8, 2, 2, 0, 0>" (template arguments in
  * declaration order).  Launches nothing; needs a current HIP
  * device.  Returns "" for invalid arguments or when no device is available.
  * The string is thread-local and valid until the thread's next fasq_* call.

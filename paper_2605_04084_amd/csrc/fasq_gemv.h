@@ -271,20 +271,19 @@ namespace fasq {
 // matrix core does 16x the useful MACs, which it has to spare at decode
 // arithmetic intensity.
 // ---------------------------------------------------------------------------
-// One matrix of a single-token launch.  Workgroups [wg_begin, wg_begin +
-// wg_count) of the grid work on it.
-struct GemvM1Mat {
-  const uint8_t* idx;
+// One part of a single-token launch: a range of rows of one matrix (its ids,
+// its codebook, its outputs).  Grid row blockIdx.y works on part blockIdx.y;
+// every part has gridDim.x workgroups.
+struct GemvM1Part {
+  const uint8_t* idx;  // first id row of the part
   const half_t* cb;
-  half_t* y;
-  int64_t N;
+  half_t* y;           // output of the part's first row
+  int64_t N;           // rows of the part
   int C;
-  int wg_begin;
-  int wg_count;
   int nsl;  // CB_SLICE: codebook slices (passes over the rows)
 };
 
-constexpr int kM1MaxMats = 4;  // matrices one single-token launch can take
+constexpr int kM1MaxParts = 8;  // parts one single-token launch can take
 
 struct GemvM1Args {
   const half_t* x;  // shared by every matrix of the launch
@@ -296,12 +295,11 @@ struct GemvM1Args {
   int cb_bytes;  // LDS bytes of the codebook (x follows)
   int x_bytes;   // LDS bytes of x (partials follow)
   int sl_shift;  // CB_SLICE: log2 of the entries per slice
-  GemvM1Mat mat[kM1MaxMats];
+  int wpp;       // workgroups per part (the grid's x size)
+  GemvM1Part part[kM1MaxParts];
 };
 
-// NM: matrix slots the workgroups choose from (1 for a single matrix,
-// kM1MaxMats for a grouped launch).
-template <int BITS, int D, int T, int MODE, bool MASK, int NM>
+template <int BITS, int D, int T, int MODE, bool MASK>
 __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
   constexpr int G = Chunk<BITS>::G;
   constexpr int DW = Chunk<BITS>::DW;
@@ -315,24 +313,18 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
 
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
-  // The matrix of this workgroup, and the workgroup's place among its own.
-  // Unused slots have wg_begin = INT_MAX and are never chosen, so all the
-  // range tests load at once; a single-matrix launch reads slot 0 directly,
-  // in the same batch of scalar loads as the other arguments.
-  int m = 0;
-#pragma unroll
-  for (int i = 1; i < NM; ++i)
-    if ((int)blockIdx.x >= a.mat[i].wg_begin) m = i;
-  const uint8_t* __restrict__ idx = a.mat[m].idx;
-  const half_t* __restrict__ cb = a.mat[m].cb;
-  half_t* __restrict__ y = a.mat[m].y;
-  const int64_t N = a.mat[m].N;
-  const int C = a.mat[m].C;
-  const int wg_begin = a.mat[m].wg_begin;
-  const int wg_count = a.mat[m].wg_count;
-  const int mat_nsl = a.mat[m].nsl;
-  const uint32_t wg = (uint32_t)blockIdx.x - (uint32_t)wg_begin;
-  const uint32_t nwg = (uint32_t)wg_count;
+  // The part of this workgroup comes from the grid position alone, so its
+  // arguments load in the same batch as the others: choosing it by the
+  // value of an argument would cost one more memory round trip before the
+  // first index load.
+  const GemvM1Part& pt = a.part[blockIdx.y];
+  const uint8_t* __restrict__ idx = pt.idx;
+  const half_t* __restrict__ cb = pt.cb;
+  half_t* __restrict__ y = pt.y;
+  const int64_t N = pt.N;
+  const int C = pt.C;
+  const uint32_t wg = blockIdx.x;
+  const uint32_t nwg = (uint32_t)a.wpp;
 
   uint8_t* xl = smem + a.cb_bytes;
   float* red = reinterpret_cast<float*>(smem + a.cb_bytes + a.x_bytes);  // [Q * NRW][P]
@@ -378,7 +370,7 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
   // j + 16 * (j / 4), register j % 4
   const bool on_diag = (j >> 2) == g;
   const int diag_reg = j & 3;
-  const int nsl = MODE == CB_SLICE ? mat_nsl : 1;
+  const int nsl = MODE == CB_SLICE ? pt.nsl : 1;
 
   for (int si = 0; si < nsl; ++si) {
     Slice sl;

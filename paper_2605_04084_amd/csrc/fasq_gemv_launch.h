@@ -12,7 +12,7 @@ constexpr int kLdsCodebookBudget = 64 * 1024;  // bytes of LDS a codebook may ta
 constexpr int kSliceReserve = 8 * 1024;        // LDS kept for row partials beside a codebook slice
 constexpr int kMinSliceBytes = 32 * 1024;      // smaller slices: gather from global memory instead
 constexpr int kReplMinIdsPerEntry = 16;        // replicate the codebook only above this many ids per workgroup and entry
-static_assert(kM1MaxMats == kMaxBatchLaunch, "grouped launches and their kernel disagree on the group size");
+static_assert(kMaxBatchLaunch <= kM1MaxParts, "a grouped launch needs a part per matrix at least");
 
 // Codebook placement for a call: replicated in LDS when the replicated table
 // fits the budget, one copy in LDS when that fits, else global memory.
@@ -157,39 +157,37 @@ hipError_t launch_gemv_bits(const Problem& p, const DeviceInfo& dev, hipStream_t
 namespace fasq {
 
 template <int BITS, int D, int T, int MODE>
-hipError_t launch_gemv_m1_variant(const GemvM1Args& a, bool mask, int threads, int blocks, int lds,
+hipError_t launch_gemv_m1_variant(const GemvM1Args& a, bool mask, int threads, dim3 grid, int lds,
                                   hipStream_t stream) {
-  const bool one = a.mat[1].wg_begin == 0x7fffffff;  // a single matrix
-  auto kern = mask ? (one ? k_gemv_m1<BITS, D, T, MODE, true, 1> : k_gemv_m1<BITS, D, T, MODE, true, kM1MaxMats>)
-                   : (one ? k_gemv_m1<BITS, D, T, MODE, false, 1> : k_gemv_m1<BITS, D, T, MODE, false, kM1MaxMats>);
-  if (plan_record("k_gemv_m1", {BITS, D, T, MODE, mask ? 1 : 0, one ? 1 : kM1MaxMats})) return hipSuccess;
+  auto kern = mask ? k_gemv_m1<BITS, D, T, MODE, true> : k_gemv_m1<BITS, D, T, MODE, false>;
+  if (plan_record("k_gemv_m1", {BITS, D, T, MODE, mask ? 1 : 0})) return hipSuccess;
   hipError_t e = prepare_kernel(kern);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3(blocks), dim3(threads), lds, stream, a);
+  hipLaunchKernelGGL(kern, grid, dim3(threads), lds, stream, a);
   return hipGetLastError();
 }
 
 template <int BITS, int D, int MODE>
-hipError_t launch_gemv_m1_t(const GemvM1Args& a, int T, bool mask, int threads, int blocks, int lds,
+hipError_t launch_gemv_m1_t(const GemvM1Args& a, int T, bool mask, int threads, dim3 grid, int lds,
                             hipStream_t stream) {
   switch (T) {
-    case 1: return launch_gemv_m1_variant<BITS, D, 1, MODE>(a, mask, threads, blocks, lds, stream);
-    case 2: return launch_gemv_m1_variant<BITS, D, 2, MODE>(a, mask, threads, blocks, lds, stream);
-    case 4: return launch_gemv_m1_variant<BITS, D, 4, MODE>(a, mask, threads, blocks, lds, stream);
-    default: return launch_gemv_m1_variant<BITS, D, 8, MODE>(a, mask, threads, blocks, lds, stream);
+    case 1: return launch_gemv_m1_variant<BITS, D, 1, MODE>(a, mask, threads, grid, lds, stream);
+    case 2: return launch_gemv_m1_variant<BITS, D, 2, MODE>(a, mask, threads, grid, lds, stream);
+    case 4: return launch_gemv_m1_variant<BITS, D, 4, MODE>(a, mask, threads, grid, lds, stream);
+    default: return launch_gemv_m1_variant<BITS, D, 8, MODE>(a, mask, threads, grid, lds, stream);
   }
 }
 
 template <int BITS, int D>
-hipError_t launch_gemv_m1_mode(const GemvM1Args& a, int mode, int T, bool mask, int threads, int blocks, int lds,
+hipError_t launch_gemv_m1_mode(const GemvM1Args& a, int mode, int T, bool mask, int threads, dim3 grid, int lds,
                                hipStream_t stream) {
   switch (mode) {
-    case CB_REPL: return launch_gemv_m1_t<BITS, D, CB_REPL>(a, T, mask, threads, blocks, lds, stream);
-    case CB_LDS: return launch_gemv_m1_t<BITS, D, CB_LDS>(a, T, mask, threads, blocks, lds, stream);
+    case CB_REPL: return launch_gemv_m1_t<BITS, D, CB_REPL>(a, T, mask, threads, grid, lds, stream);
+    case CB_LDS: return launch_gemv_m1_t<BITS, D, CB_LDS>(a, T, mask, threads, grid, lds, stream);
     case CB_SLICE:  // only 16-bit ids address codebooks larger than LDS
-      if constexpr (BITS == 16) return launch_gemv_m1_t<BITS, D, CB_SLICE>(a, T, mask, threads, blocks, lds, stream);
+      if constexpr (BITS == 16) return launch_gemv_m1_t<BITS, D, CB_SLICE>(a, T, mask, threads, grid, lds, stream);
       else return hipErrorNotSupported;
-    default: return launch_gemv_m1_t<BITS, D, CB_GLOBAL>(a, T, mask, threads, blocks, lds, stream);
+    default: return launch_gemv_m1_t<BITS, D, CB_GLOBAL>(a, T, mask, threads, grid, lds, stream);
   }
 }
 
@@ -202,7 +200,7 @@ template <int BITS>
 hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream) {
   constexpr int G = Chunk<BITS>::G;
   constexpr int CBY = Chunk<BITS>::DW * 4;
-  if (count < 1 || count > kM1MaxMats) return hipErrorNotSupported;
+  if (count < 1 || count > kM1MaxParts) return hipErrorNotSupported;
   const Problem& p = ps[0];
   const int d = p.d;
   if (p.M != 1) return hipErrorNotSupported;
@@ -266,53 +264,62 @@ hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& d
   const int64_t avail = dev.lds_per_block - cb_bytes - x_bytes;
 
   // Q row groups per workgroup: enough workgroups to cover every CU for
-  // small N, up to 16 waves per workgroup.  Workgroups are shared out in
-  // proportion to the rows of each matrix, one per CU in all.
+  // small N, up to 16 waves per workgroup.
   const int64_t ncu = dev.num_cus;
   int64_t Q = (total_rows + ncu - 1) / ncu;
   if (Q > 16 / P) Q = 16 / P;
   if (Q < 1) Q = 1;
-  int64_t wgs[kM1MaxMats];
-  int64_t used = 0;
-  for (int i = 0; i < count; ++i) {
-    int64_t w = ncu * ps[i].N / total_rows;
-    const int64_t cap = (ps[i].N + Q - 1) / Q;  // no workgroup without a row group
-    if (w > cap) w = cap;
-    if (w < 1) w = 1;
-    wgs[i] = w;
-    used += w;
-  }
-  // hand the remaining CUs to the matrices with the most rows per workgroup
-  while (used < ncu) {
-    int best = -1;
-    int64_t best_load = 0;
+
+  // Parts: matrix i is cut into cuts[i] ranges of near-equal row counts, and
+  // every part gets the same number of workgroups (the grid's x size; its y
+  // size counts the parts).  Cut where it makes the most rows per workgroup
+  // smallest, with about one workgroup per CU in all.
+  auto part_rows = [&](const int* cuts) {
+    int64_t r = 0;
     for (int i = 0; i < count; ++i) {
-      const int64_t load = (ps[i].N + wgs[i] - 1) / wgs[i];
-      if (wgs[i] < (ps[i].N + Q - 1) / Q && load > best_load) { best = i; best_load = load; }
+      const int64_t ri = (ps[i].N + cuts[i] - 1) / cuts[i];
+      if (ri > r) r = ri;
     }
-    if (best < 0) break;
-    ++wgs[best];
-    ++used;
+    return r;
+  };
+  int cuts[kM1MaxParts], best[kM1MaxParts];
+  for (int i = 0; i < count; ++i) cuts[i] = best[i] = 1;
+  int nparts = count, best_parts = count;
+  double best_cost = (double)part_rows(cuts) / (double)(ncu / count > 0 ? ncu / count : 1);
+  while (nparts < kM1MaxParts) {
+    int j = -1;  // cut the matrix with the largest parts once more
+    int64_t jr = 1;
+    for (int i = 0; i < count; ++i) {
+      const int64_t ri = (ps[i].N + cuts[i] - 1) / cuts[i];
+      if (cuts[i] < ps[i].N && ri > jr) { j = i; jr = ri; }
+    }
+    if (j < 0) break;
+    ++cuts[j];
+    ++nparts;
+    const double cost = (double)part_rows(cuts) / (double)(ncu / nparts > 0 ? ncu / nparts : 1);
+    if (cost < best_cost) {
+      best_cost = cost;
+      best_parts = nparts;
+      for (int i = 0; i < count; ++i) best[i] = cuts[i];
+    }
   }
-  int64_t nrw = 1;
-  for (int i = 0; i < count; ++i) {
-    const int64_t r = (ps[i].N + wgs[i] * Q - 1) / (wgs[i] * Q);
-    if (r > nrw) nrw = r;
-  }
+  nparts = best_parts;
+  const int64_t max_rows = part_rows(best);
+  int64_t wpp = ncu / nparts;  // workgroups per part
+  if (wpp > (max_rows + Q - 1) / Q) wpp = (max_rows + Q - 1) / Q;  // no workgroup without a row group
+  if (wpp < 1) wpp = 1;
+  int64_t nrw = (max_rows + wpp * Q - 1) / (wpp * Q);
   const int64_t nrw_max = avail / (4 * Q * P);
   if (nrw_max < 1) return hipErrorNotSupported;
   if (nrw > nrw_max) {  // LDS bound: more workgroups than CUs
     nrw = nrw_max;
-    for (int i = 0; i < count; ++i) wgs[i] = (ps[i].N + nrw * Q - 1) / (nrw * Q);
+    wpp = (max_rows + nrw * Q - 1) / (nrw * Q);
   }
-  int64_t nwg = 0;
-  for (int i = 0; i < count; ++i) {
-    // 32-bit buffer offsets must cover every row the pipeline reads, including
-    // the rows it reads ahead past the last one (those load zeros).
-    if ((wgs[i] * Q * (nrw + kGemvPipe / T + 1)) * ps[i].R >= (int64_t(1) << 32)) return hipErrorNotSupported;
-    nwg += wgs[i];
-  }
-  if (nwg > 0x7fffffff || nrw * T > 0x7fffffff) return hipErrorNotSupported;
+  // 32-bit buffer offsets must cover every row the pipeline reads, including
+  // the rows it reads ahead past the last one (those load zeros).
+  for (int i = 0; i < count; ++i)
+    if ((wpp * Q * (nrw + kGemvPipe / T + 1)) * ps[i].R >= (int64_t(1) << 32)) return hipErrorNotSupported;
+  if (wpp > 0x7fffffff || nrw * T > 0x7fffffff) return hipErrorNotSupported;
   const int lds = (int)(cb_bytes + x_bytes + Q * nrw * P * 4);
   const int threads = (int)(P * Q * kWave);
 
@@ -326,25 +333,29 @@ hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& d
   a.cb_bytes = cb_bytes;
   a.x_bytes = (int)x_bytes;
   a.sl_shift = sl_shift;
-  for (int i = count; i < kM1MaxMats; ++i) a.mat[i].wg_begin = 0x7fffffff;  // never selected
-  int64_t begin = 0;
+  a.wpp = (int)wpp;
+  int k = 0;
   for (int i = 0; i < count; ++i) {
-    GemvM1Mat& mt = a.mat[i];
-    mt.idx = static_cast<const uint8_t*>(ps[i].idx);
-    mt.cb = static_cast<const half_t*>(ps[i].codebook);
-    mt.y = static_cast<half_t*>(ps[i].y);
-    mt.N = ps[i].N;
-    mt.C = (int)ps[i].C;
-    mt.wg_begin = (int)begin;
-    mt.wg_count = (int)wgs[i];
-    mt.nsl = mode == CB_SLICE ? (int)((ps[i].C + (int64_t(1) << sl_shift) - 1) >> sl_shift) : 1;
-    begin += wgs[i];
+    const int64_t base = ps[i].N / best[i], extra = ps[i].N % best[i];
+    int64_t row = 0;
+    for (int c = 0; c < best[i]; ++c, ++k) {
+      const int64_t rows = base + (c < extra ? 1 : 0);
+      GemvM1Part& pt = a.part[k];
+      pt.idx = static_cast<const uint8_t*>(ps[i].idx) + row * ps[i].R;
+      pt.cb = static_cast<const half_t*>(ps[i].codebook);
+      pt.y = static_cast<half_t*>(ps[i].y) + row;
+      pt.N = rows;
+      pt.C = (int)ps[i].C;
+      pt.nsl = mode == CB_SLICE ? (int)((ps[i].C + (int64_t(1) << sl_shift) - 1) >> sl_shift) : 1;
+      row += rows;
+    }
   }
+  const dim3 grid((unsigned)wpp, (unsigned)nparts);
   switch (d) {
-    case 1: return launch_gemv_m1_mode<BITS, 1>(a, mode, T, mask, threads, (int)nwg, lds, stream);
-    case 2: return launch_gemv_m1_mode<BITS, 2>(a, mode, T, mask, threads, (int)nwg, lds, stream);
-    case 4: return launch_gemv_m1_mode<BITS, 4>(a, mode, T, mask, threads, (int)nwg, lds, stream);
-    default: return launch_gemv_m1_mode<BITS, 8>(a, mode, T, mask, threads, (int)nwg, lds, stream);
+    case 1: return launch_gemv_m1_mode<BITS, 1>(a, mode, T, mask, threads, grid, lds, stream);
+    case 2: return launch_gemv_m1_mode<BITS, 2>(a, mode, T, mask, threads, grid, lds, stream);
+    case 4: return launch_gemv_m1_mode<BITS, 4>(a, mode, T, mask, threads, grid, lds, stream);
+    default: return launch_gemv_m1_mode<BITS, 8>(a, mode, T, mask, threads, grid, lds, stream);
   }
 }
 

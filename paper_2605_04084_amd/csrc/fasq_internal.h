@@ -44,7 +44,7 @@ hipError_t launch_gemv(const Problem& p, const DeviceInfo& dev, hipStream_t stre
 // M = 1 and the same x, K, d and id width; at most 8).  hipErrorNotSupported
 // (without launching) when the tuned kernel does not apply to the group.
 hipError_t launch_gemv_m1_group(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream);
-constexpr int kMaxBatchLaunch = 4;  // matrices per grouped launch
+constexpr int kMaxBatchLaunch = 8;  // matrices per grouped launch
 
 // Tuned MFMA prefill kernel.  hipErrorNotSupported when no variant applies.
 hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t stream);

@@ -330,6 +330,8 @@ BATCH_CASES = [
     (1, 512, 4, 12, [(100, 4096), (33, 4096), (257, 1000)]),
     (1, 320, 4, 16, [(64, 65536), (65, 300)]),
     (1, 256, 2, 8, [(40 + 7 * i, 256) for i in range(11)]),        # more than one launch's worth
+    (1, 1024, 2, 8, [(5000, 256), (3, 256)]),                      # a large matrix cut in uneven parts
+    (1, 640, 4, 12, [(2049, 4096), (700, 4096), (1, 4096)]),       # parts of several sizes, one 1-row matrix
     (3, 256, 2, 8, [(70, 256), (130, 256)]),                       # M > 1: one call per matrix
     (1, 96, 3, 8, [(20, 7), (9, 5)]),                              # d = 3: general kernel
 ]
@@ -519,8 +521,8 @@ def test_lut_gemm_rejects_tables_larger_than_lds():
 def test_codebook_placement_follows_the_work_per_workgroup():
     """Few ids per workgroup: one LDS copy of the codebook (mode 1); many: the
     replicated table (mode 0)."""
-    assert fasq.plan("gemv", 1, 256, 128, 8, 4, 256) == "k_gemv_m1<8, 4, 1, 1, 1, 1>"
-    assert fasq.plan("gemv", 1, 4096, 4096, 8, 2, 256) == "k_gemv_m1<8, 2, 2, 0, 0, 1>"
-    assert fasq.plan("gemv_batched", 1, 4096, 4096, 8, 2, 256) == "k_gemv_m1<8, 2, 2, 0, 0, 4>"
+    assert fasq.plan("gemv", 1, 256, 128, 8, 4, 256) == "k_gemv_m1<8, 4, 1, 1, 1>"
+    assert fasq.plan("gemv", 1, 4096, 4096, 8, 2, 256) == "k_gemv_m1<8, 2, 2, 0, 0>"
+    assert fasq.plan("gemv_batched", 1, 4096, 4096, 8, 2, 256) == "k_gemv_m1<8, 2, 2, 0, 0>"
     assert fasq.plan("gemv_batched", 4, 4096, 4096, 8, 2, 256).startswith("k_gemv<")
     assert fasq.plan("gemv", 1, 320, 20000, 8, 4, 256).startswith("k_gemv_m1<8, 4, 1, 0, ")
