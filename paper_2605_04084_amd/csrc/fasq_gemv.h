@@ -26,6 +26,8 @@
 //     would wait for them.
 #pragma once
 
+#include <type_traits>
+
 #include "fasq_codebook.h"
 #include "fasq_device.h"
 
@@ -405,6 +407,9 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
     // waits for the small staging data alone, not for the whole workgroup to
     // get its loads accepted by a saturated memory queue.
     __syncthreads();
+    // (issued whether or not the wave has that many units: these loads go
+    // out first and return with the others, and a test here would make the
+    // staging below wait for them)
 #pragma unroll
     for (int i = 0; i < kM1EarlyLoads; ++i) load_unit(i, row0 + (uint32_t)(i / T) * rstride, i % T);
 
@@ -476,20 +481,48 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
     // Unit k lives in slot k % L, and kM1Window loads stay in flight.  A
     // wave computes a unit before it issues the next load, so data that has
     // arrived is never held up behind a load waiting for room in the memory
-    // queue.  First window: units below kM1EarlyLoads are already in flight.
+    // queue.  Units below kM1EarlyLoads are already in flight.  Groups of L
+    // units whose loads all lie within the wave's units run first; the last
+    // R < L + W units run in code made for R, which issues no load past the
+    // wave's last unit.  Such a load (it would read zeros) still holds the
+    // wave, which ends only once all its loads are back, and it queues behind
+    // the CU's real ones.  (A test around each load instead would make the
+    // compiler wait for every load in flight before each unit.)
     constexpr int W = kM1Window;
-#pragma unroll
-    for (int i = 0; i < L; ++i) {
-      if (i < nunits) compute_unit(i, i, i % T);
-      if (i + W >= kM1EarlyLoads) load_unit((i + W) % L, row0 + (uint32_t)((i + W) / T) * rstride, (i + W) % T);
-    }
-    uint32_t rbase = row0 + (uint32_t)(L / T) * rstride;  // offset of local row base / T
-    for (int base = L; base < nunits; base += L, rbase += (uint32_t)(L / T) * rstride) {
+    static_assert(W == kM1EarlyLoads, "the first group's loads start where the early loads end");
+    constexpr uint32_t kGroupRows = L / T;  // local rows per group of L units
+    int base = 0;
+    uint32_t rbase = row0;  // offset of local row base / T
+    for (; base + L + W <= nunits; base += L, rbase += kGroupRows * rstride) {
 #pragma unroll
       for (int i = 0; i < L; ++i) {
         if (base + i < nunits) compute_unit(i, base + i, i % T);
         load_unit((i + W) % L, rbase + (uint32_t)((i + W) / T) * rstride, (i + W) % T);
       }
+    }
+    auto last = [&](auto rc) __attribute__((always_inline)) {
+      constexpr int R = decltype(rc)::value;
+#pragma unroll
+      for (int i = 0; i < R; ++i) {
+        compute_unit(i % L, base + i, i % T);
+        if (i + W < R) load_unit((i + W) % L, rbase + (uint32_t)((i + W) / T) * rstride, (i + W) % T);
+        // each load stays right after the unit before it (moved past later
+        // units, it would leave the wave fewer loads in flight)
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    static_assert(L + W - 1 <= 10, "one case per possible remainder");
+    switch (nunits - base) {  // 1 .. L + W - 1
+      case 1: last(std::integral_constant<int, 1>{}); break;
+      case 2: last(std::integral_constant<int, 2>{}); break;
+      case 3: if constexpr (L + W > 3) last(std::integral_constant<int, 3>{}); break;
+      case 4: if constexpr (L + W > 4) last(std::integral_constant<int, 4>{}); break;
+      case 5: if constexpr (L + W > 5) last(std::integral_constant<int, 5>{}); break;
+      case 6: if constexpr (L + W > 6) last(std::integral_constant<int, 6>{}); break;
+      case 7: if constexpr (L + W > 7) last(std::integral_constant<int, 7>{}); break;
+      case 8: if constexpr (L + W > 8) last(std::integral_constant<int, 8>{}); break;
+      case 9: if constexpr (L + W > 9) last(std::integral_constant<int, 9>{}); break;
+      default: break;
     }
   }
   __syncthreads();
