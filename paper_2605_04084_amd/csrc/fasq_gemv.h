@@ -478,10 +478,10 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
       }
     };
 
-    // Unit k lives in slot k % L, and kM1Window loads stay in flight.  A
-    // wave computes a unit before it issues the next load, so data that has
-    // arrived is never held up behind a load waiting for room in the memory
-    // queue.  Units below kM1EarlyLoads are already in flight.  Groups of L
+    // Unit k lives in slot k % L, and kM1Window loads stay in flight: once
+    // unit k has arrived, the wave issues the load of unit k + W and then
+    // computes unit k, so W loads stay in flight while it computes.  Units
+    // below kM1EarlyLoads are already in flight.  Groups of L
     // units whose loads all lie within the wave's units run first; the last
     // R < L + W units run in code made for R, which issues no load past the
     // wave's last unit.  Such a load (it would read zeros) still holds the
@@ -496,17 +496,17 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
     for (; base + L + W <= nunits; base += L, rbase += kGroupRows * rstride) {
 #pragma unroll
       for (int i = 0; i < L; ++i) {
-        if (base + i < nunits) compute_unit(i, base + i, i % T);
         load_unit((i + W) % L, rbase + (uint32_t)((i + W) / T) * rstride, (i + W) % T);
+        if (base + i < nunits) compute_unit(i, base + i, i % T);
       }
     }
     auto last = [&](auto rc) __attribute__((always_inline)) {
       constexpr int R = decltype(rc)::value;
 #pragma unroll
       for (int i = 0; i < R; ++i) {
-        compute_unit(i % L, base + i, i % T);
         if (i + W < R) load_unit((i + W) % L, rbase + (uint32_t)((i + W) / T) * rstride, (i + W) % T);
-        // each load stays right after the unit before it (moved past later
+        compute_unit(i % L, base + i, i % T);
+        // each load stays before the unit it overlaps (moved past later
         // units, it would leave the wave fewer loads in flight)
         __builtin_amdgcn_sched_barrier(0);
       }
