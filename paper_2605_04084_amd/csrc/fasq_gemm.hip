@@ -18,17 +18,20 @@ hipError_t launch_gemm_variant(const GemmArgs& a, int lds, hipStream_t stream) {
   return hipGetLastError();
 }
 
-// Tile shapes, largest first: 128 x 256 on 2 x 4 waves (half the X re-reads
-// per output, two waves per SIMD), 128 x 128, 64 x 128 and 64 x 64 on 2 x 2
-// waves, with the LDS ring depth of each.  The launcher takes the largest
-// tile whose grid covers at least 3/4 of the CUs, else the smallest.  The
-// 64-row tiles (small grids) also split K over KG groups of waves inside the
-// workgroup, with a shallower ring per group.
+// Tile shapes, largest first: 256 x 256 and 128 x 256 on 2 x 4 waves (two
+// waves per SIMD; 128 x 64 and 64 x 64 per wave), 128 x 128, 64 x 128 and
+// 64 x 64 on 2 x 2 waves, with the LDS ring depth of each.  The launcher
+// takes the largest tile whose grid covers at least 3/4 of the CUs, else the
+// smallest.  A 128 x 64 wave tile reads 0.75 KB of LDS operands per MFMA
+// against 1 KB for 64 x 64, which lifts the LDS-bound MFMA loop; its ring
+// leaves no room for the replicated codebook, so it gathers from one copy.
+// The 64-row tiles (small grids) also split K over KG groups of waves inside
+// the workgroup, with a shallower ring per group.
 struct GemmTileShape {
   int bm, bn, ns;
 };
-constexpr GemmTileShape kGemmTiles[] = {{128, 256, 4}, {128, 128, 4}, {64, 128, 8}, {64, 64, 8}};
-constexpr int kGemmNumTiles = 4;
+constexpr GemmTileShape kGemmTiles[] = {{256, 256, 3}, {128, 256, 4}, {128, 128, 4}, {64, 128, 8}, {64, 64, 8}};
+constexpr int kGemmNumTiles = 5;
 // K groups tried for the 64-row tiles, in order.  Two groups (two waves per
 // SIMD) with the replicated codebook measured best; four groups only fit
 // with one codebook copy, whose bank conflicts cost more than they gain.
@@ -36,9 +39,14 @@ constexpr int kGemmSplitGroups[] = {2, 1};
 inline int gemm_group_ring(int kg, int ns) { return kg == 1 ? ns : kg == 2 ? 4 : 3; }
 
 inline int gemm_tile_waves(int t) { return kGemmTiles[t].bn == 256 ? 8 : 4; }
+// The 256 x 256 tile keeps its operands in registers only when few ids make
+// a K step: d >= 4 with 8- or 12-bit ids (the others spill).
+constexpr bool gemm_big_tile_fits(int bits, int d) { return d >= 4 && bits <= 12; }
 
-// Whether tile t splits the id copies evenly over its waves.
-inline bool gemm_tile_ok(int t, int hb) {
+// Whether tile t splits the id copies evenly over its waves (and, for the
+// 256 x 256 tile, fits the registers).
+inline bool gemm_tile_ok(int t, int hb, int bits, int d) {
+  if (t == 0 && !gemm_big_tile_fits(bits, d)) return false;
   return (kGemmTiles[t].bn * (2 * hb / 4)) % (gemm_tile_waves(t) * kWave) == 0;
 }
 
@@ -54,16 +62,20 @@ template <int BITS, int D, int MODE>
 hipError_t launch_gemm_tile(const GemmArgs& a, int tile, int kg, int lds, hipStream_t stream) {
   constexpr int IW = 2 * gemm_run_bytes<BITS, D>() / 4;
   switch (tile) {
-    case 0: return launch_gemm_variant<BITS, D, MODE, 128, 256, 2, 4, kGemmTiles[0].ns, 1>(a, lds, stream);
-    case 2:
-      if constexpr ((128 * IW) % 256 == 0)
-        return launch_gemm_groups<BITS, D, MODE, 64, 128, kGemmTiles[2].ns>(a, kg, lds, stream);
+    case 0:
+      if constexpr (gemm_big_tile_fits(BITS, D))
+        return launch_gemm_variant<BITS, D, MODE, 256, 256, 2, 4, kGemmTiles[0].ns, 1>(a, lds, stream);
       else return hipErrorNotSupported;
+    case 1: return launch_gemm_variant<BITS, D, MODE, 128, 256, 2, 4, kGemmTiles[1].ns, 1>(a, lds, stream);
     case 3:
-      if constexpr ((64 * IW) % 256 == 0)
-        return launch_gemm_groups<BITS, D, MODE, 64, 64, kGemmTiles[3].ns>(a, kg, lds, stream);
+      if constexpr ((128 * IW) % 256 == 0)
+        return launch_gemm_groups<BITS, D, MODE, 64, 128, kGemmTiles[3].ns>(a, kg, lds, stream);
       else return hipErrorNotSupported;
-    default: return launch_gemm_variant<BITS, D, MODE, 128, 128, 2, 2, kGemmTiles[1].ns, 1>(a, lds, stream);
+    case 4:
+      if constexpr ((64 * IW) % 256 == 0)
+        return launch_gemm_groups<BITS, D, MODE, 64, 64, kGemmTiles[4].ns>(a, kg, lds, stream);
+      else return hipErrorNotSupported;
+    default: return launch_gemm_variant<BITS, D, MODE, 128, 128, 2, 2, kGemmTiles[2].ns, 1>(a, lds, stream);
   }
 }
 
@@ -115,14 +127,20 @@ hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t
   auto tiles_of = [&](int t) {
     return ((p.M + kGemmTiles[t].bm - 1) / kGemmTiles[t].bm) * ((p.N + kGemmTiles[t].bn - 1) / kGemmTiles[t].bn);
   };
+  // The codebook placement of tile t: the call's, or one LDS copy when only
+  // that fits beside the tile's ring (-1: neither fits).
+  auto mode_of = [&](int t) {
+    if (lds_of(t, 1, mode) <= dev.lds_per_block) return mode;
+    if (mode == CB_REPL && lds_of(t, 1, CB_LDS) <= dev.lds_per_block) return (int)CB_LDS;
+    return -1;
+  };
   int tile = -1;
   for (int t = 0; t < kGemmNumTiles && tile < 0; ++t)
-    if (gemm_tile_ok(t, hb) && lds_of(t, 1, mode) <= dev.lds_per_block &&
-        4 * tiles_of(t) >= 3 * (int64_t)dev.num_cus)
-      tile = t;
+    if (gemm_tile_ok(t, hb, p.idx_bits, d) && mode_of(t) >= 0 && 4 * tiles_of(t) >= 3 * (int64_t)dev.num_cus) tile = t;
   for (int t = kGemmNumTiles - 1; t >= 0 && tile < 0; --t)
-    if (gemm_tile_ok(t, hb) && lds_of(t, 1, mode) <= dev.lds_per_block) tile = t;
+    if (gemm_tile_ok(t, hb, p.idx_bits, d) && mode_of(t) >= 0) tile = t;
   if (tile < 0) return hipErrorNotSupported;
+  mode = mode_of(tile);
   // K groups for the 64-row tiles: the first count in kGemmSplitGroups that
   // fits, with the replicated codebook or, failing that, one copy.
   int kg = 1;

@@ -151,7 +151,37 @@ WIDE_TILE = [
     (1030, 384, 16400, 4, 4096, 12),
     (1100, 256, 16500, 4, 65536, 16),
     (1025, 128, 16390, 8, 256, 8),
+    (1030, 320, 16400, 4, 256, 8),      # the 256 x 256 tile (one codebook copy)
 ]
+
+
+def test_gemm_tile_choice():
+    """Enough 256 x 256 tiles to fill the CUs: the big tile with one codebook
+    copy; fewer: 128 x 256 with the replicated codebook."""
+    assert fasq.plan("gemm", 2048, 4096, 14336, 8, 4, 256).startswith("k_gemm_mfma<8, 4, 1, 256, 256, 2, 4, ")
+    assert fasq.plan("gemm", 2048, 4096, 4096, 8, 4, 256).startswith("k_gemm_mfma<8, 4, 0, 128, 256, 2, 4, ")
+    assert fasq.plan("gemm", 512, 4096, 14336, 8, 4, 256).startswith("k_gemm_mfma<8, 4, 0, 128, 256, 2, 4, ")
+    # sub-vectors of 1 or 2, or 16-bit ids, would spill in the big tile
+    assert fasq.plan("gemm", 2048, 4096, 14336, 8, 2, 256).startswith("k_gemm_mfma<8, 2, 0, 128, 256, ")
+    assert fasq.plan("gemm", 2048, 4096, 14336, 16, 4, 65536).startswith("k_gemm_mfma<16, 4, 2, 128, 256, ")
+
+
+@pytest.mark.parametrize("case", [(777, 448, 12345, 4, 256, 8), (600, 384, 16400, 4, 4096, 12)])
+def test_gemm_big_tile_one_hot_bit_exact(case):
+    """Exact small-integer results on the 256 x 256 tile with ragged M, N and
+    an odd number of K chunks."""
+    M, K, N, d, C, bits = case
+    print(f"[case] gemm big tile {case}", flush=True)
+    assert ", 256, 256, " in fasq.plan("gemm", M, K, N, bits, d, C)
+    rng = np.random.default_rng(5 + sum(case))
+    cb = pi.signed_one_hot_codebook(C, d, rng)
+    ids = rng.integers(0, C, size=(N, K // d))
+    x = pi.ternary_x(rng, M, K)
+    idx = pi.pack_indices(ids, bits)
+    ref = orc.pq_linear(x, idx, bits, d, cb)
+    assert np.abs(ref).max() <= 2048
+    y = to_np(fasq.pq_gemm(to_dev(x), to_dev(idx), bits, d, to_dev(cb))).astype(np.float64)
+    assert np.array_equal(y, ref)
 
 
 @pytest.mark.parametrize("case", WIDE_TILE)
