@@ -30,6 +30,10 @@ hipError_t launch_gemv_m1_group(const Problem* ps, int count, const DeviceInfo& 
 
 hipError_t launch_gemv(const Problem& p, const DeviceInfo& dev, hipStream_t stream) {
   if (p.M == 1) return launch_gemv_m1_group(&p, 1, dev, stream);
+  if (p.M <= kM1MaxTokens) {  // the row-streaming kernel when its codebook fits LDS
+    hipError_t e = launch_gemv_m1_group(&p, 1, dev, stream);
+    if (e != hipErrorNotSupported) return e;
+  }
   if (p.M > 16) return hipErrorNotSupported;
   switch (p.idx_bits) {
     case 8: return launch_gemv_u8_m16(p, dev, stream);
@@ -198,7 +202,7 @@ fasq_status fasq_pq_gemv_batched(const void* x, int64_t M, int64_t K, int count,
       ps[i] = fasq::make_problem(x, M, K, N[off + i], idx[off + i], idx_bits, d, codebook[off + i], C[off + i],
                                  y[off + i]);
     e = hipErrorNotSupported;
-    if (M == 1 && !fasq::force_generic()) e = fasq::launch_gemv_m1_group(ps, n, dev, stream);
+    if (M <= fasq::kM1MaxTokens && !fasq::force_generic()) e = fasq::launch_gemv_m1_group(ps, n, dev, stream);
     if (e == hipErrorNotSupported) {
       for (int i = 0; i < n; ++i) {
         fasq_status s = fasq::run(ps[i], fasq::Regime::kGemv, stream);
@@ -358,7 +362,8 @@ const char* fasq_pq_plan(int regime, int64_t M, int64_t K, int64_t N, int idx_bi
     Problem ps[2] = {p, p};
     fasq::DeviceInfo dev;
     hipError_t e = fasq::device_info(&dev);
-    if (e == hipSuccess && M == 1 && !fasq::force_generic()) e = fasq::launch_gemv_m1_group(ps, 2, dev, nullptr);
+    if (e == hipSuccess && M <= fasq::kM1MaxTokens && !fasq::force_generic())
+      e = fasq::launch_gemv_m1_group(ps, 2, dev, nullptr);
     else e = hipErrorNotSupported;
     s = e == hipSuccess ? FASQ_OK : e == hipErrorNotSupported ? fasq::run(p, fasq::Regime::kGemv, nullptr)
                                                              : FASQ_ERR_HIP;

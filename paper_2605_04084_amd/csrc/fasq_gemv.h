@@ -30,6 +30,7 @@
 
 #include "fasq_codebook.h"
 #include "fasq_device.h"
+#include "fasq_internal.h"
 
 namespace fasq {
 
@@ -279,13 +280,14 @@ namespace fasq {
 struct GemvM1Part {
   const uint8_t* idx;  // first id row of the part
   const half_t* cb;
-  half_t* y;           // output of the part's first row
+  half_t* y;           // output of the part's first row (token 0)
   int64_t N;           // rows of the part
+  int64_t ldy;         // elements between the outputs of consecutive tokens
   int C;
   int nsl;  // CB_SLICE: codebook slices (passes over the rows)
 };
 
-constexpr int kM1MaxParts = 8;  // parts one single-token launch can take
+constexpr int kM1MaxParts = 8;   // parts one single-token launch can take
 
 struct GemvM1Args {
   const half_t* x;  // shared by every matrix of the launch
@@ -298,20 +300,26 @@ struct GemvM1Args {
   int x_bytes;   // LDS bytes of x (partials follow)
   int sl_shift;  // CB_SLICE: log2 of the entries per slice
   int wpp;       // workgroups per part (the grid's x size)
+  int M;         // tokens (rows of x), at most the kernel's MT
   GemvM1Part part[kM1MaxParts];
 };
 
-template <int BITS, int D, int T, int MODE, bool MASK>
-__global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
+// The body of the row-streaming decode kernel for MT token slots: x holds
+// M <= MT rows (the others are zeros), and every codeword gathered feeds MT
+// diagonal MFMAs, one per token.  k_gemv_m1 is the one-token kernel,
+// k_gemv_mt the kernel for two tokens.
+template <int BITS, int D, int T, int MODE, bool MASK, int MT>
+__device__ __forceinline__ void gemv_rows_body(const GemvM1Args& a) {
   constexpr int G = Chunk<BITS>::G;
   constexpr int DW = Chunk<BITS>::DW;
   constexpr int CBY = DW * 4;
   constexpr int SPC = G * D / 8;     // MFMA steps per chunk
+  static_assert(MT == 1 || MODE != CB_SLICE, "sliced codebooks take one token");
   // load slots: the sliced-codebook kernel keeps fewer (its extra state would
   // otherwise spill), the others a full pipeline's worth
   constexpr int L = MODE == CB_SLICE ? (T > 4 ? T : 4) : kGemvPipe;
   static_assert(L % T == 0, "pipeline depth must be a multiple of T");
-  constexpr bool kXInRegs = T * SPC <= 8;
+  constexpr bool kXInRegs = MT * T * SPC <= 8;
 
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
@@ -329,7 +337,7 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
   const uint32_t nwg = (uint32_t)a.wpp;
 
   uint8_t* xl = smem + a.cb_bytes;
-  float* red = reinterpret_cast<float*>(smem + a.cb_bytes + a.x_bytes);  // [Q * NRW][P]
+  float* red = reinterpret_cast<float*>(smem + a.cb_bytes + a.x_bytes);  // [Q * NRW][MT][P]
 
   const int wave = threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
@@ -365,9 +373,11 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
   // CB_SLICE repeats everything from the codebook staging to the end of the
   // row loop once per slice; x is staged once.
   constexpr int XWT = 2;
-  const int xw_total = (int)(a.K / 8);
+  const int xw_total = (int)(a.K / 8) * a.M;  // 16-byte words of x
+  const int xw_slots = (int)(a.K / 8) * MT;   // LDS words of x (token slots past M hold zeros)
+  const uint32_t xtok = (uint32_t)a.K * 2;    // LDS bytes between tokens
   const uint32_t lane_off = repl_lane_off<D>(lane);
-  half8_t xreg[kXInRegs ? T * SPC : 1];
+  half8_t xreg[kXInRegs ? MT * T * SPC : 1];
   // lane l holds D[4g + i][j]; the diagonal element D[j][j] sits in lane
   // j + 16 * (j / 4), register j % 4
   const bool on_diag = (j >> 2) == g;
@@ -394,6 +404,7 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
     if (si == 0) {
 #pragma unroll
       for (int k = 0; k < XWT; ++k) {
+        xst[k] = u32x4{0u, 0u, 0u, 0u};
         if (wave * kWave + k * (int)blockDim.x < xw_total) {
           int w = threadIdx.x + k * blockDim.x;
           w = w < xw_total ? w : xw_total - 1;
@@ -419,62 +430,70 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
 #pragma unroll
       for (int k = 0; k < XWT; ++k) {
         const int w = threadIdx.x + k * blockDim.x;
-        if (w < xw_total) reinterpret_cast<u32x4*>(xl)[w] = xst[k];
+        if (w < xw_slots) reinterpret_cast<u32x4*>(xl)[w] = w < xw_total ? xst[k] : u32x4{0u, 0u, 0u, 0u};
       }
-      for (int w = threadIdx.x + XWT * blockDim.x; w < xw_total; w += blockDim.x)
-        reinterpret_cast<u32x4*>(xl)[w] = reinterpret_cast<const u32x4*>(a.x)[w];
+      for (int w = threadIdx.x + XWT * blockDim.x; w < xw_slots; w += blockDim.x)
+        reinterpret_cast<u32x4*>(xl)[w] = w < xw_total ? reinterpret_cast<const u32x4*>(a.x)[w] : u32x4{0u, 0u, 0u, 0u};
     }
     __syncthreads();
 
     if (si == 0) {
       if constexpr (kXInRegs) {
 #pragma unroll
-        for (int t = 0; t < T; ++t) {
-          const bool ok = !MASK || ccol_raw(t) < CH;
+        for (int m = 0; m < MT; ++m) {
 #pragma unroll
-          for (int s = 0; s < SPC; ++s) {
-            const half8_t v = *reinterpret_cast<const half8_t*>(xl + ccol(t) * (G * D * 2) + s * 16);
-            xreg[t * SPC + s] = ok ? v : half8_t{};
+          for (int t = 0; t < T; ++t) {
+            const bool ok = !MASK || ccol_raw(t) < CH;
+#pragma unroll
+            for (int s = 0; s < SPC; ++s) {
+              const half8_t v = *reinterpret_cast<const half8_t*>(xl + m * xtok + ccol(t) * (G * D * 2) + s * 16);
+              xreg[(m * T + t) * SPC + s] = ok ? v : half8_t{};
+            }
           }
         }
       }
     }
 
-    float4_t acc0 = {0.f, 0.f, 0.f, 0.f};
-    float4_t acc1 = {0.f, 0.f, 0.f, 0.f};
+    float4_t acc0[MT], acc1[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) acc0[m] = acc1[m] = float4_t{0.f, 0.f, 0.f, 0.f};
     auto compute_unit = [&](int slot, int u, int t) {
       const uint32_t* w = buf[slot];
       const bool cval = !MASK || ccol_raw(t) < CH;
 #pragma unroll
       for (int s = 0; s < SPC; ++s) {
         half8_t aop = gather8<BITS, D, MODE>(cb, lane_off, w, s * (8 / D), sl);
-        half8_t bop;
-        if constexpr (kXInRegs) bop = xreg[t * SPC + s];
-        else bop = *reinterpret_cast<const half8_t*>(xl + ccol(t) * (G * D * 2) + s * 16);
-        if (MASK && !cval) {
-          aop = half8_t{};
-          bop = half8_t{};
+        if (MASK && !cval) aop = half8_t{};
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+          half8_t bop;
+          if constexpr (kXInRegs) bop = xreg[(m * T + t) * SPC + s];
+          else bop = *reinterpret_cast<const half8_t*>(xl + m * xtok + ccol(t) * (G * D * 2) + s * 16);
+          if (MASK && !cval) bop = half8_t{};
+          if (s & 1) acc1[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc1[m], 0, 0, 0);
+          else acc0[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc0[m], 0, 0, 0);
         }
-        if (s & 1) acc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc1, 0, 0, 0);
-        else acc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc0, 0, 0, 0);
       }
       if (t == T - 1) {
-        const float4_t acc = acc0 + acc1;
-        float v = diag_reg == 0 ? acc[0] : diag_reg == 1 ? acc[1] : diag_reg == 2 ? acc[2] : acc[3];
-        v = on_diag ? v : 0.f;
-        v = group_sum<16>(v);
-        // the four rows of 16 lanes hold partial sums: combine in a fixed order
-        const float sum = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0)) +
-                          __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16)) +
-                          __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32)) +
-                          __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
-        // slices of a row are summed in slice order, each by the same lane
-        if (lane == 0) {
-          float* r = &red[((u / T) * Q + q) * P + p];
-          *r = (MODE == CB_SLICE && si > 0) ? *r + sum : sum;
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+          const float4_t acc = acc0[m] + acc1[m];
+          float v = diag_reg == 0 ? acc[0] : diag_reg == 1 ? acc[1] : diag_reg == 2 ? acc[2] : acc[3];
+          v = on_diag ? v : 0.f;
+          v = group_sum<16>(v);
+          // the four rows of 16 lanes hold partial sums: combine in a fixed order
+          const float sum = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0)) +
+                            __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16)) +
+                            __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32)) +
+                            __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+          // slices of a row are summed in slice order, each by the same lane
+          if (lane == 0) {
+            float* r = &red[(((u / T) * Q + q) * MT + m) * P + p];
+            *r = (MODE == CB_SLICE && si > 0) ? *r + sum : sum;
+          }
+          acc0[m] = float4_t{0.f, 0.f, 0.f, 0.f};
+          acc1[m] = float4_t{0.f, 0.f, 0.f, 0.f};
         }
-        acc0 = float4_t{0.f, 0.f, 0.f, 0.f};
-        acc1 = float4_t{0.f, 0.f, 0.f, 0.f};
       }
     };
 
@@ -528,15 +547,27 @@ __global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
   __syncthreads();
 
   // fixed-order sum over the P waves of each row, one fp16 rounding
-  const int rows = Q * a.NRW;
-  for (int r = threadIdx.x; r < rows; r += blockDim.x) {
+  const int outs = Q * a.NRW * MT;
+  for (int o = threadIdx.x; o < outs; o += blockDim.x) {
+    const int r = o / MT;
+    const int m = o - r * MT;
     const int64_t n = (int64_t)wg + (int64_t)r * nwg;
-    if (n < N) {
+    if (n < N && m < a.M) {
       float sum = 0.f;
-      for (int pp = 0; pp < P; ++pp) sum += red[r * P + pp];
-      y[n] = static_cast<half_t>(sum);
+      for (int pp = 0; pp < P; ++pp) sum += red[o * P + pp];
+      y[(int64_t)m * pt.ldy + n] = static_cast<half_t>(sum);
     }
   }
+}
+
+template <int BITS, int D, int T, int MODE, bool MASK>
+__global__ __launch_bounds__(1024) void k_gemv_m1(GemvM1Args a) {
+  gemv_rows_body<BITS, D, T, MODE, MASK, 1>(a);
+}
+
+template <int BITS, int D, int T, int MODE, bool MASK, int MT>
+__global__ __launch_bounds__(1024) void k_gemv_mt(GemvM1Args a) {
+  gemv_rows_body<BITS, D, T, MODE, MASK, MT>(a);
 }
 
 }  // namespace fasq

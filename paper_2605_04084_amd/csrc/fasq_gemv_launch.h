@@ -156,46 +156,61 @@ hipError_t launch_gemv_bits(const Problem& p, const DeviceInfo& dev, hipStream_t
 
 namespace fasq {
 
-template <int BITS, int D, int T, int MODE>
-hipError_t launch_gemv_m1_variant(const GemvM1Args& a, bool mask, int threads, dim3 grid, int lds,
-                                  hipStream_t stream) {
-  auto kern = mask ? k_gemv_m1<BITS, D, T, MODE, true> : k_gemv_m1<BITS, D, T, MODE, false>;
-  if (plan_record("k_gemv_m1", {BITS, D, T, MODE, mask ? 1 : 0})) return hipSuccess;
+template <typename K>
+hipError_t launch_rows_kernel(K kern, const GemvM1Args& a, int threads, dim3 grid, int lds, hipStream_t stream) {
   hipError_t e = prepare_kernel(kern);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, grid, dim3(threads), lds, stream, a);
   return hipGetLastError();
 }
 
+// mt: token slots (1 or 2); two tokens only with the codebook in LDS.
+template <int BITS, int D, int T, int MODE>
+hipError_t launch_gemv_m1_variant(const GemvM1Args& a, int mt, bool mask, int threads, dim3 grid, int lds,
+                                  hipStream_t stream) {
+  if (mt == 1) {
+    auto kern = mask ? k_gemv_m1<BITS, D, T, MODE, true> : k_gemv_m1<BITS, D, T, MODE, false>;
+    if (plan_record("k_gemv_m1", {BITS, D, T, MODE, mask ? 1 : 0})) return hipSuccess;
+    return launch_rows_kernel(kern, a, threads, grid, lds, stream);
+  }
+  if constexpr (MODE == CB_REPL || MODE == CB_LDS) {
+    if (plan_record("k_gemv_mt", {BITS, D, T, MODE, mask ? 1 : 0, mt})) return hipSuccess;
+    return launch_rows_kernel(mask ? k_gemv_mt<BITS, D, T, MODE, true, 2> : k_gemv_mt<BITS, D, T, MODE, false, 2>, a,
+                              threads, grid, lds, stream);
+  } else {
+    return hipErrorNotSupported;
+  }
+}
+
 template <int BITS, int D, int MODE>
-hipError_t launch_gemv_m1_t(const GemvM1Args& a, int T, bool mask, int threads, dim3 grid, int lds,
+hipError_t launch_gemv_m1_t(const GemvM1Args& a, int mt, int T, bool mask, int threads, dim3 grid, int lds,
                             hipStream_t stream) {
   switch (T) {
-    case 1: return launch_gemv_m1_variant<BITS, D, 1, MODE>(a, mask, threads, grid, lds, stream);
-    case 2: return launch_gemv_m1_variant<BITS, D, 2, MODE>(a, mask, threads, grid, lds, stream);
-    case 4: return launch_gemv_m1_variant<BITS, D, 4, MODE>(a, mask, threads, grid, lds, stream);
-    default: return launch_gemv_m1_variant<BITS, D, 8, MODE>(a, mask, threads, grid, lds, stream);
+    case 1: return launch_gemv_m1_variant<BITS, D, 1, MODE>(a, mt, mask, threads, grid, lds, stream);
+    case 2: return launch_gemv_m1_variant<BITS, D, 2, MODE>(a, mt, mask, threads, grid, lds, stream);
+    case 4: return launch_gemv_m1_variant<BITS, D, 4, MODE>(a, mt, mask, threads, grid, lds, stream);
+    default: return launch_gemv_m1_variant<BITS, D, 8, MODE>(a, mt, mask, threads, grid, lds, stream);
   }
 }
 
 template <int BITS, int D>
-hipError_t launch_gemv_m1_mode(const GemvM1Args& a, int mode, int T, bool mask, int threads, dim3 grid, int lds,
-                               hipStream_t stream) {
+hipError_t launch_gemv_m1_mode(const GemvM1Args& a, int mt, int mode, int T, bool mask, int threads, dim3 grid,
+                               int lds, hipStream_t stream) {
   switch (mode) {
-    case CB_REPL: return launch_gemv_m1_t<BITS, D, CB_REPL>(a, T, mask, threads, grid, lds, stream);
-    case CB_LDS: return launch_gemv_m1_t<BITS, D, CB_LDS>(a, T, mask, threads, grid, lds, stream);
+    case CB_REPL: return launch_gemv_m1_t<BITS, D, CB_REPL>(a, mt, T, mask, threads, grid, lds, stream);
+    case CB_LDS: return launch_gemv_m1_t<BITS, D, CB_LDS>(a, mt, T, mask, threads, grid, lds, stream);
     case CB_SLICE:  // only 16-bit ids address codebooks larger than LDS
-      if constexpr (BITS == 16) return launch_gemv_m1_t<BITS, D, CB_SLICE>(a, T, mask, threads, grid, lds, stream);
+      if constexpr (BITS == 16) return launch_gemv_m1_t<BITS, D, CB_SLICE>(a, mt, T, mask, threads, grid, lds, stream);
       else return hipErrorNotSupported;
-    default: return launch_gemv_m1_t<BITS, D, CB_GLOBAL>(a, T, mask, threads, grid, lds, stream);
+    default: return launch_gemv_m1_t<BITS, D, CB_GLOBAL>(a, mt, T, mask, threads, grid, lds, stream);
   }
 }
 
-// One token, one launch over `count` <= kM1MaxMats matrices that share x, K,
-// d and the id width: choose T (wave-wide loads per row part), P (waves per
-// row), Q (row groups per workgroup), the workgroups of each matrix and the
-// rows per row group; hipErrorNotSupported when another kernel has to take
-// the call.
+// One to kM1MaxTokens tokens, one launch over `count` <= kM1MaxParts
+// matrices that share x, M, K, d and the id width: choose T (wave-wide loads
+// per row part), P (waves per row), Q (row groups per workgroup), the parts
+// and their workgroups and the rows per row group; hipErrorNotSupported when
+// another kernel has to take the call.
 template <int BITS>
 hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream) {
   constexpr int G = Chunk<BITS>::G;
@@ -203,7 +218,8 @@ hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& d
   if (count < 1 || count > kM1MaxParts) return hipErrorNotSupported;
   const Problem& p = ps[0];
   const int d = p.d;
-  if (p.M != 1) return hipErrorNotSupported;
+  if (p.M < 1 || p.M > kM1MaxTokens) return hipErrorNotSupported;
+  const int MT = (int)p.M;  // token slots of the kernel
   if (!(d == 1 || d == 2 || d == 4 || d == 8)) return hipErrorNotSupported;
   if (p.S % G || p.K % 8) return hipErrorNotSupported;
   const int64_t CH = p.S / G;
@@ -212,7 +228,7 @@ hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& d
   int64_t maxC = 0, total_rows = 0;
   for (int i = 0; i < count; ++i) {
     const Problem& pi = ps[i];
-    if (pi.M != 1 || pi.K != p.K || pi.d != d || pi.idx_bits != p.idx_bits || pi.x != p.x) return hipErrorNotSupported;
+    if (pi.M != p.M || pi.K != p.K || pi.d != d || pi.idx_bits != p.idx_bits || pi.x != p.x) return hipErrorNotSupported;
     if (pi.cb_stride != 0) return hipErrorNotSupported;
     if (pi.N * pi.R >= (int64_t(1) << 32)) return hipErrorNotSupported;
     if ((reinterpret_cast<uintptr_t>(pi.idx) & (CBY == 16 ? 15 : 3)) || (reinterpret_cast<uintptr_t>(pi.codebook) & 15))
@@ -223,7 +239,7 @@ hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& d
 
   const int SPC = G * d / 8;
   const int64_t CHW = (CH + 63) / 64;  // wave-wide loads per row
-  const int tx = SPC <= 8 ? 8 / SPC : 0;  // largest T whose x slices fit the register budget
+  const int tx = SPC * MT <= 8 ? 8 / (SPC * MT) : 0;  // largest T whose x slices fit the register budget
   int T = 0;
   for (int t : {8, 4, 2, 1}) {  // exact split, x in registers
     if (t <= tx && CHW % t == 0 && CHW / t <= 16) { T = t; break; }
@@ -250,13 +266,14 @@ hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& d
   // workgroup with few ids to gather is faster with one copy.
   if (mode == CB_REPL && (total_rows + dev.num_cus - 1) / dev.num_cus * p.S < kReplMinIdsPerEntry * maxC)
     mode = CB_LDS;
-  const int64_t x_bytes = (p.K * 2 + 15) / 16 * 16;
+  const int64_t x_bytes = (MT * p.K * 2 + 15) / 16 * 16;
   int sl_shift = 0;
   if (mode == CB_GLOBAL && (maxC * d * 2) % 16 == 0) {
     const int64_t room = dev.lds_per_block - x_bytes - kSliceReserve;
     while (sl_shift < 16 && (int64_t(2) << sl_shift) * d * 2 <= room) ++sl_shift;
     if ((int64_t(1) << sl_shift) * d * 2 >= kMinSliceBytes) mode = CB_SLICE;
   }
+  if (MT > 1 && mode != CB_REPL && mode != CB_LDS) return hipErrorNotSupported;  // several tokens: codebook in LDS
   if (mode != CB_GLOBAL)  // every codebook must be whole 16-byte words to be staged
     for (int i = 0; i < count; ++i)
       if ((ps[i].C * d * 2) % 16 != 0) return hipErrorNotSupported;
@@ -309,7 +326,7 @@ hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& d
   if (wpp > (max_rows + Q - 1) / Q) wpp = (max_rows + Q - 1) / Q;  // no workgroup without a row group
   if (wpp < 1) wpp = 1;
   int64_t nrw = (max_rows + wpp * Q - 1) / (wpp * Q);
-  const int64_t nrw_max = avail / (4 * Q * P);
+  const int64_t nrw_max = avail / (4 * Q * P * MT);
   if (nrw_max < 1) return hipErrorNotSupported;
   if (nrw > nrw_max) {  // LDS bound: more workgroups than CUs
     nrw = nrw_max;
@@ -320,7 +337,7 @@ hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& d
   for (int i = 0; i < count; ++i)
     if ((wpp * Q * (nrw + kGemvPipe / T + 1)) * ps[i].R >= (int64_t(1) << 32)) return hipErrorNotSupported;
   if (wpp > 0x7fffffff || nrw * T > 0x7fffffff) return hipErrorNotSupported;
-  const int lds = (int)(cb_bytes + x_bytes + Q * nrw * P * 4);
+  const int lds = (int)(cb_bytes + x_bytes + Q * nrw * P * MT * 4);
   const int threads = (int)(P * Q * kWave);
 
   GemvM1Args a = {};
@@ -334,6 +351,7 @@ hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& d
   a.x_bytes = (int)x_bytes;
   a.sl_shift = sl_shift;
   a.wpp = (int)wpp;
+  a.M = (int)p.M;
   int k = 0;
   for (int i = 0; i < count; ++i) {
     const int64_t base = ps[i].N / best[i], extra = ps[i].N % best[i];
@@ -345,6 +363,7 @@ hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& d
       pt.cb = static_cast<const half_t*>(ps[i].codebook);
       pt.y = static_cast<half_t*>(ps[i].y) + row;
       pt.N = rows;
+      pt.ldy = ps[i].N;
       pt.C = (int)ps[i].C;
       pt.nsl = mode == CB_SLICE ? (int)((ps[i].C + (int64_t(1) << sl_shift) - 1) >> sl_shift) : 1;
       row += rows;
@@ -352,10 +371,10 @@ hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& d
   }
   const dim3 grid((unsigned)wpp, (unsigned)nparts);
   switch (d) {
-    case 1: return launch_gemv_m1_mode<BITS, 1>(a, mode, T, mask, threads, grid, lds, stream);
-    case 2: return launch_gemv_m1_mode<BITS, 2>(a, mode, T, mask, threads, grid, lds, stream);
-    case 4: return launch_gemv_m1_mode<BITS, 4>(a, mode, T, mask, threads, grid, lds, stream);
-    default: return launch_gemv_m1_mode<BITS, 8>(a, mode, T, mask, threads, grid, lds, stream);
+    case 1: return launch_gemv_m1_mode<BITS, 1>(a, MT, mode, T, mask, threads, grid, lds, stream);
+    case 2: return launch_gemv_m1_mode<BITS, 2>(a, MT, mode, T, mask, threads, grid, lds, stream);
+    case 4: return launch_gemv_m1_mode<BITS, 4>(a, MT, mode, T, mask, threads, grid, lds, stream);
+    default: return launch_gemv_m1_mode<BITS, 8>(a, MT, mode, T, mask, threads, grid, lds, stream);
   }
 }
 

@@ -213,6 +213,10 @@ RAGGED = [
     (1, 36, 5, 4, 9, 12),               # odd 12-bit rows: general kernel
     (1, 30, 7, 3, 11, 8),               # d = 3: general kernel
     (1, 24, 9, 24, 40, 8),              # full vector quantization, d = K
+    (2, 4096, 1000, 2, 256, 8),         # two tokens: the row-streaming kernel
+    (2, 320, 77, 4, 256, 8),            # two tokens, masked chunk tail
+    (2, 128 * 12, 260, 4, 4096, 12),    # two tokens, one codebook copy in LDS
+    (2, 4096, 45, 4, 65536, 16),        # two tokens, codebook larger than LDS: the M <= 16 kernel
     (3, 256, 100, 4, 256, 8),
     (5, 192, 70, 2, 256, 8),
     (17, 640, 200, 4, 256, 8),
@@ -362,7 +366,9 @@ BATCH_CASES = [
     (1, 256, 2, 8, [(40 + 7 * i, 256) for i in range(11)]),        # more than one launch's worth
     (1, 1024, 2, 8, [(5000, 256), (3, 256)]),                      # a large matrix cut in uneven parts
     (1, 640, 4, 12, [(2049, 4096), (700, 4096), (1, 4096)]),       # parts of several sizes, one 1-row matrix
-    (3, 256, 2, 8, [(70, 256), (130, 256)]),                       # M > 1: one call per matrix
+    (2, 4096, 2, 8, [(4096, 256), (1024, 256), (1024, 256)]),      # two tokens, one launch
+    (2, 512, 4, 12, [(300, 4096), (129, 1000)]),                   # two tokens, ragged N, mixed C
+    (3, 256, 2, 8, [(70, 256), (130, 256)]),                       # M > 2: one call per matrix
     (1, 96, 3, 8, [(20, 7), (9, 5)]),                              # d = 3: general kernel
 ]
 
@@ -554,5 +560,7 @@ def test_codebook_placement_follows_the_work_per_workgroup():
     assert fasq.plan("gemv", 1, 256, 128, 8, 4, 256) == "k_gemv_m1<8, 4, 1, 1, 1>"
     assert fasq.plan("gemv", 1, 4096, 4096, 8, 2, 256) == "k_gemv_m1<8, 2, 2, 0, 0>"
     assert fasq.plan("gemv_batched", 1, 4096, 4096, 8, 2, 256) == "k_gemv_m1<8, 2, 2, 0, 0>"
+    assert fasq.plan("gemv_batched", 2, 4096, 4096, 8, 2, 256).startswith("k_gemv_mt<8, 2, ")
+    assert fasq.plan("gemv", 2, 4096, 4096, 8, 2, 256).startswith("k_gemv_mt<8, 2, ")
     assert fasq.plan("gemv_batched", 4, 4096, 4096, 8, 2, 256).startswith("k_gemv<")
     assert fasq.plan("gemv", 1, 320, 20000, 8, 4, 256).startswith("k_gemv_m1<8, 4, 1, 0, ")
