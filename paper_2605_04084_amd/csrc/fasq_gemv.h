@@ -263,18 +263,18 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
 namespace fasq {
 
 // ---------------------------------------------------------------------------
-// One token (M = 1).  Reading 16 rows x 64 bytes per wave-wide load (the
-// layout above) streams at well under half the rate of reading 1 KB of one
-// row, so the single-token kernel maps the MFMA differently: lane l of a
+// One or two tokens (M <= 2).  Reading 16 rows x 64 bytes per wave-wide load
+// (the layout above) streams at well under half the rate of reading 1 KB of
+// one row, so the row-streaming kernels map the MFMA differently: lane l of a
 // wave-wide load holds chunk l of a 1 KB span of ONE weight row (lanes in
 // address order, so every quarter-wave reads 256 contiguous bytes), and the
 // A operand's "row" i is the set of chunks {i, i + 16, i + 32, i + 48} (K
 // group g = chunk / 16).  B carries the x slice of each lane's own chunk, so
-// the wanted partial sums are the diagonal of the 16 x 16 result.  The
-// matrix core does 16x the useful MACs, which it has to spare at decode
-// arithmetic intensity.
+// the wanted partial sums are the diagonal of the 16 x 16 result (one MFMA
+// per token).  The matrix core does 16x the useful MACs, which it has to
+// spare at decode arithmetic intensity.
 // ---------------------------------------------------------------------------
-// One part of a single-token launch: a range of rows of one matrix (its ids,
+// One part of a row-streaming launch: a range of rows of one matrix (its ids,
 // its codebook, its outputs).  Grid row blockIdx.y works on part blockIdx.y;
 // every part has gridDim.x workgroups.
 struct GemvM1Part {
@@ -287,7 +287,7 @@ struct GemvM1Part {
   int nsl;  // CB_SLICE: codebook slices (passes over the rows)
 };
 
-constexpr int kM1MaxParts = 8;   // parts one single-token launch can take
+constexpr int kM1MaxParts = 8;   // parts one row-streaming launch can take
 
 struct GemvM1Args {
   const half_t* x;  // shared by every matrix of the launch

@@ -1,4 +1,4 @@
-// Decode GEMV kernels: 12-bit ids, one token (M = 1).
+// Decode GEMV kernels: 12-bit ids, one or two tokens (the row-streaming kernels).
 #include "fasq_gemv_launch.h"
 
 namespace fasq {
