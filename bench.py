@@ -659,16 +659,20 @@ def prefill(torch, fasq, pi, Ms, reps, short=1, long=4):
         for M in Ms:
             x = x_all[:M].contiguous()
             y = torch.empty((M, spec.N), dtype=torch.float16, device=dev)
+            # fasq_pq_gemm_ex: small grids also split K, with a workspace
+            # allocated here, outside the timed region
+            need = fasq.gemm_ex_workspace_bytes(M, spec.K, spec.N, base.idx_bits, base.d, base.C)
+            ws = torch.empty(max(need, 4), dtype=torch.uint8, device=dev)
             args = (x.data_ptr(), M, spec.K, spec.N, idx.data_ptr(), base.idx_bits, base.d, cb.data_ptr(),
-                    base.C, y.data_ptr(), stream.cuda_stream)
-            assert fasq.gemm_raw(*args) == 0, fasq.last_error()
+                    base.C, y.data_ptr(), ws.data_ptr(), need, stream.cuda_stream)
+            assert fasq.gemm_ex_raw(*args) == 0, fasq.last_error()
 
             def batch(count):
                 e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 torch.cuda._sleep(SPACER_CYCLES)
                 e0.record(stream)
                 for _ in range(count):
-                    assert fasq.gemm_raw(*args) == 0
+                    assert fasq.gemm_ex_raw(*args) == 0
                 e1.record(stream)
                 e1.synchronize()
                 return e0.elapsed_time(e1) * 1e-3
@@ -684,9 +688,10 @@ def prefill(torch, fasq, pi, Ms, reps, short=1, long=4):
             out.append(dict(name=spec.name, M=M, N=spec.N, K=spec.K, us=t * 1e6, tflops=fl / t / 1e12,
                             pct_mfma=100.0 * fl / t / 1e12 / FP16_MFMA_PEAK_TFLOPS,
                             dense_fp16_tflops=fl / td / 1e12, vs_dense_fp16=td / t,
-                            kernel=fasq.plan("gemm", M, spec.K, spec.N, base.idx_bits, base.d, base.C)))
+                            kernel=fasq.plan("gemm", M, spec.K, spec.N, base.idx_bits, base.d, base.C),
+                            k_split=max(1, need // (M * spec.N * 4))))
             log(f"[bench] prefill {spec.name} M={M}: {t * 1e6:.1f} us, {fl / t / 1e12:.1f} TFLOP/s "
-                f"(dense fp16 library GEMM: {fl / td / 1e12:.1f})")
+                f"(dense fp16 library GEMM: {fl / td / 1e12:.1f}){' K split ' + str(need // (M * spec.N * 4)) if need else ''}")
         del x_all, idx, cb, w_dense
     torch.cuda.empty_cache()
     return out

@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define FASQ_ABI_VERSION 3
+#define FASQ_ABI_VERSION 4
 
 typedef enum {
   FASQ_OK = 0,
@@ -125,6 +125,32 @@ fasq_status fasq_pq_gemm(const void* x, int64_t M, int64_t K, int64_t N,
                          const void* idx, int idx_bits, int d,
                          const void* codebook, int64_t C,
                          void* y, hipStream_t stream);
+
+/*
+ * fasq_pq_gemm with a workspace (FASQ Sec. 4.2 splits the subspaces, i.e. K,
+ * over blocks; Sec. 4.4 tunes the split for the prefill length).  When the
+ * output tiles alone leave compute units idle (small M or N), the tuned
+ * kernel also splits K over up to 8 workgroups per tile, which write fp32
+ * partial sums to the workspace; a second kernel adds them in a fixed order
+ * and rounds once to fp16 (deterministic for a given shape and device).
+ *
+ *   workspace  device scratch of at least fasq_pq_gemm_ex_workspace_bytes()
+ *              bytes (4-byte aligned; may be NULL when that is 0); contents
+ *              are overwritten.  A NULL or smaller workspace runs exactly
+ *              fasq_pq_gemm (no split).
+ *
+ * Other arguments, layouts and errors as fasq_pq_gemm, plus
+ * FASQ_ERR_INVALID_ARG for workspace_bytes < 0.
+ */
+fasq_status fasq_pq_gemm_ex(const void* x, int64_t M, int64_t K, int64_t N,
+                            const void* idx, int idx_bits, int d,
+                            const void* codebook, int64_t C,
+                            void* y, void* workspace, int64_t workspace_bytes,
+                            hipStream_t stream);
+
+/* Workspace bytes fasq_pq_gemm_ex splits K with on the current device (0
+ * when it would not split), -1 for invalid sizes. */
+int64_t fasq_pq_gemm_ex_workspace_bytes(int64_t M, int64_t K, int64_t N, int idx_bits, int d, int64_t C);
 
 /*
  * The paper's own prefill kernel design (FASQ Sec. 4.2, Alg. 3), kept for

@@ -40,6 +40,9 @@ __all__ = [
     "gemm_lut_raw",
     "gemv_ex_raw",
     "gemv_ex_workspace_bytes",
+    "pq_gemm_ex",
+    "gemm_ex_raw",
+    "gemm_ex_workspace_bytes",
     "encode_raw",
     "encode_workspace_bytes",
     "gemv_raw",
@@ -56,7 +59,7 @@ __all__ = [
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfasq.so")
 
-ABI_VERSION = 3  # FASQ_ABI_VERSION of include/fasq.h
+ABI_VERSION = 4  # FASQ_ABI_VERSION of include/fasq.h
 
 FASQ_OK = 0
 FASQ_ERR_INVALID_ARG = 1
@@ -78,6 +81,8 @@ EXPORTED_SYMBOLS = (
     "fasq_pq_gemv_ex",
     "fasq_pq_gemv_ex_workspace_bytes",
     "fasq_pq_gemm_lut",
+    "fasq_pq_gemm_ex",
+    "fasq_pq_gemm_ex_workspace_bytes",
 )
 
 
@@ -142,6 +147,11 @@ def lib() -> ctypes.CDLL:
         L.fasq_pq_gemv_ex.restype = _c_int
         L.fasq_pq_gemv_ex_workspace_bytes.argtypes = [_c_i64, _c_i64, _c_i64, _c_int, _c_int, _c_i64, _c_i64]
         L.fasq_pq_gemv_ex_workspace_bytes.restype = _c_i64
+        L.fasq_pq_gemm_ex.argtypes = [_c_vp, _c_i64, _c_i64, _c_i64, _c_vp, _c_int, _c_int, _c_vp, _c_i64, _c_vp,
+                                      _c_vp, _c_i64, _c_vp]
+        L.fasq_pq_gemm_ex.restype = _c_int
+        L.fasq_pq_gemm_ex_workspace_bytes.argtypes = [_c_i64, _c_i64, _c_i64, _c_int, _c_int, _c_i64]
+        L.fasq_pq_gemm_ex_workspace_bytes.restype = _c_i64
         _lib = L
         return L
 
@@ -442,3 +452,34 @@ def pq_gemv_ex(x, idx, idx_bits: int, d: int, codebook, out=None, workspace=None
         _check(gemv_ex_raw(x.data_ptr(), M, K, N, idx.data_ptr(), idx_bits, d, codebook.data_ptr(), C, stride,
                            out.data_ptr(), ws_ptr, ws_bytes, _stream_handle(x)))
     return out
+
+
+def gemm_ex_workspace_bytes(M: int, K: int, N: int, idx_bits: int, d: int, C: int) -> int:
+    return lib().fasq_pq_gemm_ex_workspace_bytes(M, K, N, idx_bits, d, C)
+
+
+def gemm_ex_raw(x, M, K, N, idx, idx_bits, d, codebook, C, y, workspace, workspace_bytes, stream=0) -> int:
+    return lib().fasq_pq_gemm_ex(x, M, K, N, idx, idx_bits, d, codebook, C, y, workspace, workspace_bytes, stream)
+
+
+def pq_gemm_ex(x, idx, idx_bits: int, d: int, codebook, out=None, workspace=None):
+    """Prefill-regime ``y = x . W_hat^T`` that may also split K over
+    workgroups, with a workspace for the partial sums (allocated here when
+    not given); see ``fasq_pq_gemm_ex``."""
+    torch = _torch()
+    _require(x, "x", torch.float16, 2)
+    M, K = x.shape
+    N = idx.shape[0] if isinstance(idx, torch.Tensor) and idx.dim() == 2 else 0
+    C = codebook.shape[0] if isinstance(codebook, torch.Tensor) and codebook.dim() == 2 else 0
+    need = gemm_ex_workspace_bytes(M, K, N, idx_bits, d, C) if N and C else 0
+    if need < 0:
+        raise ValueError("invalid sizes")
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
+    ws_ptr = workspace.data_ptr() if workspace is not None else 0
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+
+    def call(xp, M_, K_, N_, ip, bits, dd, cp, C_, yp, stream):
+        return lib().fasq_pq_gemm_ex(xp, M_, K_, N_, ip, bits, dd, cp, C_, yp, ws_ptr, ws_bytes, stream)
+
+    return _matmul(call, x, idx, idx_bits, d, codebook, out)

@@ -100,14 +100,15 @@ Problem make_problem(const void* x, int64_t M, int64_t K, int64_t N, const void*
 
 enum class Regime { kGemv, kGemm };
 
-fasq_status run(const Problem& p, Regime regime, hipStream_t stream) {
+fasq_status run(const Problem& p, Regime regime, hipStream_t stream, void* workspace = nullptr,
+               int64_t workspace_bytes = 0) {
   DeviceInfo dev;
   hipError_t e = device_info(&dev);
   if (e != hipSuccess) return hip_fail("querying the current device", e);
   e = hipErrorNotSupported;
   if (!force_generic()) {
     if (regime == Regime::kGemv) e = launch_gemv(p, dev, stream);
-    if (e == hipErrorNotSupported) e = launch_gemm_mfma(p, dev, stream);
+    if (e == hipErrorNotSupported) e = launch_gemm_mfma(p, dev, stream, workspace, workspace_bytes);
   }
   if (e == hipErrorNotSupported) e = launch_generic(p, stream);
   if (e != hipSuccess) return hip_fail("kernel launch", e);
@@ -298,6 +299,25 @@ fasq_status fasq_pq_gemv_ex(const void* x, int64_t M, int64_t K, int64_t N, cons
   if (e != hipSuccess) return fasq::hip_fail("kernel launch", e);
   fasq::t_last_error.clear();
   return FASQ_OK;
+}
+
+int64_t fasq_pq_gemm_ex_workspace_bytes(int64_t M, int64_t K, int64_t N, int idx_bits, int d, int64_t C) {
+  const void* fake = reinterpret_cast<const void*>(uintptr_t(1) << 20);
+  if (fasq::validate(M, K, N, idx_bits, d, C, fake, fake, fake, fake, true) != FASQ_OK) return -1;
+  Problem p = fasq::make_problem(fake, M, K, N, fake, idx_bits, d, fake, C, const_cast<void*>(fake));
+  fasq::DeviceInfo dev;
+  if (fasq::device_info(&dev) != hipSuccess) return -1;
+  return fasq::gemm_workspace_bytes(p, dev);
+}
+
+fasq_status fasq_pq_gemm_ex(const void* x, int64_t M, int64_t K, int64_t N, const void* idx, int idx_bits, int d,
+                            const void* codebook, int64_t C, void* y, void* workspace, int64_t workspace_bytes,
+                            hipStream_t stream) {
+  fasq_status s = fasq::validate(M, K, N, idx_bits, d, C, x, idx, codebook, y, true);
+  if (s != FASQ_OK) return s;
+  if (workspace_bytes < 0) return fasq::fail(FASQ_ERR_INVALID_ARG, "workspace_bytes must be >= 0");
+  return fasq::run(fasq::make_problem(x, M, K, N, idx, idx_bits, d, codebook, C, y), fasq::Regime::kGemm, stream,
+                   workspace, workspace_bytes);
 }
 
 int64_t fasq_pq_encode_workspace_bytes(int64_t N, int64_t K, int d, int64_t C) {

@@ -13,7 +13,7 @@ hipError_t launch_gemm_variant(const GemmArgs& a, int lds, hipStream_t stream) {
   if (plan_record("k_gemm_mfma", {BITS, D, MODE, BM, BN, WGM, WGN, NS, KG})) return hipSuccess;
   hipError_t e = prepare_kernel(kern);
   if (e != hipSuccess) return e;
-  dim3 grid((unsigned)((a.N + BN - 1) / BN), (unsigned)((a.M + BM - 1) / BM));
+  dim3 grid((unsigned)((a.N + BN - 1) / BN), (unsigned)((a.M + BM - 1) / BM), (unsigned)a.ksplit);
   hipLaunchKernelGGL(kern, grid, dim3(WGM * WGN * KG * kWave), lds, stream, a);
   return hipGetLastError();
 }
@@ -102,19 +102,32 @@ hipError_t launch_gemm_bits(const GemmArgs& a, int d, int mode, int tile, int kg
 
 }  // namespace
 
-hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t stream) {
+// The launch plan of a call: tile, K groups, codebook placement, LDS bytes
+// and the workgroups along K (ksplit > 1 needs ksplit * M * N * 4 bytes of
+// workspace); false when the tuned kernel does not apply.
+struct GemmPlan {
+  int tile = 0, kg = 1, mode = 0, lds = 0, ksplit = 1;
+};
+
+// K ranges per output tile when the grid leaves CUs idle: enough to reach
+// about one workgroup per CU, at most kGemmMaxSplit, each range at least
+// kGemmMinSplitChunks chunks of 64 per K group.
+constexpr int kGemmMaxSplit = 8;
+constexpr int kGemmMinSplitChunks = 4;
+
+bool gemm_plan(const Problem& p, const DeviceInfo& dev, GemmPlan* out) {
   const int d = p.d;
-  if (p.cb_stride != 0) return hipErrorNotSupported;
-  if (!(d == 1 || d == 2 || d == 4 || d == 8)) return hipErrorNotSupported;
-  if (p.idx_bits == 12 && d == 8) return hipErrorNotSupported;
-  if (p.K % kGemmKC) return hipErrorNotSupported;
-  if (p.R * 8 != p.S * p.idx_bits) return hipErrorNotSupported;
+  if (p.cb_stride != 0) return false;
+  if (!(d == 1 || d == 2 || d == 4 || d == 8)) return false;
+  if (p.idx_bits == 12 && d == 8) return false;
+  if (p.K % kGemmKC) return false;
+  if (p.R * 8 != p.S * p.idx_bits) return false;
   if ((reinterpret_cast<uintptr_t>(p.x) & 15) || (reinterpret_cast<uintptr_t>(p.codebook) & 15) ||
       (reinterpret_cast<uintptr_t>(p.idx) & 15) || (p.R & 3))
-    return hipErrorNotSupported;
+    return false;
   // id runs are copied as 4-byte words
   const int hb = (32 / d) * p.idx_bits / 8;
-  if (hb % 4) return hipErrorNotSupported;
+  if (hb % 4) return false;
 
   int mode = choose_cb_mode(p.C, d);
   auto lds_of = [&](int t, int kg, int m) {
@@ -139,7 +152,7 @@ hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t
     if (gemm_tile_ok(t, hb, p.idx_bits, d) && mode_of(t) >= 0 && 4 * tiles_of(t) >= 3 * (int64_t)dev.num_cus) tile = t;
   for (int t = kGemmNumTiles - 1; t >= 0 && tile < 0; --t)
     if (gemm_tile_ok(t, hb, p.idx_bits, d) && mode_of(t) >= 0) tile = t;
-  if (tile < 0) return hipErrorNotSupported;
+  if (tile < 0) return false;
   mode = mode_of(tile);
   // K groups for the 64-row tiles: the first count in kGemmSplitGroups that
   // fits, with the replicated codebook or, failing that, one copy.
@@ -155,6 +168,36 @@ hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t
     }
   }
   const int lds = (int)lds_of(tile, kg, mode);
+  int ksplit = 1;
+  const int64_t tiles = tiles_of(tile);
+  const int64_t chunks = p.K / kGemmKC;
+  while (ksplit < kGemmMaxSplit && tiles * (ksplit + 1) <= dev.num_cus &&
+         chunks / (ksplit + 1) >= (int64_t)kGemmMinSplitChunks * kg)
+    ++ksplit;
+  out->tile = tile;
+  out->kg = kg;
+  out->mode = mode;
+  out->lds = lds;
+  out->ksplit = ksplit;
+  return true;
+}
+
+int64_t gemm_workspace_bytes(const Problem& p, const DeviceInfo& dev) {
+  GemmPlan pl;
+  if (!gemm_plan(p, dev, &pl) || pl.ksplit == 1) return 0;
+  return (int64_t)pl.ksplit * p.M * p.N * 4;
+}
+
+hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t stream, void* workspace,
+                            int64_t workspace_bytes) {
+  GemmPlan pl;
+  if (!gemm_plan(p, dev, &pl)) return hipErrorNotSupported;
+  const int d = p.d;
+  // the K split only with a workspace that holds its partials
+  if (pl.ksplit > 1 && (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) & 3) ||
+                        workspace_bytes < (int64_t)pl.ksplit * p.M * p.N * 4))
+    pl.ksplit = 1;
+  const int tile = pl.tile, kg = pl.kg, mode = pl.mode, lds = pl.lds;
   const int cb_bytes = (int)cb_lds_bytes(mode, p.C, d);
 
   GemmArgs a;
@@ -168,11 +211,20 @@ hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t
   a.C = (int)p.C;
   a.cb_lds_bytes = cb_bytes;
   a.y = static_cast<half_t*>(p.y);
+  a.ksplit = pl.ksplit;
+  a.ws = static_cast<float*>(workspace);
+  hipError_t e;
   switch (p.idx_bits) {
-    case 8: return launch_gemm_bits<8>(a, d, mode, tile, kg, lds, stream);
-    case 12: return launch_gemm_bits<12>(a, d, mode, tile, kg, lds, stream);
-    default: return launch_gemm_bits<16>(a, d, mode, tile, kg, lds, stream);
+    case 8: e = launch_gemm_bits<8>(a, d, mode, tile, kg, lds, stream); break;
+    case 12: e = launch_gemm_bits<12>(a, d, mode, tile, kg, lds, stream); break;
+    default: e = launch_gemm_bits<16>(a, d, mode, tile, kg, lds, stream); break;
   }
+  if (e != hipSuccess || a.ksplit == 1 || plan().active) return e;
+  const int64_t mn = p.M * p.N;
+  const int64_t blocks = (mn + 255) / 256;
+  hipLaunchKernelGGL(k_gemm_split_reduce, dim3((unsigned)(blocks < 65536 ? blocks : 65536)), dim3(256), 0, stream,
+                     static_cast<const float*>(workspace), mn, a.ksplit, a.y);
+  return hipGetLastError();
 }
 
 }  // namespace fasq

@@ -45,6 +45,8 @@ struct GemmArgs {
   int C;
   int cb_lds_bytes;
   half_t* y;
+  int ksplit;  // workgroups along K (grid z); above 1 the partials go to ws
+  float* ws;   // [ksplit][M][N] fp32 partial sums when ksplit > 1
 };
 
 // Bytes of one packed-id run (one lane half, one chunk) and of one stage.
@@ -114,7 +116,10 @@ __global__ __launch_bounds__(WGM * WGN * KG * 64) void k_gemm_mfma(GemmArgs a) {
   const int h = lane >> 5, l32 = lane & 31;
   const int64_t m0 = (int64_t)blockIdx.y * BM;
   const int64_t n0 = (int64_t)blockIdx.x * BN;
-  const int nchunks = (int)(a.K / kGemmKC);
+  // K range of this workgroup: chunks [c_begin, c_begin + nchunks) of K / 64
+  const int all_chunks = (int)(a.K / kGemmKC);
+  const int c_begin = (int)((int64_t)blockIdx.z * all_chunks / a.ksplit);
+  const int nchunks = (int)((int64_t)(blockIdx.z + 1) * all_chunks / a.ksplit) - c_begin;
   const int niter = (nchunks + KG - 1) / KG;       // chunks per group (the last ones may lie past K)
   uint8_t* ring = smem + a.cb_lds_bytes + kg * (NS * SBYTES);  // NS stages of [X tile][id tile]
   // data chunk of iteration it, clamped into K for the copies
@@ -137,7 +142,8 @@ __global__ __launch_bounds__(WGM * WGN * KG * 64) void k_gemm_mfma(GemmArgs a) {
     const int64_t n = n0 + gl / IW;
     isrc[j] = a.idx + (n < a.N ? n : 0) * a.R + (gl % IW) * 4;
   }
-  auto issue = [&](int c, int stage) {
+  auto issue = [&](int lc, int stage) {
+    const int c = c_begin + lc;
     uint8_t* sb = ring + stage * SBYTES;
 #pragma unroll
     for (int j = 0; j < XI; ++j)
@@ -269,7 +275,9 @@ __global__ __launch_bounds__(WGM * WGN * KG * 64) void k_gemm_mfma(GemmArgs a) {
     }
   }
 
-  // ---- epilogue: lane l holds rows (i/4)*8 + h*4 + i%4, column l32 of each 32x32 tile
+  // ---- epilogue: lane l holds rows (i/4)*8 + h*4 + i%4, column l32 of each
+  //      32x32 tile; fp16 outputs, or this K range's fp32 partial sums
+  float* part = a.ws + (int64_t)blockIdx.z * a.M * a.N;
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm) {
 #pragma unroll
@@ -279,9 +287,20 @@ __global__ __launch_bounds__(WGM * WGN * KG * 64) void k_gemm_mfma(GemmArgs a) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int64_t m = m0 + wm * WM + fm * 32 + (i / 4) * 8 + h * 4 + (i % 4);
-        if (m < a.M) a.y[m * a.N + n] = static_cast<half_t>(acc[fm][fn][i]);
+        if (m >= a.M) continue;
+        if (a.ksplit > 1) part[m * a.N + n] = acc[fm][fn][i];
+        else a.y[m * a.N + n] = static_cast<half_t>(acc[fm][fn][i]);
       }
     }
+  }
+}
+
+// y = fp16(sum over the K ranges, in range order, of the fp32 partials)
+__global__ void k_gemm_split_reduce(const float* __restrict__ ws, int64_t MN, int ksplit, half_t* __restrict__ y) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < MN; i += (int64_t)gridDim.x * blockDim.x) {
+    float s = 0.f;
+    for (int k = 0; k < ksplit; ++k) s += ws[(int64_t)k * MN + i];
+    y[i] = static_cast<half_t>(s);
   }
 }
 

@@ -48,7 +48,12 @@ constexpr int kMaxBatchLaunch = 8;  // matrices per grouped launch
 constexpr int kM1MaxTokens = 2;     // tokens the row-streaming decode kernel takes at once
 
 // Tuned MFMA prefill kernel.  hipErrorNotSupported when no variant applies.
-hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
+// With a workspace of at least gemm_workspace_bytes() a grid too small for
+// the CUs is also split along K (fp32 partials summed by a second kernel);
+// otherwise the workspace is not touched.
+hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t stream, void* workspace = nullptr,
+                            int64_t workspace_bytes = 0);
+int64_t gemm_workspace_bytes(const Problem& p, const DeviceInfo& dev);
 
 // The paper's lookup-table GEMM (Alg. 3), kept for comparison with the MFMA
 // GEMM.  hipErrorNotSupported when its tables do not fit in LDS.

@@ -184,3 +184,32 @@ def test_encode_invalid_arguments_rejected_without_launch(L, args, why, status):
                          a["idx"], a["ws"], a["ws_bytes"], 0)
     assert st == status
     assert why in fasq.last_error()
+
+
+# ---------------------------------------------------------------------------
+# Prefill with a workspace (K split over workgroups): validation before any
+# HIP call
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("args,why", [
+    (dict(M=0), "M, K and N"),
+    (dict(K=10, d=4), "multiple of d"),
+    (dict(idx_bits=10), "idx_bits"),
+    (dict(C=257), "C must"),
+    (dict(y=0), "NULL"),
+    (dict(ws_bytes=-1), "workspace_bytes"),
+])
+def test_gemm_ex_invalid_arguments_rejected_without_launch(L, args, why):
+    a = dict(x=DUMMY, M=1, K=16, N=4, idx=DUMMY, idx_bits=8, d=2, codebook=DUMMY, C=256, y=DUMMY, ws=DUMMY,
+             ws_bytes=1 << 20)
+    a.update(args)
+    st = fasq.gemm_ex_raw(a["x"], a["M"], a["K"], a["N"], a["idx"], a["idx_bits"], a["d"], a["codebook"], a["C"],
+                          a["y"], a["ws"], a["ws_bytes"], 0)
+    assert st == fasq.FASQ_ERR_INVALID_ARG
+    assert why in fasq.last_error()
+
+
+def test_gemm_ex_workspace_bytes_invalid_sizes(L):
+    assert fasq.gemm_ex_workspace_bytes(0, 16, 4, 8, 2, 256) == -1
+    assert fasq.gemm_ex_workspace_bytes(1, 10, 4, 8, 4, 256) == -1
+    assert fasq.gemm_ex_workspace_bytes(1, 16, 4, 8, 2, 300) == -1

@@ -564,3 +564,77 @@ def test_codebook_placement_follows_the_work_per_workgroup():
     assert fasq.plan("gemv", 2, 4096, 4096, 8, 2, 256).startswith("k_gemv_mt<8, 2, ")
     assert fasq.plan("gemv_batched", 4, 4096, 4096, 8, 2, 256).startswith("k_gemv<")
     assert fasq.plan("gemv", 1, 320, 20000, 8, 4, 256).startswith("k_gemv_m1<8, 4, 1, 0, ")
+
+
+# ---------------------------------------------------------------------------
+# Prefill with K split over workgroups (fasq_pq_gemm_ex and its workspace)
+# ---------------------------------------------------------------------------
+
+SPLIT_K = [
+    # M, K, N, d, C, bits: grids that leave CUs idle
+    (8, 4096, 512, 4, 256, 8),           # 8 tiles: eight K ranges
+    (128, 4096, 4096, 4, 256, 8),        # the prefill q_proj shape at M = 128
+    (130, 4096 + 64 * 3, 700, 2, 256, 8),
+    (40, 14336, 200, 4, 4096, 12),
+    (33, 2048, 100, 4, 65536, 16),
+]
+
+
+def _gemm_ex(x, idx, bits, d, cb, ws_bytes=None):
+    need = fasq.gemm_ex_workspace_bytes(x.shape[0], x.shape[1], idx.shape[0], bits, d, cb.shape[0])
+    n = need if ws_bytes is None else ws_bytes
+    ws = torch.zeros(max(n, 4), dtype=torch.uint8, device="cuda:0")
+    y = torch.empty((x.shape[0], idx.shape[0]), dtype=torch.float16, device="cuda:0")
+    xd, idd, cbd = to_dev(x), to_dev(idx), to_dev(cb)  # held until the call has run
+    st = fasq.gemm_ex_raw(xd.data_ptr(), x.shape[0], x.shape[1], idx.shape[0], idd.data_ptr(), bits, d,
+                          cbd.data_ptr(), cb.shape[0], y.data_ptr(), ws.data_ptr(), n, 0)
+    assert st == fasq.FASQ_OK, fasq.last_error()
+    torch.cuda.synchronize()
+    return to_np(y), need
+
+
+@pytest.mark.parametrize("case", SPLIT_K)
+def test_gemm_split_k_one_hot_bit_exact(case):
+    """Exact small-integer results: a K range summed twice or dropped would
+    show as an exact mismatch."""
+    M, K, N, d, C, bits = case
+    print(f"[case] gemm split k {case}", flush=True)
+    rng = np.random.default_rng(23 + sum(case))
+    cb = pi.signed_one_hot_codebook(C, d, rng)
+    ids = rng.integers(0, C, size=(N, K // d))
+    x = pi.ternary_x(rng, M, K)
+    idx = pi.pack_indices(ids, bits)
+    ref = orc.pq_linear(x, idx, bits, d, cb)
+    assert np.abs(ref).max() <= 2048
+    y, need = _gemm_ex(x, idx, bits, d, cb)
+    assert need > 0  # the call does split
+    assert np.array_equal(y.astype(np.float64), ref)
+
+
+@pytest.mark.parametrize("case", SPLIT_K[:3])
+def test_gemm_split_k_random_against_oracle(case):
+    M, K, N, d, C, bits = case
+    print(f"[case] gemm split k random {case}", flush=True)
+    rng = np.random.default_rng(29 + sum(case))
+    p = pi.draw_problem(rng, M, K, N, d, C, bits)
+    y, need = _gemm_ex(p.x, p.idx, bits, d, p.codebook)
+    assert need > 0
+    assert_close(y, orc.pq_linear(p.x, p.idx, bits, d, p.codebook), f"split k {case}")
+    # deterministic: the same call gives the same bits
+    y2, _ = _gemm_ex(p.x, p.idx, bits, d, p.codebook)
+    assert np.array_equal(y.view(np.uint16), y2.view(np.uint16))
+
+
+def test_gemm_ex_small_workspace_is_the_plain_gemm():
+    M, K, N, d, C, bits = SPLIT_K[1]
+    rng = np.random.default_rng(31)
+    p = pi.draw_problem(rng, M, K, N, d, C, bits)
+    y_small, need = _gemm_ex(p.x, p.idx, bits, d, p.codebook, ws_bytes=16)
+    assert need > 16
+    y_plain = to_np(fasq.pq_gemm(to_dev(p.x), to_dev(p.idx), bits, d, to_dev(p.codebook)))
+    assert np.array_equal(y_small.view(np.uint16), y_plain.view(np.uint16))
+
+
+def test_gemm_ex_no_split_for_full_grids():
+    assert fasq.gemm_ex_workspace_bytes(2048, 4096, 14336, 8, 4, 256) == 0
+    assert fasq.gemm_ex_workspace_bytes(128, 4096, 4096, 8, 4, 256) == 2 * 128 * 4096 * 4
