@@ -807,6 +807,9 @@ def main():
         extra["llama3_8b_3bit"] = r3
         extra["prefill"] = prefill(torch, fasq, pi, (128, 512, 2048), 10)
         extra["tiny"] = tiny_latency(torch, fasq, pi)
+        r2 = decode_layer(torch, fasq, pi, "llama3_8b_4bit", max(10, args.steps // 2), 3, M=2)
+        report_layer("4bit, M=2", r2)
+        extra["llama3_8b_4bit_M2"] = r2
     if args.per_matrix:
         r1 = decode_layer(torch, fasq, pi, "llama3_8b_4bit", max(10, args.steps // 2), 3, grouped=False)
         report_layer("4bit, one launch per matrix", r1)
