@@ -95,7 +95,8 @@ class MatrixSet:
 
     ``groups`` lists the launch groups (lists of matrix indices); a group of
     several matrices is one fasq_pq_gemv_batched call on the x of its first
-    matrix, a group of one is one fasq_pq_gemv call.
+    matrix, a group of one is one fasq_pq_gemv call (fasq_pq_gemv_ex with a
+    workspace when the call can use one).
     """
 
     def __init__(self, torch, fasq, problems, names, groups=None, min_copies=1, rotation_bytes=ROTATION_BYTES,
@@ -122,6 +123,12 @@ class MatrixSet:
                 s.append(t)
             self.sets.append(s)
         del base
+        # one workspace per matrix (launches run in order on one stream), for
+        # the decode calls that use one
+        self.ws = []
+        for p in problems:
+            need = fasq.gemv_ex_workspace_bytes(p.M, p.K, p.N, p.idx_bits, p.d, p.C, 0) if regime == "gemv" else 0
+            self.ws.append(torch.empty(need, dtype=torch.uint8, device=dev) if need > 0 else None)
         torch.cuda.synchronize()
 
     def group_bytes(self, g):
@@ -146,9 +153,17 @@ class MatrixSet:
         p0, x = self.problems[members[0]], s[members[0]]["x"].data_ptr()
         if len(members) == 1:
             t = s[members[0]]
-            fn = dict(gemm=self.fasq.gemm_raw, lut=self.fasq.gemm_lut_raw).get(self.regime, self.fasq.gemv_raw)
-            st = fn(x, p0.M, p0.K, p0.N, t["idx"].data_ptr(), p0.idx_bits, p0.d,
-                    t["cb"].data_ptr(), p0.C, t["y"].data_ptr(), stream)
+            ws = self.ws[members[0]]
+            if self.regime == "gemv" and ws is not None:
+                # the decode call hands this matrix to the GEMM, which may split
+                # K with a workspace (fasq_pq_gemv_ex with one shared codebook)
+                st = self.fasq.gemv_ex_raw(x, p0.M, p0.K, p0.N, t["idx"].data_ptr(), p0.idx_bits, p0.d,
+                                           t["cb"].data_ptr(), p0.C, 0, t["y"].data_ptr(), ws.data_ptr(),
+                                           ws.numel(), stream)
+            else:
+                fn = dict(gemm=self.fasq.gemm_raw, lut=self.fasq.gemm_lut_raw).get(self.regime, self.fasq.gemv_raw)
+                st = fn(x, p0.M, p0.K, p0.N, t["idx"].data_ptr(), p0.idx_bits, p0.d,
+                        t["cb"].data_ptr(), p0.C, t["y"].data_ptr(), stream)
         else:
             st = self.fasq.gemv_batched_raw(
                 x, p0.M, p0.K, [s[i]["idx"].data_ptr() for i in members], [self.problems[i].N for i in members],

@@ -182,7 +182,10 @@ fasq_status fasq_pq_gemm_lut(const void* x, int64_t M, int64_t K, int64_t N,
  * Other arguments, layouts and errors as fasq_pq_gemv.  With per-subspace
  * books and M = 1 the tuned kernel splits K over workgroups whose books fit
  * in LDS and adds the partials in a fixed order (deterministic); other shapes,
- * or a workspace that is too small, take the general kernel.
+ * or a workspace that is too small, take the general kernel.  With one shared
+ * codebook the call is fasq_pq_gemv, except that when the decode kernels hand
+ * it to the prefill GEMM (M > 16, or rows of x too long for LDS) the GEMM may
+ * split K with the workspace as fasq_pq_gemm_ex does.
  */
 fasq_status fasq_pq_gemv_ex(const void* x, int64_t M, int64_t K, int64_t N,
                             const void* idx, int idx_bits, int d,
@@ -190,8 +193,9 @@ fasq_status fasq_pq_gemv_ex(const void* x, int64_t M, int64_t K, int64_t N,
                             void* y, void* workspace, int64_t workspace_bytes,
                             hipStream_t stream);
 
-/* Workspace bytes the tuned per-subspace kernel of fasq_pq_gemv_ex needs on
- * the current device (0 when no workspace is used), -1 for invalid sizes. */
+/* Workspace bytes fasq_pq_gemv_ex uses on the current device for these sizes
+ * (per-subspace books: the tuned kernel's partials; one shared codebook: the
+ * K split of the GEMM fallback), 0 when none is used, -1 for invalid sizes. */
 int64_t fasq_pq_gemv_ex_workspace_bytes(int64_t M, int64_t K, int64_t N, int idx_bits, int d,
                                         int64_t C, int64_t cb_stride);
 

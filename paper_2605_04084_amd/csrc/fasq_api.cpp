@@ -276,7 +276,11 @@ int64_t fasq_pq_gemv_ex_workspace_bytes(int64_t M, int64_t K, int64_t N, int idx
   p.cb_stride = cb_stride;
   fasq::DeviceInfo dev;
   if (fasq::device_info(&dev) != hipSuccess) return -1;
-  return fasq::gemv_sub_workspace_bytes(p, dev);
+  if (cb_stride != 0) return fasq::gemv_sub_workspace_bytes(p, dev);
+  // one shared codebook: a workspace serves the GEMM when the decode kernels
+  // hand it the call (its K split)
+  if (std::strncmp(fasq_pq_plan(0, M, K, N, idx_bits, d, C), "k_gemm_mfma", 11) != 0) return 0;
+  return fasq::gemm_workspace_bytes(p, dev);
 }
 
 fasq_status fasq_pq_gemv_ex(const void* x, int64_t M, int64_t K, int64_t N, const void* idx, int idx_bits, int d,
@@ -288,7 +292,7 @@ fasq_status fasq_pq_gemv_ex(const void* x, int64_t M, int64_t K, int64_t N, cons
     return fasq::fail(FASQ_ERR_INVALID_ARG, "cb_stride must be 0 (one shared codebook) or C * d (one per subspace)");
   if (workspace_bytes < 0) return fasq::fail(FASQ_ERR_INVALID_ARG, "workspace_bytes must be >= 0");
   Problem p = fasq::make_problem(x, M, K, N, idx, idx_bits, d, codebook, C, y);
-  if (cb_stride == 0) return fasq::run(p, fasq::Regime::kGemv, stream);
+  if (cb_stride == 0) return fasq::run(p, fasq::Regime::kGemv, stream, workspace, workspace_bytes);
   p.cb_stride = cb_stride;
   fasq::DeviceInfo dev;
   hipError_t e = fasq::device_info(&dev);

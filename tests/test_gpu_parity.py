@@ -638,3 +638,25 @@ def test_gemm_ex_small_workspace_is_the_plain_gemm():
 def test_gemm_ex_no_split_for_full_grids():
     assert fasq.gemm_ex_workspace_bytes(2048, 4096, 14336, 8, 4, 256) == 0
     assert fasq.gemm_ex_workspace_bytes(128, 4096, 4096, 8, 4, 256) == 2 * 128 * 4096 * 4
+
+
+def test_gemv_ex_shared_codebook_gemm_fallback_splits_k():
+    """fasq_pq_gemv_ex with one shared codebook hands M > 16 to the GEMM, which
+    splits K with the workspace; exact on small-integer data."""
+    M, K, N, d, C, bits = 20, 2048, 300, 4, 256, 8
+    assert fasq.gemv_ex_workspace_bytes(1, K, N, bits, d, C, 0) == 0
+    need = fasq.gemv_ex_workspace_bytes(M, K, N, bits, d, C, 0)
+    assert need > 0
+    rng = np.random.default_rng(37)
+    cb = pi.signed_one_hot_codebook(C, d, rng)
+    ids = rng.integers(0, C, size=(N, K // d))
+    x = pi.ternary_x(rng, M, K)
+    idx = pi.pack_indices(ids, bits)
+    ref = orc.pq_linear(x, idx, bits, d, cb)
+    xd, idd, cbd = to_dev(x), to_dev(idx), to_dev(cb)
+    ws = torch.zeros(need, dtype=torch.uint8, device="cuda:0")
+    y = torch.empty((M, N), dtype=torch.float16, device="cuda:0")
+    st = fasq.gemv_ex_raw(xd.data_ptr(), M, K, N, idd.data_ptr(), bits, d, cbd.data_ptr(), C, 0, y.data_ptr(),
+                          ws.data_ptr(), need, 0)
+    assert st == fasq.FASQ_OK, fasq.last_error()
+    assert np.array_equal(to_np(y).astype(np.float64), ref)
