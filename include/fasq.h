@@ -99,9 +99,9 @@ fasq_status fasq_pq_gemv(const void* x, int64_t M, int64_t K, int64_t N,
  * with W_hat_i given by idx[i] (N[i] rows of fasq_idx_row_bytes(K, d,
  * idx_bits) bytes) and codebook[i] (fp16 [C[i] x d]).  x, M, K, idx_bits and d
  * are shared; every array holds `count` entries and lives in HOST memory,
- * while the buffers it points to are device memory.  For M <= 2 up to eight
- * matrices run in one launch; otherwise, or when the grouped kernel does not
- * apply, the matrices are computed one call after another.  Every y[i] is
+ * while the buffers it points to are device memory.  For M <= 16 up to eight
+ * matrices run in one launch; when no grouped kernel applies (d = 3, for
+ * instance) the matrices are computed one call after another.  Every y[i] is
  * bit-for-bit what fasq_pq_gemv would write for matrix i alone.
  *
  * Returns FASQ_ERR_INVALID_ARG when count < 1, an array is NULL, or any

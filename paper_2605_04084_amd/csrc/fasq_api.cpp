@@ -16,30 +16,31 @@ namespace fasq {
 hipError_t launch_gemv_u8_m1(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream);
 hipError_t launch_gemv_u12_m1(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream);
 hipError_t launch_gemv_u16_m1(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream);
-hipError_t launch_gemv_u8_m16(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
-hipError_t launch_gemv_u12_m16(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
-hipError_t launch_gemv_u16_m16(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
+hipError_t launch_gemv_u8_m16(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream);
+hipError_t launch_gemv_u12_m16(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream);
+hipError_t launch_gemv_u16_m16(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream);
 
-hipError_t launch_gemv_m1_group(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream) {
-  switch (ps[0].idx_bits) {
-    case 8: return launch_gemv_u8_m1(ps, count, dev, stream);
-    case 12: return launch_gemv_u12_m1(ps, count, dev, stream);
-    default: return launch_gemv_u16_m1(ps, count, dev, stream);
+hipError_t launch_gemv_group(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream) {
+  const Problem& p = ps[0];
+  if (p.M < 1 || p.M > 16) return hipErrorNotSupported;
+  if (p.M <= kM1MaxTokens) {  // the row-streaming kernel when its codebook placement allows
+    hipError_t e;
+    switch (p.idx_bits) {
+      case 8: e = launch_gemv_u8_m1(ps, count, dev, stream); break;
+      case 12: e = launch_gemv_u12_m1(ps, count, dev, stream); break;
+      default: e = launch_gemv_u16_m1(ps, count, dev, stream);
+    }
+    if (e != hipErrorNotSupported || p.M == 1) return e;
+  }
+  switch (p.idx_bits) {
+    case 8: return launch_gemv_u8_m16(ps, count, dev, stream);
+    case 12: return launch_gemv_u12_m16(ps, count, dev, stream);
+    default: return launch_gemv_u16_m16(ps, count, dev, stream);
   }
 }
 
 hipError_t launch_gemv(const Problem& p, const DeviceInfo& dev, hipStream_t stream) {
-  if (p.M == 1) return launch_gemv_m1_group(&p, 1, dev, stream);
-  if (p.M <= kM1MaxTokens) {  // the row-streaming kernel when its codebook fits LDS
-    hipError_t e = launch_gemv_m1_group(&p, 1, dev, stream);
-    if (e != hipErrorNotSupported) return e;
-  }
-  if (p.M > 16) return hipErrorNotSupported;
-  switch (p.idx_bits) {
-    case 8: return launch_gemv_u8_m16(p, dev, stream);
-    case 12: return launch_gemv_u12_m16(p, dev, stream);
-    default: return launch_gemv_u16_m16(p, dev, stream);
-  }
+  return launch_gemv_group(&p, 1, dev, stream);
 }
 
 namespace {
@@ -203,7 +204,7 @@ fasq_status fasq_pq_gemv_batched(const void* x, int64_t M, int64_t K, int count,
       ps[i] = fasq::make_problem(x, M, K, N[off + i], idx[off + i], idx_bits, d, codebook[off + i], C[off + i],
                                  y[off + i]);
     e = hipErrorNotSupported;
-    if (M <= fasq::kM1MaxTokens && !fasq::force_generic()) e = fasq::launch_gemv_m1_group(ps, n, dev, stream);
+    if (!fasq::force_generic()) e = fasq::launch_gemv_group(ps, n, dev, stream);
     if (e == hipErrorNotSupported) {
       for (int i = 0; i < n; ++i) {
         fasq_status s = fasq::run(ps[i], fasq::Regime::kGemv, stream);
@@ -386,8 +387,7 @@ const char* fasq_pq_plan(int regime, int64_t M, int64_t K, int64_t N, int idx_bi
     Problem ps[2] = {p, p};
     fasq::DeviceInfo dev;
     hipError_t e = fasq::device_info(&dev);
-    if (e == hipSuccess && M <= fasq::kM1MaxTokens && !fasq::force_generic())
-      e = fasq::launch_gemv_m1_group(ps, 2, dev, nullptr);
+    if (e == hipSuccess && !fasq::force_generic()) e = fasq::launch_gemv_group(ps, 2, dev, nullptr);
     else e = hipErrorNotSupported;
     s = e == hipSuccess ? FASQ_OK : e == hipErrorNotSupported ? fasq::run(p, fasq::Regime::kGemv, nullptr)
                                                              : FASQ_ERR_HIP;

@@ -34,22 +34,32 @@
 
 namespace fasq {
 
+// One part of a k_gemv launch: a range of rows of one matrix.  Grid row
+// blockIdx.y works on part blockIdx.y; every part has gridDim.x workgroups.
+struct GemvPart {
+  const uint8_t* idx;  // id row of the part's first row
+  const half_t* cb;
+  half_t* y;           // output of the part's first row, token 0
+  int64_t N;           // rows of the part
+  int64_t ldy;         // elements between the outputs of consecutive tokens
+  int C;
+  int nsl;             // CB_SLICE: slices (passes over the rows)
+};
+
+constexpr int kGemvMaxParts = 8;  // parts one k_gemv launch can take
+
 struct GemvArgs {
   const half_t* x;
-  int64_t M, K, N;
-  const uint8_t* idx;
+  int64_t M, K;
   int64_t R;   // bytes per row (= CH * chunk bytes)
   int64_t CH;  // chunks per row
-  const half_t* cb;
-  int C;
   int P;         // waves per row (K split inside the workgroup)
   int TW;        // 16-row tiles per workgroup, a multiple of waves / P
   int cb_bytes;  // LDS bytes of the codebook (x follows)
   int xs;        // LDS bytes between rows of x
   int x_bytes;   // LDS bytes of x (partials follow)
   int sl_shift;  // CB_SLICE: log2 of the entries per slice
-  int nsl;       // CB_SLICE: slices (passes over the rows)
-  half_t* y;
+  GemvPart part[kGemvMaxParts];
 };
 
 constexpr int kGemvPipe = 8;      // load units per wave in the software pipeline
@@ -80,6 +90,7 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   uint8_t* xl = smem + a.cb_bytes;
   float* red = reinterpret_cast<float*>(smem + a.cb_bytes + a.x_bytes);  // [RW][M][P]
+  const GemvPart& pt = a.part[blockIdx.y];  // the rows this workgroup works on
 
   const int wave = threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
@@ -115,9 +126,9 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
   uint32_t buf[L][DW];
   auto load_unit = [&](int slot, int u, int t) {
     const int64_t tile = tile_of(u / T);
-    const bool live = u < nunits && tile * 16 + nl < a.N;
+    const bool live = u < nunits && tile * 16 + nl < pt.N;
     const uint32_t off = (uint32_t)tile * tile_stride + lane_off0 + (uint32_t)ccol(t) * CBY;
-    load_chunk<BITS>(a.idx + (live ? off : 0u), buf[slot]);
+    load_chunk<BITS>(pt.idx + (live ? off : 0u), buf[slot]);
   };
 
   // ---- prologue.  The vector L1 returns loads in order, so an L2-resident
@@ -138,22 +149,22 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
   // at every step.
   constexpr bool kXInRegs = !MASK && T * SPC <= 8;
   half8_t xreg[kXInRegs ? T * SPC : 1];
-  const int nsl = MODE == CB_SLICE ? a.nsl : 1;
+  const int nsl = MODE == CB_SLICE ? pt.nsl : 1;
 
   for (int si = 0; si < nsl; ++si) {
     Slice sl;
-    const half_t* scb = a.cb;
-    int sC = a.C;
+    const half_t* scb = pt.cb;
+    int sC = pt.C;
     if constexpr (MODE == CB_SLICE) {
       sl.base = (uint32_t)si << a.sl_shift;
       sl.mask = (1u << a.sl_shift) - 1u;
-      scb = a.cb + (size_t)sl.base * D;
-      sC = a.C - (int)sl.base < (1 << a.sl_shift) ? a.C - (int)sl.base : (1 << a.sl_shift);
+      scb = pt.cb + (size_t)sl.base * D;
+      sC = pt.C - (int)sl.base < (1 << a.sl_shift) ? pt.C - (int)sl.base : (1 << a.sl_shift);
       if (si > 0) __syncthreads();  // every wave is done with the previous slice
     }
     CbStage cst;
     if constexpr (MODE == CB_SLICE) slice_fetch(scb, sC * D * 2 / 16, cst);
-    else cb_fetch<D, MODE>(a.cb, a.C, cst);
+    else cb_fetch<D, MODE>(pt.cb, pt.C, cst);
     u32x4 xst[XWT];
     if (si == 0) {
 #pragma unroll
@@ -168,7 +179,7 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
     for (int i = 0; i < L - 1; ++i) load_unit(i, i, i % T);
 
     if constexpr (MODE == CB_SLICE) slice_store(smem, scb, sC * D * 2 / 16, cst);
-    else cb_store<D, MODE>(smem, a.cb, a.C, cst);
+    else cb_store<D, MODE>(smem, pt.cb, pt.C, cst);
     if (si == 0) {
 #pragma unroll
       for (int k = 0; k < XWT; ++k) {
@@ -210,7 +221,7 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
           const bool cval = !MASK || ccol_raw(t) < CH;
 #pragma unroll
           for (int s = 0; s < SPC; ++s) {
-            half8_t bop = gather8<BITS, D, MODE>(a.cb, lane_off, w, s * (8 / D), sl);
+            half8_t bop = gather8<BITS, D, MODE>(pt.cb, lane_off, w, s * (8 / D), sl);
             half8_t aop;
             if constexpr (kXInRegs) aop = xreg[t * SPC + s];
             else aop = *reinterpret_cast<const half8_t*>(xa + s * 16);
@@ -249,11 +260,11 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
     const int m = o / RW;
     const int r = o - m * RW;
     const int64_t n = ((int64_t)blockIdx.x + (int64_t)(r / 16) * gridDim.x) * 16 + (r & 15);
-    if (n < a.N) {
+    if (n < pt.N) {
       float sum = 0.f;
       const float* pr = red + (r * M + m) * P;
       for (int pp = 0; pp < P; ++pp) sum += pr[pp];
-      a.y[(int64_t)m * a.N + n] = static_cast<half_t>(sum);
+      pt.y[(int64_t)m * pt.ldy + n] = static_cast<half_t>(sum);
     }
   }
 }

@@ -1,6 +1,7 @@
 // Host-side variant selection and launch of the decode GEMV (M <= 16).
 #pragma once
 
+#include <algorithm>
 #include <atomic>
 
 #include "fasq_gemv.h"
@@ -12,7 +13,8 @@ constexpr int kLdsCodebookBudget = 64 * 1024;  // bytes of LDS a codebook may ta
 constexpr int kSliceReserve = 8 * 1024;        // LDS kept for row partials beside a codebook slice
 constexpr int kMinSliceBytes = 32 * 1024;      // smaller slices: gather from global memory instead
 constexpr int kReplMinIdsPerEntry = 16;        // replicate the codebook only above this many ids per workgroup and entry
-static_assert(kMaxBatchLaunch <= kM1MaxParts, "a grouped launch needs a part per matrix at least");
+static_assert(kMaxBatchLaunch <= kM1MaxParts && kMaxBatchLaunch <= kGemvMaxParts,
+              "a grouped launch needs a part per matrix at least");
 
 // Codebook placement for a call: replicated in LDS when the replicated table
 // fits the budget, one copy in LDS when that fits, else global memory.
@@ -23,18 +25,59 @@ inline int choose_cb_mode(int64_t C, int d) {
   return CB_GLOBAL;
 }
 
+// Cuts `count` matrices of units[i] units each (rows, or 16-row tiles) into
+// parts of near-equal size, at most max_parts in all, every part taking the
+// same number of workgroups.  A matrix with the largest parts is cut once
+// more at each step; the cut kept is the one whose largest part per
+// workgroup is smallest, with about one workgroup per CU in all.  cuts[i]
+// receives the parts of matrix i; returns the number of parts.
+constexpr int kMaxLaunchParts = 8;
+static_assert(kM1MaxParts <= kMaxLaunchParts && kGemvMaxParts <= kMaxLaunchParts, "part cuts per launch");
+inline int choose_part_cuts(const int64_t* units, int count, int64_t ncu, int max_parts, int* cuts) {
+  auto largest = [&](const int* c) {
+    int64_t r = 0;
+    for (int i = 0; i < count; ++i) {
+      const int64_t ri = (units[i] + c[i] - 1) / c[i];
+      if (ri > r) r = ri;
+    }
+    return r;
+  };
+  int cur[kMaxLaunchParts];
+  for (int i = 0; i < count; ++i) cur[i] = cuts[i] = 1;
+  int nparts = count, best_parts = count;
+  double best_cost = (double)largest(cur) / (double)(ncu / count > 0 ? ncu / count : 1);
+  while (nparts < max_parts) {
+    int j = -1;
+    int64_t jr = 1;
+    for (int i = 0; i < count; ++i) {
+      const int64_t ri = (units[i] + cur[i] - 1) / cur[i];
+      if (cur[i] < units[i] && ri > jr) { j = i; jr = ri; }
+    }
+    if (j < 0) break;
+    ++cur[j];
+    ++nparts;
+    const double cost = (double)largest(cur) / (double)(ncu / nparts > 0 ? ncu / nparts : 1);
+    if (cost < best_cost) {
+      best_cost = cost;
+      best_parts = nparts;
+      for (int i = 0; i < count; ++i) cuts[i] = cur[i];
+    }
+  }
+  return best_parts;
+}
+
 template <int BITS, int D, int T, int MODE, int MR>
-hipError_t launch_gemv_variant(const GemvArgs& a, bool mask, int threads, int blocks, int lds, hipStream_t stream) {
+hipError_t launch_gemv_variant(const GemvArgs& a, bool mask, int threads, dim3 blocks, int lds, hipStream_t stream) {
   auto kern = mask ? k_gemv<BITS, D, T, MODE, MR, true> : k_gemv<BITS, D, T, MODE, MR, false>;
   if (plan_record("k_gemv", {BITS, D, T, MODE, MR, mask ? 1 : 0})) return hipSuccess;
   hipError_t e = prepare_kernel(kern);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3(blocks), dim3(threads), lds, stream, a);
+  hipLaunchKernelGGL(kern, blocks, dim3(threads), lds, stream, a);
   return hipGetLastError();
 }
 
 template <int BITS, int MR, int D, int MODE>
-hipError_t launch_gemv_t(const GemvArgs& a, int T, bool mask, int threads, int blocks, int lds,
+hipError_t launch_gemv_t(const GemvArgs& a, int T, bool mask, int threads, dim3 blocks, int lds,
                          hipStream_t stream) {
   switch (T) {
     case 1: return launch_gemv_variant<BITS, D, 1, MODE, MR>(a, mask, threads, blocks, lds, stream);
@@ -45,7 +88,7 @@ hipError_t launch_gemv_t(const GemvArgs& a, int T, bool mask, int threads, int b
 }
 
 template <int BITS, int MR, int D>
-hipError_t launch_gemv_mode(const GemvArgs& a, int mode, int T, bool mask, int threads, int blocks, int lds,
+hipError_t launch_gemv_mode(const GemvArgs& a, int mode, int T, bool mask, int threads, dim3 blocks, int lds,
                             hipStream_t stream) {
   switch (mode) {
     case CB_REPL: return launch_gemv_t<BITS, MR, D, CB_REPL>(a, T, mask, threads, blocks, lds, stream);
@@ -57,24 +100,35 @@ hipError_t launch_gemv_mode(const GemvArgs& a, int mode, int T, bool mask, int t
   }
 }
 
-// Select (T, P, Q, codebook placement, rows per workgroup) and launch;
+// 2 to 16 tokens, one launch over `count` <= kGemvMaxParts matrices that
+// share x, M, K, d and the id width: select T, P, Q, the codebook placement,
+// the parts and the 16-row tiles per workgroup, and launch;
 // hipErrorNotSupported when another kernel has to take the call.
 template <int BITS, int MR>
-hipError_t launch_gemv_bits(const Problem& p, const DeviceInfo& dev, hipStream_t stream) {
+hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream) {
   constexpr int G = Chunk<BITS>::G;
   constexpr int CBY = Chunk<BITS>::DW * 4;
+  if (count < 1 || count > kGemvMaxParts) return hipErrorNotSupported;
+  const Problem& p = ps[0];
   const int d = p.d;
   if (MR == 1 ? p.M != 1 : (p.M < 2 || p.M > 16)) return hipErrorNotSupported;
-  if (p.cb_stride != 0) return hipErrorNotSupported;
   if (!(d == 1 || d == 2 || d == 4 || d == 8)) return hipErrorNotSupported;
   if (p.S % G || p.K % 8) return hipErrorNotSupported;
   const int64_t CH = p.S / G;
   if (CH * CBY != p.R) return hipErrorNotSupported;
-  if (p.N * p.R >= (int64_t(1) << 32) || 16 * p.R >= (int64_t(1) << 24)) return hipErrorNotSupported;
-  const uintptr_t ia = reinterpret_cast<uintptr_t>(p.idx);
-  if ((ia & (CBY == 16 ? 15 : 3)) || (reinterpret_cast<uintptr_t>(p.x) & 15) ||
-      (reinterpret_cast<uintptr_t>(p.codebook) & 15))
-    return hipErrorNotSupported;
+  if (16 * p.R >= (int64_t(1) << 24) || (reinterpret_cast<uintptr_t>(p.x) & 15)) return hipErrorNotSupported;
+  int64_t maxC = 0, total_rows = 0;
+  int64_t tiles_of[kGemvMaxParts];
+  for (int i = 0; i < count; ++i) {
+    const Problem& pi = ps[i];
+    if (pi.M != p.M || pi.K != p.K || pi.d != d || pi.idx_bits != p.idx_bits || pi.x != p.x) return hipErrorNotSupported;
+    if (pi.cb_stride != 0 || pi.N * pi.R >= (int64_t(1) << 32)) return hipErrorNotSupported;
+    if ((reinterpret_cast<uintptr_t>(pi.idx) & (CBY == 16 ? 15 : 3)) || (reinterpret_cast<uintptr_t>(pi.codebook) & 15))
+      return hipErrorNotSupported;
+    maxC = std::max(maxC, pi.C);
+    total_rows += pi.N;
+    tiles_of[i] = (pi.N + 15) / 16;
+  }
 
   const int64_t QC = (CH + 3) / 4;  // chunk columns of the four K groups
   int T = 0;
@@ -87,33 +141,42 @@ hipError_t launch_gemv_bits(const Problem& p, const DeviceInfo& dev, hipStream_t
   const bool mask = (int64_t)P * T * 4 != CH;  // the last wave sees columns past the row end
   const int threads = P * Q * kWave;
 
-  int mode = choose_cb_mode(p.C, d);
-  if (mode == CB_REPL && (p.N + dev.num_cus - 1) / dev.num_cus * p.S < kReplMinIdsPerEntry * p.C) mode = CB_LDS;
+  // One codebook placement for the launch: the largest codebook decides it.
+  int mode = choose_cb_mode(maxC, d);
+  if (mode == CB_REPL && (total_rows + dev.num_cus - 1) / dev.num_cus * p.S < kReplMinIdsPerEntry * maxC) mode = CB_LDS;
   const int xs = (int)(p.M == 1 ? p.K * 2 : p.K * 2 + 16);
   const int64_t x_bytes = p.M * (int64_t)xs;
   // The replicated table (up to 64 KB) gives way to one copy when it leaves
   // too little room beside x for one row group's partials.
   if (mode == CB_REPL &&
-      cb_lds_bytes(CB_REPL, p.C, d) + x_bytes + (int64_t)Q * 16 * p.M * P * 4 > dev.lds_per_block)
+      cb_lds_bytes(CB_REPL, maxC, d) + x_bytes + (int64_t)Q * 16 * p.M * P * 4 > dev.lds_per_block)
     mode = CB_LDS;
   // A codebook too large for the LDS budget still goes to LDS when all of it
   // fits beside x and the partials of two row groups (one slice, one pass).
   // More passes do not pay here: each pass costs as much as the whole
   // gather-from-L2 kernel at M >= 4.
   int sl_shift = 0;
-  if (mode == CB_GLOBAL && (p.C * d * 2) % 16 == 0) {
+  if (mode == CB_GLOBAL && (maxC * d * 2) % 16 == 0) {
     const int64_t red_min = 2 * (int64_t)Q * 16 * p.M * P * 4;
     const int64_t room = dev.lds_per_block - x_bytes - (red_min > kSliceReserve ? red_min : kSliceReserve);
     while (sl_shift < 16 && (int64_t(2) << sl_shift) * d * 2 <= room) ++sl_shift;
-    if ((int64_t(1) << sl_shift) * d * 2 >= kMinSliceBytes && (int64_t(1) << sl_shift) >= p.C) mode = CB_SLICE;
+    if ((int64_t(1) << sl_shift) * d * 2 >= kMinSliceBytes && (int64_t(1) << sl_shift) >= maxC) mode = CB_SLICE;
   }
-  const int cb_bytes = mode == CB_SLICE ? (int)((int64_t(1) << sl_shift) * d * 2) : (int)cb_lds_bytes(mode, p.C, d);
+  if (mode != CB_GLOBAL)  // every codebook must be whole 16-byte words to be staged
+    for (int i = 0; i < count; ++i)
+      if ((ps[i].C * d * 2) % 16 != 0) return hipErrorNotSupported;
+  const int cb_bytes = mode == CB_SLICE ? (int)((int64_t(1) << sl_shift) * d * 2) : (int)cb_lds_bytes(mode, maxC, d);
   const int64_t avail = dev.lds_per_block - cb_bytes - x_bytes;
 
-  // Row tiles of 16 are dealt round-robin to at most one workgroup per CU;
-  // each workgroup gets a whole number of tiles per row group.
-  const int64_t ntiles = (p.N + 15) / 16;
-  int64_t nwg = dev.num_cus;
+  // Parts: matrix i is cut into cuts[i] ranges of whole 16-row tiles; every
+  // part gets the grid's x size in workgroups (its y size counts the parts).
+  // Within a part, row tiles are dealt round-robin to the workgroups; each
+  // workgroup gets a whole number of tiles per row group.
+  int cuts[kGemvMaxParts];
+  const int nparts = choose_part_cuts(tiles_of, count, dev.num_cus, kGemvMaxParts, cuts);
+  int64_t ntiles = 0;  // tiles of the largest part
+  for (int i = 0; i < count; ++i) ntiles = std::max(ntiles, (tiles_of[i] + cuts[i] - 1) / cuts[i]);
+  int64_t nwg = std::max<int64_t>(dev.num_cus / nparts, 1);
   if (nwg > (ntiles + Q - 1) / Q) nwg = (ntiles + Q - 1) / Q;
   int64_t tw = (ntiles + nwg - 1) / nwg;
   tw = (tw + Q - 1) / Q * Q;
@@ -126,29 +189,41 @@ hipError_t launch_gemv_bits(const Problem& p, const DeviceInfo& dev, hipStream_t
   if (nwg > 0x7fffffff || tw * 16 > 0x7fffffff) return hipErrorNotSupported;
   const int lds = (int)(cb_bytes + x_bytes + tw * 16 * p.M * P * 4);
 
-  GemvArgs a;
+  GemvArgs a = {};
   a.x = static_cast<const half_t*>(p.x);
   a.M = p.M;
   a.K = p.K;
-  a.N = p.N;
-  a.idx = static_cast<const uint8_t*>(p.idx);
   a.R = p.R;
   a.CH = CH;
-  a.cb = static_cast<const half_t*>(p.codebook);
-  a.C = (int)p.C;
   a.P = P;
   a.TW = (int)tw;
   a.cb_bytes = cb_bytes;
   a.xs = xs;
   a.x_bytes = (int)x_bytes;
   a.sl_shift = sl_shift;
-  a.nsl = mode == CB_SLICE ? (int)((p.C + (int64_t(1) << sl_shift) - 1) >> sl_shift) : 1;
-  a.y = static_cast<half_t*>(p.y);
+  int k = 0;
+  for (int i = 0; i < count; ++i) {
+    const int64_t base = tiles_of[i] / cuts[i], extra = tiles_of[i] % cuts[i];
+    int64_t row = 0;
+    for (int c = 0; c < cuts[i]; ++c, ++k) {
+      const int64_t rows = std::min((base + (c < extra ? 1 : 0)) * 16, ps[i].N - row);
+      GemvPart& pt = a.part[k];
+      pt.idx = static_cast<const uint8_t*>(ps[i].idx) + row * ps[i].R;
+      pt.cb = static_cast<const half_t*>(ps[i].codebook);
+      pt.y = static_cast<half_t*>(ps[i].y) + row;
+      pt.N = rows;
+      pt.ldy = ps[i].N;
+      pt.C = (int)ps[i].C;
+      pt.nsl = mode == CB_SLICE ? (int)((ps[i].C + (int64_t(1) << sl_shift) - 1) >> sl_shift) : 1;
+      row += rows;
+    }
+  }
+  const dim3 grid((unsigned)nwg, (unsigned)nparts);
   switch (d) {
-    case 1: return launch_gemv_mode<BITS, MR, 1>(a, mode, T, mask, threads, (int)nwg, lds, stream);
-    case 2: return launch_gemv_mode<BITS, MR, 2>(a, mode, T, mask, threads, (int)nwg, lds, stream);
-    case 4: return launch_gemv_mode<BITS, MR, 4>(a, mode, T, mask, threads, (int)nwg, lds, stream);
-    default: return launch_gemv_mode<BITS, MR, 8>(a, mode, T, mask, threads, (int)nwg, lds, stream);
+    case 1: return launch_gemv_mode<BITS, MR, 1>(a, mode, T, mask, threads, grid, lds, stream);
+    case 2: return launch_gemv_mode<BITS, MR, 2>(a, mode, T, mask, threads, grid, lds, stream);
+    case 4: return launch_gemv_mode<BITS, MR, 4>(a, mode, T, mask, threads, grid, lds, stream);
+    default: return launch_gemv_mode<BITS, MR, 8>(a, mode, T, mask, threads, grid, lds, stream);
   }
 }
 
@@ -287,41 +362,15 @@ hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& d
   if (Q > 16 / P) Q = 16 / P;
   if (Q < 1) Q = 1;
 
-  // Parts: matrix i is cut into cuts[i] ranges of near-equal row counts, and
+  // Parts: matrix i is cut into best[i] ranges of near-equal row counts, and
   // every part gets the same number of workgroups (the grid's x size; its y
-  // size counts the parts).  Cut where it makes the most rows per workgroup
-  // smallest, with about one workgroup per CU in all.
-  auto part_rows = [&](const int* cuts) {
-    int64_t r = 0;
-    for (int i = 0; i < count; ++i) {
-      const int64_t ri = (ps[i].N + cuts[i] - 1) / cuts[i];
-      if (ri > r) r = ri;
-    }
-    return r;
-  };
-  int cuts[kM1MaxParts], best[kM1MaxParts];
-  for (int i = 0; i < count; ++i) cuts[i] = best[i] = 1;
-  int nparts = count, best_parts = count;
-  double best_cost = (double)part_rows(cuts) / (double)(ncu / count > 0 ? ncu / count : 1);
-  while (nparts < kM1MaxParts) {
-    int j = -1;  // cut the matrix with the largest parts once more
-    int64_t jr = 1;
-    for (int i = 0; i < count; ++i) {
-      const int64_t ri = (ps[i].N + cuts[i] - 1) / cuts[i];
-      if (cuts[i] < ps[i].N && ri > jr) { j = i; jr = ri; }
-    }
-    if (j < 0) break;
-    ++cuts[j];
-    ++nparts;
-    const double cost = (double)part_rows(cuts) / (double)(ncu / nparts > 0 ? ncu / nparts : 1);
-    if (cost < best_cost) {
-      best_cost = cost;
-      best_parts = nparts;
-      for (int i = 0; i < count; ++i) best[i] = cuts[i];
-    }
-  }
-  nparts = best_parts;
-  const int64_t max_rows = part_rows(best);
+  // size counts the parts).
+  int64_t rows_of[kM1MaxParts];
+  int best[kM1MaxParts];
+  for (int i = 0; i < count; ++i) rows_of[i] = ps[i].N;
+  const int nparts = choose_part_cuts(rows_of, count, ncu, kM1MaxParts, best);
+  int64_t max_rows = 0;
+  for (int i = 0; i < count; ++i) max_rows = std::max(max_rows, (ps[i].N + best[i] - 1) / best[i]);
   int64_t wpp = ncu / nparts;  // workgroups per part
   if (wpp > (max_rows + Q - 1) / Q) wpp = (max_rows + Q - 1) / Q;  // no workgroup without a row group
   if (wpp < 1) wpp = 1;

@@ -2,7 +2,7 @@
 #include "fasq_gemv_launch.h"
 
 namespace fasq {
-hipError_t launch_gemv_u8_m16(const Problem& p, const DeviceInfo& dev, hipStream_t stream) {
-  return launch_gemv_bits<8, 16>(p, dev, stream);
+hipError_t launch_gemv_u8_m16(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream) {
+  return launch_gemv_bits<8, 16>(ps, count, dev, stream);
 }
 }  // namespace fasq

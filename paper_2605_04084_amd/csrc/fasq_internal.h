@@ -40,10 +40,12 @@ hipError_t launch_generic(const Problem& p, hipStream_t stream);
 // launching) when no tuned variant applies.
 hipError_t launch_gemv(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
 
-// Tuned row-streaming decode kernel over several matrices in one launch (all
-// with the same M <= kM1MaxTokens, x, K, d and id width; at most 8).
-// hipErrorNotSupported (without launching) when it does not apply.
-hipError_t launch_gemv_m1_group(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream);
+// Tuned decode kernels over one to kMaxBatchLaunch matrices in one launch,
+// all with the same M <= 16, x, K, d and id width: the row-streaming kernel
+// for M <= kM1MaxTokens where its codebook placement allows, else the
+// 16-row-tile kernel.  hipErrorNotSupported (without launching) when
+// neither applies.
+hipError_t launch_gemv_group(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream);
 constexpr int kMaxBatchLaunch = 8;  // matrices per grouped launch
 constexpr int kM1MaxTokens = 2;     // tokens the row-streaming decode kernel takes at once
 

@@ -368,8 +368,16 @@ BATCH_CASES = [
     (1, 640, 4, 12, [(2049, 4096), (700, 4096), (1, 4096)]),       # parts of several sizes, one 1-row matrix
     (2, 4096, 2, 8, [(4096, 256), (1024, 256), (1024, 256)]),      # two tokens, one launch
     (2, 512, 4, 12, [(300, 4096), (129, 1000)]),                   # two tokens, ragged N, mixed C
-    (3, 256, 2, 8, [(70, 256), (130, 256)]),                       # M > 2: one call per matrix
+    (3, 256, 2, 8, [(70, 256), (130, 256)]),                       # M > 2: the 16-row-tile kernel, one launch
+    (4, 4096, 2, 8, [(4096, 256), (1024, 256), (1024, 256)]),      # q, k, v shapes, four tokens
+    (16, 1024, 2, 8, [(5000, 256), (3, 256)]),                     # sixteen tokens, uneven parts
+    (8, 512, 4, 12, [(300, 4096), (129, 1000), (1, 4096)]),        # ragged N, mixed C, a 1-row matrix
+    (7, 640, 4, 12, [(2049, 4096), (700, 4096), (1, 4096)]),       # rows not a whole number of wave spans
+    (5, 320, 4, 16, [(64, 65536), (65, 300)]),                     # codebook gathered from global memory
+    (2, 320, 4, 16, [(64, 65536), (65, 300)]),                     # two tokens, codebook too large for LDS
+    (4, 256, 2, 8, [(40 + 7 * i, 256) for i in range(11)]),        # more than one launch's worth
     (1, 96, 3, 8, [(20, 7), (9, 5)]),                              # d = 3: general kernel
+    (4, 96, 3, 8, [(20, 7), (9, 5)]),                              # d = 3, four tokens
 ]
 
 
@@ -563,6 +571,8 @@ def test_codebook_placement_follows_the_work_per_workgroup():
     assert fasq.plan("gemv_batched", 2, 4096, 4096, 8, 2, 256).startswith("k_gemv_mt<8, 2, ")
     assert fasq.plan("gemv", 2, 4096, 4096, 8, 2, 256).startswith("k_gemv_mt<8, 2, ")
     assert fasq.plan("gemv_batched", 4, 4096, 4096, 8, 2, 256).startswith("k_gemv<")
+    # two tokens with a codebook too large for LDS: the 16-row-tile kernel, global gathers (mode 2)
+    assert fasq.plan("gemv_batched", 2, 320, 64, 16, 4, 65536) == "k_gemv<16, 4, 1, 2, 16, 1>"
     assert fasq.plan("gemv", 1, 320, 20000, 8, 4, 256).startswith("k_gemv_m1<8, 4, 1, 0, ")
 
 
