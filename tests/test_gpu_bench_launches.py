@@ -1,0 +1,78 @@
+"""The decode layers exactly as bench.py launches and times them, at full size.
+
+Each workload's matrices go out in bench.py's launch groups (q+k+v and
+gate+up as one grouped call, the others alone, a workspace where the call
+takes one), first eagerly and then from a captured HIP graph replayed several
+times.  Sampled rows of every output are compared with the oracle, and every
+replay must equal the eager result bit for bit.
+"""
+
+import numpy as np
+import pytest
+
+import bench
+import pq_inputs as pi
+from oracle import pq_oracle as orc
+from gpu_util import assert_close, sample_rows
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+fasq = pytest.importorskip("paper_2605_04084_amd")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    fasq.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+LAYERS = [
+    ("llama3_8b_4bit", 1),
+    ("llama3_8b_4bit", 2),
+    ("llama3_8b_3bit", 1),
+    ("qwen3_8b_sweep", 1),
+    ("qwen3_8b_sweep", 4),
+    ("qwen3_8b_sweep", 16),
+]
+
+
+@pytest.mark.parametrize("wl_name,M", LAYERS)
+def test_decode_layer_as_timed(wl_name, M):
+    print(f"[case] bench layer {wl_name} M={M}", flush=True)
+    wl = pi.workload(wl_name)
+    problems = [wl.problem(i, M=M) for i in range(len(wl.matrices))]
+    names = [m.name for m in wl.matrices]
+    ms = bench.MatrixSet(torch, fasq, problems, names, bench.launch_groups(names), min_copies=1,
+                         rotation_bytes=0)
+    assert ms.copies == 1
+    ys = [s["y"] for s in ms.sets[0]]
+    stream = torch.cuda.current_stream().cuda_stream
+
+    # eager launches, checked against the oracle on sampled rows; a grouped
+    # call reads the x of its first matrix for every member
+    x_of = {i: problems[g[0]].x for g in ms.groups for i in g}
+    for y in ys:
+        y.fill_(float("nan"))
+    ms.launch_all(0, stream)
+    torch.cuda.synchronize()
+    eager = [y.cpu().numpy() for y in ys]
+    for i, (p, name, got) in enumerate(zip(problems, names, eager)):
+        rows = sample_rows(p.N, 128)
+        ref = orc.pq_linear(x_of[i], p.idx, p.idx_bits, p.d, p.codebook, rows=rows)
+        assert_close(got.astype(np.float64)[:, rows], ref, f"{wl_name} M={M} {name}")
+
+    # the same launches from a graph (capture_graphs warms up eagerly first)
+    graphs = ms.capture_graphs(1)
+    for rep in range(3):
+        for y in ys:
+            y.fill_(float("nan"))
+        torch.cuda.synchronize()
+        graphs[0].replay()
+        torch.cuda.synchronize()
+        for name, y, e in zip(names, ys, eager):
+            assert np.array_equal(y.cpu().numpy().view(np.uint16), e.view(np.uint16)), f"replay {rep} {name}"
+    del graphs
