@@ -76,3 +76,26 @@ def test_decode_layer_as_timed(wl_name, M):
         for name, y, e in zip(names, ys, eager):
             assert np.array_equal(y.cpu().numpy().view(np.uint16), e.view(np.uint16)), f"replay {rep} {name}"
     del graphs
+
+
+@pytest.mark.parametrize("M", [128, 512, 2048])
+@pytest.mark.parametrize("mat", range(3))
+def test_prefill_as_timed(mat, M):
+    """fasq_pq_gemm_ex with the workspace bench.py gives it (K split where the
+    grid leaves CUs idle), at the prefill shapes."""
+    wl = pi.workload("prefill")
+    spec = wl.matrices[mat]
+    print(f"[case] bench prefill {spec.name} M={M}", flush=True)
+    p = wl.problem(mat, M=M)
+    dev = torch.device("cuda:0")
+    x, idx, cb = (torch.from_numpy(a).to(dev) for a in (p.x, p.idx, p.codebook))
+    y = torch.full((M, p.N), float("nan"), dtype=torch.float16, device=dev)
+    need = fasq.gemm_ex_workspace_bytes(M, p.K, p.N, p.idx_bits, p.d, p.C)
+    ws = torch.empty(max(need, 4), dtype=torch.uint8, device=dev)
+    st = fasq.gemm_ex_raw(x.data_ptr(), M, p.K, p.N, idx.data_ptr(), p.idx_bits, p.d, cb.data_ptr(), p.C,
+                          y.data_ptr(), ws.data_ptr(), need, torch.cuda.current_stream().cuda_stream)
+    assert st == fasq.FASQ_OK, fasq.last_error()
+    torch.cuda.synchronize()
+    rows = sample_rows(p.N, 128)
+    ref = orc.pq_linear(p.x, p.idx, p.idx_bits, p.d, p.codebook, rows=rows)
+    assert_close(y.cpu().numpy().astype(np.float64)[:, rows], ref, f"prefill {spec.name} M={M} (workspace {need} B)")
