@@ -14,7 +14,9 @@ namespace fasq {
 //   CB_SLICE : LDS, one slice of 2^k entries at a time (codebooks larger than
 //              LDS): the kernel makes one pass over its rows per slice, and
 //              an id contributes only in the pass of its own slice.
-enum CbMode { CB_REPL = 0, CB_LDS = 1, CB_GLOBAL = 2, CB_SLICE = 3 };
+//   CB_SPLIT : the first entries in LDS, as many as fit, the rest gathered
+//              from global memory (codebooks larger than LDS, one pass).
+enum CbMode { CB_REPL = 0, CB_LDS = 1, CB_GLOBAL = 2, CB_SLICE = 3, CB_SPLIT = 4 };
 
 // One lane's unit of the packed index stream.
 template <int BITS>
@@ -243,7 +245,8 @@ __device__ __forceinline__ void read_codeword_lds(uint32_t addr, uint32_t* out) 
   }
 }
 
-// The codebook slice resident in LDS (CB_SLICE): entries [base, base + mask].
+// The codebook slice resident in LDS (CB_SLICE, CB_SPLIT): entries
+// [base, base + mask].
 struct Slice {
   uint32_t base = 0;
   uint32_t mask = 0;
@@ -252,6 +255,23 @@ struct Slice {
 // Gather codeword u into `out` (layout as for read_codeword_lds).  In
 // CB_SLICE mode an id outside the resident slice reads nothing and yields
 // a zero codeword.
+// Codeword u read straight from the codebook in global memory.
+template <int D>
+__device__ __forceinline__ void read_codeword_global(const half_t* __restrict__ gcb, uint32_t u, uint32_t* out) {
+  const uint8_t* p = reinterpret_cast<const uint8_t*>(gcb) + (size_t)u * (2 * D);
+  if constexpr (D == 1) {
+    out[0] = *reinterpret_cast<const uint16_t*>(p);
+  } else if constexpr (D == 2) {
+    out[0] = *reinterpret_cast<const uint32_t*>(p);
+  } else if constexpr (D == 4) {
+    const u32x2 v = *reinterpret_cast<const u32x2*>(p);
+    out[0] = v[0]; out[1] = v[1];
+  } else {
+    const u32x4 v = *reinterpret_cast<const u32x4*>(p);
+    out[0] = v[0]; out[1] = v[1]; out[2] = v[2]; out[3] = v[3];
+  }
+}
+
 template <int D, int MODE>
 __device__ __forceinline__ void gather(const half_t* __restrict__ gcb, uint32_t lane_off, uint32_t u,
                                        uint32_t* out, Slice sl = Slice()) {
@@ -264,19 +284,11 @@ __device__ __forceinline__ void gather(const half_t* __restrict__ gcb, uint32_t 
 #pragma unroll
     for (int k = 0; k < (D + 1) / 2; ++k) out[k] = 0u;
     if (loc <= sl.mask) read_codeword_lds<D>(loc * (2 * D), out);
+  } else if constexpr (MODE == CB_SPLIT) {
+    if (u <= sl.mask) read_codeword_lds<D>(u * (2 * D), out);
+    else read_codeword_global<D>(gcb, u, out);
   } else {
-    const uint8_t* p = reinterpret_cast<const uint8_t*>(gcb) + (size_t)u * (2 * D);
-    if constexpr (D == 1) {
-      out[0] = *reinterpret_cast<const uint16_t*>(p);
-    } else if constexpr (D == 2) {
-      out[0] = *reinterpret_cast<const uint32_t*>(p);
-    } else if constexpr (D == 4) {
-      const u32x2 v = *reinterpret_cast<const u32x2*>(p);
-      out[0] = v[0]; out[1] = v[1];
-    } else {
-      const u32x4 v = *reinterpret_cast<const u32x4*>(p);
-      out[0] = v[0]; out[1] = v[1]; out[2] = v[2]; out[3] = v[3];
-    }
+    read_codeword_global<D>(gcb, u, out);
   }
 }
 

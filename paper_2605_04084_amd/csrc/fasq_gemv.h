@@ -59,6 +59,7 @@ struct GemvArgs {
   int xs;        // LDS bytes between rows of x
   int x_bytes;   // LDS bytes of x (partials follow)
   int sl_shift;  // CB_SLICE: log2 of the entries per slice
+  int head;      // CB_SPLIT: entries staged in LDS (the rest are read from global memory)
   GemvPart part[kGemvMaxParts];
 };
 
@@ -161,9 +162,13 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
       scb = pt.cb + (size_t)sl.base * D;
       sC = pt.C - (int)sl.base < (1 << a.sl_shift) ? pt.C - (int)sl.base : (1 << a.sl_shift);
       if (si > 0) __syncthreads();  // every wave is done with the previous slice
+    } else if constexpr (MODE == CB_SPLIT) {
+      sl.mask = (uint32_t)a.head - 1u;
+      sC = a.head;
     }
+    constexpr bool kStageSlice = MODE == CB_SLICE || MODE == CB_SPLIT;
     CbStage cst;
-    if constexpr (MODE == CB_SLICE) slice_fetch(scb, sC * D * 2 / 16, cst);
+    if constexpr (kStageSlice) slice_fetch(scb, sC * D * 2 / 16, cst);
     else cb_fetch<D, MODE>(pt.cb, pt.C, cst);
     u32x4 xst[XWT];
     if (si == 0) {
@@ -178,7 +183,7 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
 #pragma unroll
     for (int i = 0; i < L - 1; ++i) load_unit(i, i, i % T);
 
-    if constexpr (MODE == CB_SLICE) slice_store(smem, scb, sC * D * 2 / 16, cst);
+    if constexpr (kStageSlice) slice_store(smem, scb, sC * D * 2 / 16, cst);
     else cb_store<D, MODE>(smem, pt.cb, pt.C, cst);
     if (si == 0) {
 #pragma unroll

@@ -96,6 +96,9 @@ hipError_t launch_gemv_mode(const GemvArgs& a, int mode, int T, bool mask, int t
     case CB_SLICE:  // only 16-bit ids address codebooks larger than LDS
       if constexpr (BITS == 16) return launch_gemv_t<BITS, MR, D, CB_SLICE>(a, T, mask, threads, blocks, lds, stream);
       else return hipErrorNotSupported;
+    case CB_SPLIT:
+      if constexpr (BITS == 16) return launch_gemv_t<BITS, MR, D, CB_SPLIT>(a, T, mask, threads, blocks, lds, stream);
+      else return hipErrorNotSupported;
     default: return launch_gemv_t<BITS, MR, D, CB_GLOBAL>(a, T, mask, threads, blocks, lds, stream);
   }
 }
@@ -162,10 +165,26 @@ hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev,
     while (sl_shift < 16 && (int64_t(2) << sl_shift) * d * 2 <= room) ++sl_shift;
     if ((int64_t(1) << sl_shift) * d * 2 >= kMinSliceBytes && (int64_t(1) << sl_shift) >= maxC) mode = CB_SLICE;
   }
-  if (mode != CB_GLOBAL)  // every codebook must be whole 16-byte words to be staged
+  // Otherwise the first entries of the codebooks go to LDS, as many as fit
+  // beside x and the partials of two row groups (whole 16-byte words, and no
+  // more than the smallest codebook holds); ids past them gather from
+  // global memory.
+  int64_t head = 0;
+  if (BITS == 16 && mode == CB_GLOBAL) {
+    int64_t minC = maxC;
+    for (int i = 0; i < count; ++i) minC = std::min(minC, ps[i].C);
+    const int64_t red_min = 2 * (int64_t)Q * 16 * p.M * P * 4;
+    const int64_t room = dev.lds_per_block - x_bytes - std::max<int64_t>(red_min, kSliceReserve);
+    const int64_t per_word = 16 / (2 * d);  // entries per 16-byte word
+    head = std::min(room / (2 * d), minC) / per_word * per_word;
+    if (head * d * 2 >= kMinSliceBytes) mode = CB_SPLIT;
+  }
+  if (mode != CB_GLOBAL && mode != CB_SPLIT)  // every codebook must be whole 16-byte words to be staged
     for (int i = 0; i < count; ++i)
       if ((ps[i].C * d * 2) % 16 != 0) return hipErrorNotSupported;
-  const int cb_bytes = mode == CB_SLICE ? (int)((int64_t(1) << sl_shift) * d * 2) : (int)cb_lds_bytes(mode, maxC, d);
+  const int cb_bytes = mode == CB_SLICE   ? (int)((int64_t(1) << sl_shift) * d * 2)
+                       : mode == CB_SPLIT ? (int)(head * d * 2)
+                                          : (int)cb_lds_bytes(mode, maxC, d);
   const int64_t avail = dev.lds_per_block - cb_bytes - x_bytes;
 
   // Parts: matrix i is cut into cuts[i] ranges of whole 16-row tiles; every
@@ -201,6 +220,7 @@ hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev,
   a.xs = xs;
   a.x_bytes = (int)x_bytes;
   a.sl_shift = sl_shift;
+  a.head = (int)head;
   int k = 0;
   for (int i = 0; i < count; ++i) {
     const int64_t base = tiles_of[i] / cuts[i], extra = tiles_of[i] % cuts[i];

@@ -571,8 +571,9 @@ def test_codebook_placement_follows_the_work_per_workgroup():
     assert fasq.plan("gemv_batched", 2, 4096, 4096, 8, 2, 256).startswith("k_gemv_mt<8, 2, ")
     assert fasq.plan("gemv", 2, 4096, 4096, 8, 2, 256).startswith("k_gemv_mt<8, 2, ")
     assert fasq.plan("gemv_batched", 4, 4096, 4096, 8, 2, 256).startswith("k_gemv<")
-    # two tokens with a codebook too large for LDS: the 16-row-tile kernel, global gathers (mode 2)
-    assert fasq.plan("gemv_batched", 2, 320, 64, 16, 4, 65536) == "k_gemv<16, 4, 1, 2, 16, 1>"
+    # two tokens with a codebook too large for LDS: the 16-row-tile kernel, the codebook's first
+    # entries in LDS and the rest gathered from global memory (mode 4)
+    assert fasq.plan("gemv_batched", 2, 320, 64, 16, 4, 65536) == "k_gemv<16, 4, 1, 4, 16, 1>"
     assert fasq.plan("gemv", 1, 320, 20000, 8, 4, 256).startswith("k_gemv_m1<8, 4, 1, 0, ")
 
 
@@ -670,3 +671,46 @@ def test_gemv_ex_shared_codebook_gemm_fallback_splits_k():
                           ws.data_ptr(), need, 0)
     assert st == fasq.FASQ_OK, fasq.last_error()
     assert np.array_equal(to_np(y).astype(np.float64), ref)
+
+
+# ---------------------------------------------------------------------------
+# Codebooks larger than LDS at 2 to 16 tokens: the first entries in LDS, the
+# rest gathered from global memory, in one pass
+# ---------------------------------------------------------------------------
+
+SPLIT_BOOK = [
+    # M, K, N, d, C, bits
+    (4, 4096, 300, 4, 65536, 16),       # Qwen3-8B-like rows at four tokens, ragged N
+    (7, 2048, 129, 4, 40000, 16),       # C not a power of two
+    (3, 512, 4100, 8, 30000, 16),       # d = 8
+    (2, 1024, 1000, 2, 65536, 16),      # d = 2, two tokens
+]
+
+
+@pytest.mark.parametrize("case", SPLIT_BOOK)
+def test_split_codebook_one_hot_bit_exact(case):
+    """Exact small-integer results: an id read from the wrong place (LDS for
+    an entry past the staged ones, or the wrong entry) shows as a mismatch."""
+    M, K, N, d, C, bits = case
+    print(f"[case] split codebook one-hot {case}", flush=True)
+    assert fasq.plan("gemv", M, K, N, bits, d, C).split(", ")[3] == "4"
+    rng = np.random.default_rng(47 + sum(case))
+    cb = pi.signed_one_hot_codebook(C, d, rng)
+    ids = rng.integers(0, C, size=(N, K // d))
+    ids[:, 0] = C - 1   # the last entry, from global memory
+    ids[:, 1] = 0       # the first entry, from LDS
+    x = pi.ternary_x(rng, M, K)
+    idx = pi.pack_indices(ids, bits)
+    ref = orc.pq_linear(x, idx, bits, d, cb)
+    y = to_np(fasq.pq_gemv(to_dev(x), to_dev(idx), bits, d, to_dev(cb)))
+    assert np.array_equal(y.astype(np.float64), ref)
+
+
+@pytest.mark.parametrize("case", SPLIT_BOOK[:2])
+def test_split_codebook_random_against_oracle(case):
+    M, K, N, d, C, bits = case
+    print(f"[case] split codebook random {case}", flush=True)
+    rng = np.random.default_rng(53 + sum(case))
+    p = pi.draw_problem(rng, M, K, N, d, C, bits)
+    y = run("gemv", p)
+    assert_close(y, orc.pq_linear(p.x, p.idx, bits, d, p.codebook), f"split codebook {case}")
