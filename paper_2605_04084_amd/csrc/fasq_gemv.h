@@ -146,8 +146,9 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
   const uint32_t lane_off = repl_lane_off<D>(lane);
   const int mrow = MR == 1 ? 0 : (nl < M ? nl : M - 1);  // x row this lane feeds to the A operand
   const uint8_t* xrow = xl + mrow * a.xs;
-  // A operands (x) live in registers when they fit, else are read from LDS
-  // at every step.
+  // A operands (x) live in registers when they fit, loaded straight from
+  // global memory with the codebook (x takes no LDS then); else x is staged
+  // in LDS and read at every step.
   constexpr bool kXInRegs = !MASK && T * SPC <= 8;
   half8_t xreg[kXInRegs ? T * SPC : 1];
   const int nsl = MODE == CB_SLICE ? pt.nsl : 1;
@@ -170,13 +171,22 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
     CbStage cst;
     if constexpr (kStageSlice) slice_fetch(scb, sC * D * 2 / 16, cst);
     else cb_fetch<D, MODE>(pt.cb, pt.C, cst);
-    u32x4 xst[XWT];
+    u32x4 xst[kXInRegs ? 1 : XWT];
     if (si == 0) {
+      if constexpr (kXInRegs) {
+        const half_t* xg = a.x + (int64_t)mrow * a.K;
 #pragma unroll
-      for (int k = 0; k < XWT; ++k) {
-        int w = threadIdx.x + k * blockDim.x;
-        w = w < xw_total ? w : xw_total - 1;
-        xst[k] = reinterpret_cast<const u32x4*>(a.x)[w];
+        for (int t = 0; t < T; ++t)
+#pragma unroll
+          for (int s = 0; s < SPC; ++s)
+            xreg[t * SPC + s] = *reinterpret_cast<const half8_t*>(xg + ccol(t) * (G * D) + s * 8);
+      } else {
+#pragma unroll
+        for (int k = 0; k < XWT; ++k) {
+          int w = threadIdx.x + k * blockDim.x;
+          w = w < xw_total ? w : xw_total - 1;
+          xst[k] = reinterpret_cast<const u32x4*>(a.x)[w];
+        }
       }
     }
     __syncthreads();
@@ -185,7 +195,7 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
 
     if constexpr (kStageSlice) slice_store(smem, scb, sC * D * 2 / 16, cst);
     else cb_store<D, MODE>(smem, pt.cb, pt.C, cst);
-    if (si == 0) {
+    if (!kXInRegs && si == 0) {
 #pragma unroll
       for (int k = 0; k < XWT; ++k) {
         const int w = threadIdx.x + k * blockDim.x;
@@ -200,16 +210,6 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
       }
     }
     __syncthreads();
-
-    if (si == 0) {
-      if constexpr (kXInRegs) {
-#pragma unroll
-        for (int t = 0; t < T; ++t)
-#pragma unroll
-          for (int s = 0; s < SPC; ++s)
-            xreg[t * SPC + s] = *reinterpret_cast<const half8_t*>(xrow + ccol(t) * (G * D * 2) + s * 16);
-      }
-    }
 
     float4_t acc0 = {0.f, 0.f, 0.f, 0.f};
     float4_t acc1 = {0.f, 0.f, 0.f, 0.f};

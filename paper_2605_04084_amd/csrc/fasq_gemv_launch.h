@@ -148,7 +148,9 @@ hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev,
   int mode = choose_cb_mode(maxC, d);
   if (mode == CB_REPL && (total_rows + dev.num_cus - 1) / dev.num_cus * p.S < kReplMinIdsPerEntry * maxC) mode = CB_LDS;
   const int xs = (int)(p.M == 1 ? p.K * 2 : p.K * 2 + 16);
-  const int64_t x_bytes = p.M * (int64_t)xs;
+  // x in registers (loaded from global memory by each lane) needs no LDS
+  const bool x_in_regs = !mask && T * (G * d / 8) <= 8;
+  const int64_t x_bytes = x_in_regs ? 0 : p.M * (int64_t)xs;
   // The replicated table (up to 64 KB) gives way to one copy when it leaves
   // too little room beside x for one row group's partials.
   if (mode == CB_REPL &&

@@ -476,11 +476,13 @@ def test_sliced_codebook_boundaries_bit_exact(case):
     assert np.array_equal(y, ref)
 
 
-def test_wide_x_takes_the_decode_kernel_with_one_codebook_copy():
-    """M = 16 at K = 4096 keeps the decode kernel: the codebook drops to one
-    LDS copy (mode 1) to make room for x."""
-    assert fasq.plan("gemv", 16, 4096, 4096, 8, 2, 256).startswith("k_gemv<8, 2, ")
-    assert ", 1, 16, " in fasq.plan("gemv", 16, 4096, 4096, 8, 2, 256)
+def test_wide_x_in_registers_keeps_the_replicated_codebook():
+    """M = 16 at K = 4096 keeps the decode kernel: x goes from global memory
+    straight to registers and takes no LDS, so the replicated codebook
+    (mode 0) still fits; with x in LDS (a masked row) it drops to one copy
+    (mode 1)."""
+    assert fasq.plan("gemv", 16, 4096, 4096, 8, 2, 256) == "k_gemv<8, 2, 2, 0, 16, 0>"
+    assert ", 1, 16, 1>" in fasq.plan("gemv", 16, 4096 + 64, 4096, 8, 2, 256)
 
 
 # ---------------------------------------------------------------------------
