@@ -19,9 +19,11 @@ roofline figures and the kernel-sum microseconds per layer.  --per-matrix
 adds the same layer with one launch per matrix.
 
 Also reported: the effective 3-bit layer plus lm_head (d = 4, C = 4096,
-12-bit ids) and the prefill GEMM (M = 128 / 512 / 2048 tokens, d = 4,
-C = 256, 8-bit ids) in TFLOP/s.  --sweep adds the Qwen3-8B decode sweep
-(M = 1, 4, 16; C = 65536, 16-bit ids, codebook in L2).
+12-bit ids), the prefill GEMM (M = 128 / 512 / 2048 tokens, d = 4,
+C = 256, 8-bit ids) in TFLOP/s, and the Qwen3-8B decode layer at M = 1, 4
+and 16 tokens (C = 65536, 16-bit ids, a codebook larger than LDS), with the
+L2 request counts of its launches when profiles/counters.json matches the
+kernel sources.
 
 Algorithmic bytes of one GEMV: N*R (packed ids) + C*d*2 (codebook) +
 M*K*2 (x) + M*N*2 (y), with x counted once per grouped launch; flops of one
@@ -52,6 +54,7 @@ METRIC = "PQ GEMV HBM GB/s (% of peak) + us per Llama-3-8B layer; prefill PQ GEM
 ROTATION_BYTES = 1 << 30
 SPACER_CYCLES = 2_000_000      # spin kernel queued ahead of event-timed launches
 TIMING_COPIES = 12             # distinct copies one timing sample walks through
+MODEL_LAYERS = 32              # decoder layers of Llama-3-8B: the most layers one graph replays
 
 
 def log(*a):
@@ -127,7 +130,8 @@ class MatrixSet:
         # the decode calls that use one
         self.ws = []
         for p in problems:
-            need = fasq.gemv_ex_workspace_bytes(p.M, p.K, p.N, p.idx_bits, p.d, p.C, 0) if regime == "gemv" else 0
+            need = (fasq.gemv_ex_workspace_bytes(p.M, p.K, p.N, p.idx_bits, p.d, p.C, 0) if regime == "gemv" else
+                    fasq.gemm_ex_workspace_bytes(p.M, p.K, p.N, p.idx_bits, p.d, p.C) if regime == "gemm_ex" else 0)
             self.ws.append(torch.empty(need, dtype=torch.uint8, device=dev) if need > 0 else None)
         torch.cuda.synchronize()
 
@@ -145,6 +149,7 @@ class MatrixSet:
         if self.regime == "lut":
             return "k_gemm_lut"
         regime = "gemv_batched" if self.regime == "gemv" and len(self.groups[g]) > 1 else self.regime
+        regime = "gemm" if regime == "gemm_ex" else regime
         return self.fasq.plan(regime, p.M, p.K, p.N, p.idx_bits, p.d, p.C)
 
     def launch(self, c, g, stream):
@@ -154,7 +159,12 @@ class MatrixSet:
         if len(members) == 1:
             t = s[members[0]]
             ws = self.ws[members[0]]
-            if self.regime == "gemv" and ws is not None:
+            if self.regime == "gemm_ex":
+                st = self.fasq.gemm_ex_raw(x, p0.M, p0.K, p0.N, t["idx"].data_ptr(), p0.idx_bits, p0.d,
+                                           t["cb"].data_ptr(), p0.C, t["y"].data_ptr(),
+                                           ws.data_ptr() if ws is not None else 0, ws.numel() if ws is not None else 0,
+                                           stream)
+            elif self.regime == "gemv" and ws is not None:
                 # the decode call hands this matrix to the GEMM, which may split
                 # K with a workspace (fasq_pq_gemv_ex with one shared codebook)
                 st = self.fasq.gemv_ex_raw(x, p0.M, p0.K, p0.N, t["idx"].data_ptr(), p0.idx_bits, p0.d,
@@ -256,111 +266,393 @@ def source_hash():
     return h.hexdigest()[:16]
 
 
-TRAFFIC_PATH = os.path.join(ROOT, "profiles", "traffic.json")
-
-
-def load_traffic(kernel, names):
-    """Mean HBM bytes per launch of `kernel` over the launches `names` (launch
-    group names), from the committed rocprofv3 counter summary; None unless
-    that summary was taken on the current kernel sources."""
-    if not os.path.exists(TRAFFIC_PATH):
-        return None
-    try:
-        with open(TRAFFIC_PATH) as f:
-            data = json.load(f)
-    except (OSError, ValueError):
-        return None
-    if data.get("source_hash") != source_hash():
-        return None
-    per = data.get("launches", {})
-    vals = []
-    for n in names:
-        e = per.get(n)
-        if e is None or e.get("kernel") != kernel:
-            return None
-        vals.append(e["hbm_bytes_per_launch"])
-    return float(np.mean(vals))
-
-
 # ---------------------------------------------------------------------------
-# Counter passes: rocprofv3 --pmc runs a short fixed launch sequence, once for
-# FETCH_SIZE and once for WRITE_SIZE; --pmc-summarize turns the two CSVs into
-# profiles/traffic.json.
+# Counter passes.  `--pmc-pass MANIFEST` runs a short fixed launch sequence
+# (a calibration kernel of known traffic, then PMC_REPS cold launches of every
+# launch of the counter workloads below) under one `rocprofv3 --pmc` run per
+# counter group; `--pmc-report MANIFEST OUT_DIR PASS_DIR...` maps the
+# dispatches of all passes back onto the manifest and writes
+# profiles/counters.json (keyed to the kernel sources) and one Markdown
+# summary per kernel family.
 # ---------------------------------------------------------------------------
 
 PMC_REPS = 4
+COUNTERS_PATH = os.path.join(ROOT, "profiles", "counters.json")
+
+# rocprofv3 --pmc groups, one run each (within the per-block limits: at most
+# 8 SQ, 4 TCC, 4 TCP, 2 GRBM counters per run).
+PMC_GROUPS = {
+    "fetch": ["FETCH_SIZE"],
+    "write": ["WRITE_SIZE"],
+    "lds": ["SQ_INSTS_LDS", "SQ_LDS_BANK_CONFLICT", "SQ_LDS_ADDR_CONFLICT", "SQ_ACTIVE_INST_LDS",
+            "SQ_WAIT_INST_LDS", "SQ_LDS_IDX_ACTIVE", "SQ_BUSY_CU_CYCLES", "SQ_WAVES", "GRBM_GUI_ACTIVE"],
+    "alu": ["SQ_INSTS_VALU", "SQ_INSTS_MFMA", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_ACTIVE_INST_VALU",
+            "SQ_INSTS_SALU", "SQ_INSTS_VMEM_RD", "SQ_INSTS_SMEM", "SQ_WAVE_CYCLES", "GRBM_GUI_ACTIVE"],
+    "util": ["MfmaUtil", "LDSBankConflict", "VALUBusy"],
+    "l2": ["TCC_HIT_sum", "TCC_MISS_sum", "TCC_REQ_sum", "TCC_TAG_STALL_sum",
+           "TCP_TOTAL_CACHE_ACCESSES_sum", "TCP_TCC_READ_REQ_sum", "TCP_PENDING_STALL_CYCLES_sum",
+           "TCP_TCR_TCP_STALL_CYCLES_sum"],
+}
+
+# Counter workloads: (set, workload, M, launch grouping).  Every launch of a
+# set goes out PMC_REPS times on distinct copies.
+PMC_SETS = (
+    ("llama3_8b_4bit", "llama3_8b_4bit", 1),
+    ("llama3_8b_3bit", "llama3_8b_3bit", 1),
+    ("qwen3_8b_M1", "qwen3_8b_sweep", 1),
+    ("qwen3_8b_M4", "qwen3_8b_sweep", 4),
+    ("qwen3_8b_M16", "qwen3_8b_sweep", 16),
+)
+PMC_PREFILL = ((0, 128), (0, 2048), (1, 2048), (2, 512))  # (prefill matrix, M)
+
+
+def _ids_of(p):
+    return p.N * (p.K // p.d)
 
 
 def pmc_pass(torch, fasq, pi, manifest_path):
-    """The calibration kernel, then PMC_REPS cold launches of each launch group
-    of the effective-4-bit layer, in order.  Writes the launch manifest."""
+    """The calibration kernel, then PMC_REPS cold launches of every launch of
+    the counter workloads, in order.  Writes the launch manifest."""
     calibration_kernel(torch)
-    wl = pi.workload("llama3_8b_4bit")
-    problems = [wl.problem(i) for i in range(len(wl.matrices))]
-    names = [m.name for m in wl.matrices]
-    ms = MatrixSet(torch, fasq, problems, names, launch_groups(names), min_copies=PMC_REPS)
     stream = torch.cuda.current_stream().cuda_stream
-    torch.cuda.synchronize()
     seq = []
-    for g in range(len(ms.groups)):
-        for r in range(PMC_REPS):
-            ms.launch(r % ms.copies, g, stream)
+    for set_name, wl_name, M in PMC_SETS:
+        wl = pi.workload(wl_name)
+        problems = [wl.problem(i, M=M) for i in range(len(wl.matrices))]
+        names = [m.name for m in wl.matrices]
+        ms = MatrixSet(torch, fasq, problems, names, launch_groups(names), min_copies=PMC_REPS)
         torch.cuda.synchronize()
-        seq.append(dict(name=ms.group_name(g), reps=PMC_REPS, bytes=ms.group_bytes(g), kernel=ms.group_kernel(g)))
+        for g in range(len(ms.groups)):
+            for r in range(PMC_REPS):
+                ms.launch(r % ms.copies, g, stream)
+            torch.cuda.synchronize()
+            ps = [problems[i] for i in ms.groups[g]]
+            seq.append(dict(set=set_name, name=ms.group_name(g), reps=PMC_REPS, bytes=ms.group_bytes(g),
+                            kernel=ms.group_kernel(g), M=M, K=ps[0].K, N=[p.N for p in ps],
+                            ids=sum(_ids_of(p) for p in ps), flops=sum(2 * p.M * p.N * p.K for p in ps)))
+        del ms
+        torch.cuda.empty_cache()
+    wl = pi.workload("prefill")
+    dev = torch.device("cuda:0")
+    for i, M in PMC_PREFILL:
+        p = wl.problem(i, M=M)
+        x, idx, cb = (torch.from_numpy(a).to(dev) for a in (p.x, p.idx, p.codebook))
+        y = torch.empty((M, p.N), dtype=torch.float16, device=dev)
+        need = fasq.gemm_ex_workspace_bytes(M, p.K, p.N, p.idx_bits, p.d, p.C)
+        ws = torch.empty(max(need, 4), dtype=torch.uint8, device=dev)
+        torch.cuda.synchronize()
+        for r in range(PMC_REPS):
+            st = fasq.gemm_ex_raw(x.data_ptr(), M, p.K, p.N, idx.data_ptr(), p.idx_bits, p.d, cb.data_ptr(), p.C,
+                                  y.data_ptr(), ws.data_ptr(), need, stream)
+            assert st == 0, fasq.last_error()
+        torch.cuda.synchronize()
+        seq.append(dict(set="prefill", name=f"{wl.matrices[i].name} M={M}", reps=PMC_REPS,
+                        bytes=gemv_bytes(M, p.K, p.N, p.d, p.C, p.idx_bits),
+                        kernel=fasq.plan("gemm", M, p.K, p.N, p.idx_bits, p.d, p.C), M=M, K=p.K, N=[p.N],
+                        ids=_ids_of(p), flops=2 * M * p.N * p.K, k_split=need // (M * p.N * 4) if need else 1))
+        del x, idx, cb, y, ws
+    torch.cuda.empty_cache()
     with open(manifest_path, "w") as f:
         json.dump(dict(source_hash=source_hash(), calibration_bytes=CALIBRATION_BYTES, launches=seq), f, indent=1)
-    log(f"[bench] pmc pass: {len(seq)} launch groups x {PMC_REPS} launches, manifest {manifest_path}")
+    log(f"[bench] pmc pass: {len(seq)} launches x {PMC_REPS}, manifest {manifest_path}")
 
 
-def _read_counter_csv(path_or_dir, counter):
+def _read_counter_rows(pass_dir):
+    """{dispatch id: (kernel name, start, end, {counter: value})} of one pass."""
     import csv
     import glob
 
-    files = [path_or_dir] if os.path.isfile(path_or_dir) else sorted(
-        glob.glob(os.path.join(path_or_dir, "**", "*counter_collection.csv"), recursive=True))
+    files = [pass_dir] if os.path.isfile(pass_dir) else sorted(
+        glob.glob(os.path.join(pass_dir, "**", "*counter_collection.csv"), recursive=True))
     if not files:
-        raise SystemExit(f"no counter_collection.csv under {path_or_dir}")
-    rows = []
+        raise SystemExit(f"no counter_collection.csv under {pass_dir}")
+    out = {}
     for fn in files:
         with open(fn) as f:
             for r in csv.DictReader(f):
-                if r["Counter_Name"] == counter:
-                    rows.append((int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"])))
-    rows.sort()
-    return rows
+                d = out.setdefault(int(r["Dispatch_Id"]), [r["Kernel_Name"], int(r["Start_Timestamp"]),
+                                                           int(r["End_Timestamp"]), {}])
+                d[3][r["Counter_Name"]] = d[3].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    return out
 
 
-def pmc_summarize(manifest_path, fetch_dir, write_dir, out_path):
+def _short_kernel(name):
+    """'k_gemv_m1' from 'void fasq::k_gemv_m1<8, 2, 2, 0, false>(fasq::GemvM1Args)'."""
+    i = name.find("fasq::")
+    rest = name[i + 6:] if i >= 0 else name
+    return rest.split("<")[0].split("(")[0]
+
+
+def _pass_launches(rows, man):
+    """Counter sums of every manifest launch (all its dispatches, averaged over
+    its reps), the calibration counters, and the main kernel's mean duration."""
+    disp = sorted(rows.items())
+    cal = [v for _, v in disp if "neg" in v[0]]
+    ours = [v for _, v in disp if "fasq::" in v[0]]
+    pos = 0
+    res = []
+    for e in man["launches"]:
+        base = e["kernel"].split("<")[0]
+        sums, durs = {}, []
+        for _ in range(e["reps"]):
+            if pos >= len(ours) or _short_kernel(ours[pos][0]) != base:
+                got = _short_kernel(ours[pos][0]) if pos < len(ours) else "nothing"
+                raise SystemExit(f"dispatch {pos}: expected {base} for {e['set']}/{e['name']}, found {got}")
+            durs.append(ours[pos][2] - ours[pos][1])
+            while True:  # the main kernel and any helper kernels it queues (e.g. a split-K sum)
+                for c, v in ours[pos][3].items():
+                    sums[c] = sums.get(c, 0.0) + v
+                pos += 1
+                if pos >= len(ours) or _short_kernel(ours[pos][0]) == base or \
+                        not _short_kernel(ours[pos][0]).startswith(("k_gemm_split_reduce", "k_sub_reduce")):
+                    break
+        res.append(({c: v / e["reps"] for c, v in sums.items()}, float(np.median(durs)) * 1e-3))
+    if pos != len(ours):
+        raise SystemExit(f"{len(ours) - pos} library dispatches left over after the manifest")
+    calc = {}
+    for v in cal:
+        for c, x in v[3].items():
+            calc.setdefault(c, []).append(x)
+    return res, {c: float(np.median(x)) for c, x in calc.items()}
+
+
+def pmc_report(manifest_path, out_dir, pass_dirs):
     with open(manifest_path) as f:
         man = json.load(f)
-    result = dict(source_hash=man["source_hash"], counters_kib_per_dispatch=True, launches={})
-    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
-        rows = _read_counter_csv(d, counter)
-        cal = [v for _, k, v in rows if "neg" in k]
-        ours = [(k, v) for _, k, v in rows if "fasq::" in k]
-        if not cal:
-            raise SystemExit(f"{counter}: calibration kernel not found")
-        factor = float(np.median(cal)) * 1024.0 / man["calibration_bytes"]
-        result[f"{counter.lower()}_calibration_factor"] = factor
-        want = sum(e["reps"] for e in man["launches"])
-        if len(ours) != want:
-            raise SystemExit(f"{counter}: {len(ours)} library dispatches, manifest lists {want}")
-        pos = 0
-        for e in man["launches"]:
-            vals = [v for _, v in ours[pos:pos + e["reps"]]]
-            pos += e["reps"]
-            m = result["launches"].setdefault(e["name"], dict(kernel=e["kernel"], algorithmic_bytes=e["bytes"]))
-            m[f"{counter.lower()}_kib_raw"] = float(np.mean(vals))
-            m[f"{counter.lower()}_bytes"] = float(np.mean(vals)) * 1024.0 / factor
-    for m in result["launches"].values():
-        m["hbm_bytes_per_launch"] = m["fetch_size_bytes"] + m["write_size_bytes"]
-        m["traffic_over_algorithmic"] = m["hbm_bytes_per_launch"] / m["algorithmic_bytes"]
-    with open(out_path, "w") as f:
-        json.dump(result, f, indent=1)
+    launches = [dict(e, counters={}, counter_us={}) for e in man["launches"]]
+    factors = {}
+    for d in pass_dirs:
+        res, cal = _pass_launches(_read_counter_rows(d), man)
+        for (cnt, us), L in zip(res, launches):
+            L["counters"].update(cnt)
+            for c in cnt:
+                L["counter_us"][c] = us
+        for c in ("FETCH_SIZE", "WRITE_SIZE"):
+            if c in cal:  # KiB the counter reads per byte the calibration kernel moves
+                factors[c] = cal[c] * 1024.0 / man["calibration_bytes"]
+    for L in launches:
+        c = L["counters"]
+        der = {}
+        if "FETCH_SIZE" in c and "WRITE_SIZE" in c and factors:
+            hbm = c["FETCH_SIZE"] * 1024.0 / factors["FETCH_SIZE"] + c["WRITE_SIZE"] * 1024.0 / factors["WRITE_SIZE"]
+            der["hbm_bytes"] = hbm
+            der["traffic_over_algorithmic"] = hbm / L["bytes"]
+        if c.get("SQ_INSTS_LDS"):
+            der["lds_bank_conflict_cycles_per_lds_inst"] = c.get("SQ_LDS_BANK_CONFLICT", 0.0) / c["SQ_INSTS_LDS"]
+        for k, name in (("SQ_INSTS_VALU", "valu"), ("SQ_INSTS_MFMA", "mfma"), ("SQ_INSTS_LDS", "lds"),
+                        ("SQ_INSTS_VMEM_RD", "vmem_rd"), ("SQ_INSTS_SALU", "salu")):
+            if k in c:  # wave instructions x 64 lanes, per id
+                der[f"{name}_lane_insts_per_id"] = c[k] * 64.0 / L["ids"]
+        for k in ("MfmaUtil", "LDSBankConflict", "VALUBusy"):
+            if k in c:
+                der[k] = c[k]
+        if "TCC_HIT_sum" in c and "TCC_MISS_sum" in c and c["TCC_HIT_sum"] + c["TCC_MISS_sum"] > 0:
+            der["l2_hit_pct"] = 100.0 * c["TCC_HIT_sum"] / (c["TCC_HIT_sum"] + c["TCC_MISS_sum"])
+        for k, name in (("TCC_REQ_sum", "l2_requests"), ("TCP_TOTAL_CACHE_ACCESSES_sum", "l1_tag_accesses"),
+                        ("TCP_TCC_READ_REQ_sum", "l1_to_l2_reads")):
+            if k in c:
+                der[f"{name}_per_id"] = c[k] / L["ids"]
+        L["derived"] = der
+    out = dict(source_hash=man["source_hash"], calibration_factors=factors, reps=PMC_REPS,
+               launches={f"{L['set']}/{L['name']}": L for L in launches})
+    os.makedirs(out_dir, exist_ok=True)
+    with open(os.path.join(out_dir, "counters.json"), "w") as f:
+        json.dump(out, f, indent=1)
         f.write("\n")
-    for name, m in result["launches"].items():
-        log(f"{name:26s} {m['kernel']:28s} traffic {m['hbm_bytes_per_launch'] / 1e6:8.3f} MB, "
-            f"algorithmic {m['algorithmic_bytes'] / 1e6:8.3f} MB, ratio {m['traffic_over_algorithmic']:.3f}")
+    for L in launches:
+        d = L["derived"]
+        log(f"{L['set'] + '/' + L['name']:40s} {L['kernel']:36s} " +
+            " ".join(f"{k}={v:.3g}" for k, v in d.items()))
+
+
+# Markdown summaries of counters.json, one per counter set family.
+PMC_MD_FILES = (
+    ("k_gemv_m1_llama3_8b_4bit_counters.md", ("llama3_8b_4bit",),
+     "k_gemv_m1: Llama-3-8B decode layer at effective 4 bits (d = 2, C = 256, 8-bit ids, M = 1)"),
+    ("k_gemv_m1_llama3_8b_3bit_counters.md", ("llama3_8b_3bit",),
+     "k_gemv_m1: Llama-3-8B decode layer at effective 3 bits, lm_head included (d = 4, C = 4096, 12-bit ids, M = 1)"),
+    ("decode_qwen3_8b_counters.md", ("qwen3_8b_M1", "qwen3_8b_M4", "qwen3_8b_M16"),
+     "Qwen3-8B decode layer, 65536-entry codebooks larger than LDS (d = 4, 16-bit ids), M = 1, 4, 16"),
+    ("k_gemm_mfma_prefill_counters.md", ("prefill",),
+     "k_gemm_mfma: prefill GEMM (d = 4, C = 256, 8-bit ids) on Llama-3-8B shapes"),
+)
+
+PMC_MD_DERIVED = (
+    ("traffic_over_algorithmic", "HBM / algorithmic bytes", "{:.2f}"),
+    ("lds_bank_conflict_cycles_per_lds_inst", "LDS conflict cycles / LDS inst", "{:.2f}"),
+    ("LDSBankConflict", "LDS conflict % of time", "{:.1f}"),
+    ("valu_lane_insts_per_id", "VALU / id", "{:.2f}"),
+    ("mfma_lane_insts_per_id", "MFMA / id", "{:.3f}"),
+    ("lds_lane_insts_per_id", "LDS / id", "{:.2f}"),
+    ("VALUBusy", "VALU busy %", "{:.1f}"),
+    ("MfmaUtil", "MFMA busy %", "{:.1f}"),
+    ("l2_hit_pct", "L2 hit %", "{:.1f}"),
+    ("l2_requests_per_id", "L2 requests / id", "{:.3f}"),
+    ("l1_tag_accesses_per_id", "L1 tag accesses / id", "{:.3f}"),
+)
+
+
+def pmc_markdown(counters_path, out_dir):
+    with open(counters_path) as f:
+        data = json.load(f)
+    groups = "\n".join(f"timeout -s KILL 300 rocprofv3 --pmc {' '.join(cs)} --output-format csv -d gpurun_out/pmc_{g} "
+                       f"-o run -- \\\n    python3 bench.py --pmc-pass gpurun_out/pmc_manifest.json"
+                       for g, cs in PMC_GROUPS.items())
+    report = ("python3 bench.py --pmc-report gpurun_out/pmc_manifest.json gpurun_out/counters " +
+              " ".join(f"gpurun_out/pmc_{g}" for g in PMC_GROUPS) +
+              f"\npython3 bench.py --pmc-markdown gpurun_out/counters/counters.json profiles")
+    fac = data.get("calibration_factors", {})
+    for fname, sets, title in PMC_MD_FILES:
+        rows = [(k, e) for k, e in data["launches"].items() if e["set"] in sets]
+        if not rows:
+            continue
+        lines = [f"# {title}: rocprofv3 counters", "",
+                 "Commands (from the repository root on one MI355X; one `rocprofv3 --pmc` run per counter group, "
+                 "each over the same fixed launch sequence):", "", "```", "export TMPDIR=/tmp", groups, report, "```",
+                 "",
+                 f"Every launch below ran {data.get('reps', PMC_REPS)} times on distinct cold copies of its "
+                 "operands; values are means per launch.  SQ instruction counters count wave instructions; "
+                 "\"per id\" columns are wave instructions x 64 lanes / codeword ids of the launch (lane "
+                 "instructions per id), or L2 / L1 requests per id.  HBM bytes are FETCH_SIZE and WRITE_SIZE "
+                 "scaled by what they read for a 256 MiB fp16 negation (factors "
+                 + ", ".join(f"{k} {v:.4f}" for k, v in fac.items()) + "); FETCH_SIZE counts every L2 miss, "
+                 "so a line served by the Infinity Cache counts as HBM traffic here.  MfmaUtil, LDSBankConflict "
+                 "and VALUBusy are rocprofv3's derived percentages of GPU time.",
+                 "", f"Kernel sources hash: `{data['source_hash']}` (bench.py uses these counters only while the "
+                 "sources match).", ""]
+        hdr = "| Launch | Kernel | µs (counter run) | " + " | ".join(h for _, h, _ in PMC_MD_DERIVED) + " |"
+        lines += [hdr, "|" + "---|" * 3 + "---:|" * len(PMC_MD_DERIVED)]
+        for k, e in rows:
+            d = e["derived"]
+            us = next(iter(e.get("counter_us", {}).values()), float("nan"))
+            cells = [fmt.format(d[key]) if key in d else "—" for key, _, fmt in PMC_MD_DERIVED]
+            lines.append(f"| {k} | `{e['kernel']}` | {us:.1f} | " + " | ".join(cells) + " |")
+        lines += ["", "Raw counters (mean per launch):", ""]
+        names = sorted({c for _, e in rows for c in e["counters"]})
+        lines += ["| Launch | " + " | ".join(names) + " |", "|---|" + "---:|" * len(names)]
+        for k, e in rows:
+            lines.append(f"| {k} | " + " | ".join(f"{e['counters'][c]:.4g}" if c in e["counters"] else "—"
+                                                     for c in names) + " |")
+        lines += ["", "Algorithmic bytes, ids and flops per launch:", "",
+                  "| Launch | Algorithmic bytes | HBM bytes (counters) | ids | flops |", "|---|---:|---:|---:|---:|"]
+        for k, e in rows:
+            hb = e["derived"].get("hbm_bytes")
+            lines.append(f"| {k} | {e['bytes']} | {hb:.0f} | {e['ids']} | {e['flops']} |" if hb is not None else
+                         f"| {k} | {e['bytes']} | — | {e['ids']} | {e['flops']} |")
+        with open(os.path.join(out_dir, fname), "w") as f:
+            f.write("\n".join(lines) + "\n")
+        log(f"[bench] wrote {os.path.join(out_dir, fname)}")
+
+
+def trace_markdown(trace_dir, bench_json, out_path):
+    """The kernel-statistics summary of a `rocprofv3 --kernel-trace --stats`
+    run of the default bench (without the CPU leg), with the agreement between
+    the profiler's durations and bench.py's HIP-event figures."""
+    import csv
+    import glob
+
+    def one(pattern):
+        files = sorted(glob.glob(os.path.join(trace_dir, "**", pattern), recursive=True))
+        if not files:
+            raise SystemExit(f"no {pattern} under {trace_dir}")
+        with open(files[0]) as f:
+            return list(csv.DictReader(f))
+
+    stats = one("*kernel_stats.csv")
+    trace = sorted(one("*kernel_trace.csv"), key=lambda r: int(r["Dispatch_Id"]))
+    with open(bench_json) as f:
+        bt = json.load(f)
+
+    def short(name):
+        return name.replace("void fasq::", "").split("(")[0].replace("false", "0").replace("true", "1")
+
+    lines = ["# libfasq kernels: rocprofv3 kernel statistics of the default bench.py run", "",
+             "Command (from the repository root, on one MI355X):", "", "```", "export TMPDIR=/tmp",
+             "rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof -o run -- \\",
+             "    python3 bench.py --no-cpu --out gpurun_out/bench_under_trace.json",
+             f"python3 bench.py --trace-markdown gpurun_out/prof gpurun_out/bench_under_trace.json {out_path}",
+             "```", "",
+             "The profiled run is the default bench without the CPU oracle leg: the Llama-3-8B decode layers at "
+             "effective 4 bits (M = 1 and 2) and 3 bits (lm_head included), the prefill GEMM, the Qwen3-8B decode "
+             "layer at M = 1, 4, 16, the batch-size crossover and the sensitivity points.  Only library kernels "
+             "are listed.", "",
+             "| Kernel | Calls | Average µs | Min µs | Max µs |", "|---|---:|---:|---:|---:|"]
+    avg = {}
+    for r in stats:
+        if "fasq::" not in r["Name"]:
+            continue
+        avg[short(r["Name"])] = float(r["AverageNs"]) / 1e3
+        lines.append(f"| `{short(r['Name'])}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.3f} | "
+                     f"{float(r['MinNs']) / 1e3:.3f} | {float(r['MaxNs']) / 1e3:.3f} |")
+    rl = bt["roofline"]
+    dom, on = rl["kernel"].split(" on ")
+    lines += ["", f"Dominant kernel of the decode layer: `{dom}` ({on}).", "",
+              f"- bench.py, HIP events in the same profiled run: {rl['us_per_launch']:.3f} µs per launch "
+              "(mean over its launches)",
+              f"- rocprofv3 average over every launch of that kernel in the run: {avg.get(dom, float('nan')):.3f} µs "
+              "(this average also takes in the eager warm-up launches and every other workload that maps to the "
+              "same instantiation)", ""]
+    tab = bt["launch_table"]
+    nl = len(tab)
+    lpg = int(bt["config"]["timed_region"].split("HIP graph replays, ")[1].split(" ")[0])
+    kern = {r["kernel"] for r in tab}
+    g = [r for r in trace if short(r["Kernel_Name"]) in kern]
+    dur = np.array([(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in g])
+    # the layer's launches come first: the eager warm-up (one layer per copy),
+    # then the warm-up and timed graph replays, lpg layers each
+    nlay = bt["config"]["rotation_copies"] + (bt["warmup"] + bt["steps"] // lpg) * lpg
+    if dur.size >= nlay * nl:
+        D = dur[:nlay * nl].reshape(nlay, nl)
+        lines += ["Per launch of the effective-4-bit layer (M = 1): rocprofv3 median duration over the eager "
+                  "warm-up and the graph replays, against bench.py's HIP events:", "",
+                  "| Launch | rows (N) × K | rocprofv3 median µs | bench.py µs (events) |", "|---|---|---:|---:|"]
+        for j, m in enumerate(tab):
+            lines.append(f"| {m['name']} | {'+'.join(str(n) for n in m['N'])} × {m['K']} | "
+                         f"{np.median(D[:, j]):.2f} | {m['us_median']:.2f} |")
+        # gaps between consecutive kernels inside the timed graph replays
+        starts = np.array([int(r["Start_Timestamp"]) for r in g[:nlay * nl]], dtype=np.float64)
+        ends = np.array([int(r["End_Timestamp"]) for r in g[:nlay * nl]], dtype=np.float64)
+        first_timed = (bt["config"]["rotation_copies"] + bt["warmup"] * lpg) * nl
+        gaps = []
+        for k in range(bt["steps"] // lpg):
+            a = first_timed + k * lpg * nl
+            gaps.extend((starts[a + 1:a + lpg * nl] - ends[a:a + lpg * nl - 1]) / 1e3)
+        if gaps:
+            gaps = np.array(gaps)
+            lines += ["", f"Gap between the end of one kernel and the start of the next inside the timed graph "
+                      f"replays ({gaps.size} gaps): median {np.median(gaps):.2f} µs, mean {gaps.mean():.2f} µs, "
+                      f"max {gaps.max():.2f} µs."]
+    with open(out_path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    log(f"[bench] wrote {out_path}")
+
+
+def load_counters():
+    """counters.json if it was taken on the current kernel sources, else None."""
+    if not os.path.exists(COUNTERS_PATH):
+        return None
+    try:
+        with open(COUNTERS_PATH) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        return None
+    return data if data.get("source_hash") == source_hash() else None
+
+
+def load_traffic(kernel, set_name, names):
+    """Mean HBM bytes per launch of `kernel` over the launches `names` of
+    counter set `set_name`; None unless the counters were taken on the
+    current kernel sources."""
+    data = load_counters()
+    if data is None:
+        return None
+    vals = []
+    for n in names:
+        e = data["launches"].get(f"{set_name}/{n}")
+        if e is None or e.get("kernel") != kernel or "hbm_bytes" not in e.get("derived", {}):
+            return None
+        vals.append(e["derived"]["hbm_bytes"])
+    return float(np.mean(vals))
 
 
 # ---------------------------------------------------------------------------
@@ -374,21 +666,25 @@ def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None, gro
     problems = [wl.problem(i, M=M) for i in mats]
     names = [wl.matrices[i].name for i in mats]
     groups = launch_groups(names) if grouped else None
-    ms = MatrixSet(torch, fasq, problems, names, groups, min_copies=TIMING_COPIES)
-    log(f"[bench] {wl_name}: {ms.bytes_per_set / 1e6:.1f} MB per layer, {ms.copies} copies, "
-        f"{len(ms.groups)} launches")
     # Consecutive layers go into one graph, as a decode step replays every
     # layer of the model from one graph: the graph launch boundary is paid
     # once per lpg layers, lpg the largest divisor of the step count that is
-    # at most the number of copies.
-    lpg = max(k for k in range(1, min(steps, ms.copies) + 1) if steps % k == 0)
+    # at most MODEL_LAYERS.  Each layer of a graph reads its own copy.
+    lpg = max(k for k in range(1, min(steps, MODEL_LAYERS) + 1) if steps % k == 0)
+    ms = MatrixSet(torch, fasq, problems, names, groups, min_copies=max(TIMING_COPIES, lpg))
+    log(f"[bench] {wl_name}: {ms.bytes_per_set / 1e6:.1f} MB per layer, {ms.copies} copies, "
+        f"{len(ms.groups)} launches, {lpg} layers per graph")
     graphs = ms.capture_graphs(lpg)
     for s in range(warmup):
         graphs[s % ms.copies].replay()
     torch.cuda.synchronize()
+    # The timed replays continue where the last warm-up graph stopped (it read
+    # copies w .. w + lpg - 1): every copy the timed loop reads was last read
+    # at least copies - 1 layers earlier, far more than the 256 MB MALL holds.
+    start = ((warmup - 1) % ms.copies + lpg) % ms.copies if warmup > 0 else 0
     t0 = time.perf_counter()
     for r in range(steps // lpg):
-        graphs[(r * lpg) % ms.copies].replay()
+        graphs[(start + r * lpg) % ms.copies].replay()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     del graphs
@@ -513,7 +809,11 @@ def time_dense(torch, M, K, N, steps=10, short=2, long=10):
     return max(float(np.median(per)), 1e-7)
 
 
-def sensitivity(torch, fasq, pi):
+def sensitivity(torch, fasq, pi, core=False):
+    """The paper's sensitivity sweeps (Sec. 4.4, Fig. sensitivity) on one
+    4096 x 4096 layer.  core: the points the default run reports (codebook
+    size 16 / 64 / 256, every sub-vector length, the L = 32 prefill, the
+    per-subspace layer); the batch-size sweep is the crossover measurement."""
     out = dict(shape=f"{SENS_N}x{SENS_K}", codebook_size=[], subvector=[], batch=[], prefill=[])
     rng = np.random.default_rng(2026)
 
@@ -528,7 +828,7 @@ def sensitivity(torch, fasq, pi):
     dense1 = time_dense(torch, 1, SENS_K, SENS_N)
     out["dense_fp16_gemv_us"] = dense1 * 1e6
     log(f"[bench] sensitivity: dense fp16 GEMV (torch.matmul, M=1) {dense1 * 1e6:.2f} us")
-    for C in (16, 32, 64, 128, 256):
+    for C in ((16, 64, 256) if core else (16, 32, 64, 128, 256)):
         r = gemv_row(1, 2, C, 8)
         out["codebook_size"].append(r)
         log(f"[bench] sensitivity C={C:4d} d=2: {r['us']:.2f} us ({r['gbs']:.0f} GB/s) {r['kernel']}")
@@ -536,7 +836,7 @@ def sensitivity(torch, fasq, pi):
         r = gemv_row(1, d, 256, 8)
         out["subvector"].append(r)
         log(f"[bench] sensitivity d={d} C=256: {r['us']:.2f} us ({r['gbs']:.0f} GB/s) {r['kernel']}")
-    for M in (1, 2, 4, 8, 16, 32, 64, 128):
+    for M in (() if core else (1, 2, 4, 8, 16, 32, 64, 128)):
         row = dict(M=M, dense_us=time_dense(torch, M, SENS_K, SENS_N) * 1e6)
         if M <= 16:
             row["gemv_us"] = gemv_row(M, 2, 256, 8)["us"]
@@ -544,15 +844,90 @@ def sensitivity(torch, fasq, pi):
         out["batch"].append(row)
         log(f"[bench] sensitivity batch M={M:3d}: gemv {row.get('gemv_us', float('nan')):8.2f} us, "
             f"gemm {row['gemm_us']:8.2f} us, dense fp16 {row['dense_us']:8.2f} us")
-    for L in (32, 64, 128, 256, 512, 1024, 2048):
+    for L in ((32,) if core else (32, 64, 128, 256, 512, 1024, 2048)):
         r = gemv_row(L, 2, 256, 8, regime="gemm")
+        r["k_split_us"] = gemv_row(L, 2, 256, 8, regime="gemm_ex")["us"]
         r["dense_us"] = time_dense(torch, L, SENS_K, SENS_N) * 1e6
         if L in (32, 128, 512, 2048):  # the paper's lookup-table GEMM design (Alg. 3), for comparison
             r["lut_us"] = gemv_row(L, 2, 256, 8, regime="lut")["us"]
         out["prefill"].append(r)
         log(f"[bench] sensitivity prefill L={L:5d}: {r['us']:8.2f} us ({r['tflops']:.0f} TFLOP/s), "
+            f"with K split {r['k_split_us']:8.2f} us, "
             f"dense fp16 {r['dense_us']:8.2f} us" + (f", lookup-table GEMM {r['lut_us']:9.2f} us" if "lut_us" in r else ""))
     torch.cuda.empty_cache()
+    return out
+
+
+CROSSOVER_M = (1, 2, 4, 8, 12, 16, 20, 24, 32, 48, 64)
+CROSSOVER_MATS = (0, 1, 4, 6)  # q_proj, k_proj, gate_proj, down_proj of the Llama-3-8B layer
+
+
+def crossover(torch, fasq, pi, Ms=CROSSOVER_M, steps=5, short=2, long=10):
+    """Batch-size dispatch of the decode entry point (the paper leaves an
+    adaptive GEMV/GEMM switch to future work, Sec. 4.4 "Batch size").
+
+    On the four distinct Llama-3-8B layer shapes at effective 4 bits (d = 2,
+    C = 256, 8-bit ids), per-call time of fasq_pq_gemv (the kernel its
+    dispatch picks for M tokens) and of the prefill GEMM with its K split
+    (fasq_pq_gemm_ex, workspace allocated outside the timed region), at every
+    M in Ms.  The id table is read cold (rotated copies); x and y stay hot."""
+    wl = pi.workload("llama3_8b_4bit")
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    out = []
+    for i in CROSSOVER_MATS:
+        spec = wl.matrices[i]
+        p = wl.problem(i, M=max(Ms))
+        copies = max(short + long, math.ceil(ROTATION_BYTES / p.idx.nbytes) + 1)
+        base = torch.from_numpy(p.idx).to(dev)
+        idxs = [base.clone() for _ in range(copies)]
+        del base
+        cb = torch.from_numpy(p.codebook).to(dev)
+        x_all = torch.from_numpy(p.x).to(dev)
+        y = torch.empty((max(Ms), p.N), dtype=torch.float16, device=dev)
+        need_max = max(fasq.gemm_ex_workspace_bytes(M, p.K, p.N, p.idx_bits, p.d, p.C) for M in Ms)
+        ws = torch.empty(max(need_max, 4), dtype=torch.uint8, device=dev)
+        torch.cuda.synchronize()
+        for M in Ms:
+            x = x_all[:M]
+            need = fasq.gemm_ex_workspace_bytes(M, p.K, p.N, p.idx_bits, p.d, p.C)
+
+            def call(regime, c):
+                if regime == "gemv":
+                    st = fasq.gemv_raw(x.data_ptr(), M, p.K, p.N, idxs[c].data_ptr(), p.idx_bits, p.d, cb.data_ptr(),
+                                       p.C, y.data_ptr(), stream.cuda_stream)
+                else:
+                    st = fasq.gemm_ex_raw(x.data_ptr(), M, p.K, p.N, idxs[c].data_ptr(), p.idx_bits, p.d,
+                                          cb.data_ptr(), p.C, y.data_ptr(), ws.data_ptr(), need, stream.cuda_stream)
+                assert st == 0, fasq.last_error()
+
+            row = dict(name=spec.name, N=p.N, K=p.K, M=M)
+            for regime in ("gemv", "gemm_ex"):
+                for c in range(copies):
+                    call(regime, c)
+
+                def batch(first, count):
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    torch.cuda._sleep(SPACER_CYCLES)
+                    e0.record(stream)
+                    for j in range(count):
+                        call(regime, (first + j) % copies)
+                    e1.record(stream)
+                    e1.synchronize()
+                    return e0.elapsed_time(e1) * 1e-3
+
+                t = [(batch(0, long) - batch(long, short)) / (long - short) for _ in range(steps)]
+                row[f"{regime}_us"] = max(float(np.median(t)), 1e-7) * 1e6
+            row["gemv_kernel"] = fasq.plan("gemv", M, p.K, p.N, p.idx_bits, p.d, p.C)
+            row["gemm_kernel"] = fasq.plan("gemm", M, p.K, p.N, p.idx_bits, p.d, p.C)
+            row["gemm_k_split"] = need // (M * p.N * 4) if need else 1
+            row["faster"] = "gemv" if row["gemv_us"] <= row["gemm_ex_us"] else "gemm_ex"
+            out.append(row)
+            log(f"[bench] crossover {spec.name:9s} M={M:3d}: fasq_pq_gemv {row['gemv_us']:7.2f} us "
+                f"({row['gemv_kernel']}), GEMM with K split {row['gemm_ex_us']:7.2f} us "
+                f"(split {row['gemm_k_split']})")
+        del idxs, cb, x_all, y, ws
+        torch.cuda.empty_cache()
     return out
 
 
@@ -741,6 +1116,31 @@ def cpu_baseline(pi, frac=1.0):
                        f"{blas} BLAS threads; {len(os.sched_getaffinity(0))} cores in the affinity mask")
 
 
+# L2 (TCC) request rate of MI355X: 8 XCDs x 16 channels, one 128-byte tag
+# lookup per channel and clock, at the 2.4 GHz peak engine clock.
+L2_REQ_PER_S = 8 * 16 * 2.4e9
+
+
+def qwen_l2_summary(counters, M, res):
+    """L2 requests per layer of the Qwen3-8B launches at M tokens (counters
+    taken on the current sources), and the time the L2 request rate alone
+    would need for them; None without such counters."""
+    if counters is None:
+        return None
+    reqs, hits, misses = 0.0, 0.0, 0.0
+    for r in res["launch_table"]:
+        e = counters["launches"].get(f"qwen3_8b_M{M}/{r['name']}")
+        if e is None or "TCC_REQ_sum" not in e["counters"]:
+            return None
+        c = e["counters"]
+        reqs += c["TCC_REQ_sum"]
+        hits += c.get("TCC_HIT_sum", 0.0)
+        misses += c.get("TCC_MISS_sum", 0.0)
+    return dict(requests_per_layer=reqs, l2_hit_pct=100.0 * hits / max(hits + misses, 1.0),
+                request_floor_us=reqs / L2_REQ_PER_S * 1e6, request_rate_assumed_per_s=L2_REQ_PER_S,
+                source="profiles/counters.json (rocprofv3 --pmc TCC_REQ_sum, TCC_HIT_sum, TCC_MISS_sum)")
+
+
 def report_layer(tag, res):
     for r in res["launch_table"]:
         log(f"[bench] {tag} {r['name']:26s} K={r['K']:6d}: {r['us_median']:7.2f} us "
@@ -755,7 +1155,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--sweep", action="store_true", help="add the Qwen3-8B M=1/4/16 decode sweep")
+    ap.add_argument("--sweep", action="store_true",
+                    help="the Qwen3-8B M=1/4/16 decode sweep even with --no-extra (it is part of the default run)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-extra", action="store_true", help="only the effective-4-bit decode layer")
     ap.add_argument("--per-matrix", action="store_true", help="add the 4-bit layer with one launch per matrix")
@@ -765,12 +1166,30 @@ def main():
     ap.add_argument("--out", default=None, help="also write the JSON record to this file")
     ap.add_argument("--pmc-pass", metavar="MANIFEST", default=None,
                     help="run the short launch sequence for a rocprofv3 --pmc pass and write its manifest")
-    ap.add_argument("--pmc-summarize", nargs=4, metavar=("MANIFEST", "FETCH_DIR", "WRITE_DIR", "OUT"),
-                    default=None, help="turn two --pmc passes (FETCH_SIZE, WRITE_SIZE) into a traffic summary")
+    ap.add_argument("--pmc-groups", action="store_true",
+                    help="print the rocprofv3 --pmc counter groups, one line each (name: counters)")
+    ap.add_argument("--pmc-report", nargs="+", metavar="ARG", default=None,
+                    help="MANIFEST OUT_DIR PASS_DIR...: turn --pmc passes into counters.json")
+    ap.add_argument("--trace-markdown", nargs=3, metavar=("TRACE_DIR", "BENCH_JSON", "OUT_MD"), default=None,
+                    help="write the kernel-statistics summary of a rocprofv3 --kernel-trace --stats run")
+    ap.add_argument("--pmc-markdown", nargs=2, metavar=("COUNTERS_JSON", "OUT_DIR"), default=None,
+                    help="write the Markdown counter summaries of a counters.json")
     args = ap.parse_args()
 
-    if args.pmc_summarize:
-        pmc_summarize(*args.pmc_summarize)
+    if args.pmc_groups:
+        for g, cs in PMC_GROUPS.items():
+            print(f"{g}: {' '.join(cs)}")
+        return
+    if args.trace_markdown:
+        trace_markdown(*args.trace_markdown)
+        return
+    if args.pmc_markdown:
+        pmc_markdown(*args.pmc_markdown)
+        return
+    if args.pmc_report:
+        if len(args.pmc_report) < 3:
+            ap.error("--pmc-report needs MANIFEST OUT_DIR PASS_DIR...")
+        pmc_report(args.pmc_report[0], args.pmc_report[1], args.pmc_report[2:])
         return
 
     if args.gpus != 1:
@@ -811,7 +1230,8 @@ def main():
     dom_kernel, dom = max(pools.items(), key=lambda kv: kv[1]["us"])
     achieved = (dom["bytes"] / dom["n"]) / (dom["us"] / dom["n"] * 1e-6) / 1e9
     roofline = dict(bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
-                    frac=achieved / HBM_PEAK_GBS, traffic=load_traffic(dom_kernel, dom["names"]),
+                    frac=achieved / HBM_PEAK_GBS,
+                    traffic=load_traffic(dom_kernel, "llama3_8b_4bit", dom["names"]),
                     kernel=f"{dom_kernel} on {', '.join(dom['names'])}",
                     bytes_per_launch=dom["bytes"] / dom["n"], us_per_launch=dom["us"] / dom["n"])
 
@@ -829,15 +1249,27 @@ def main():
         r1 = decode_layer(torch, fasq, pi, "llama3_8b_4bit", max(10, args.steps // 2), 3, grouped=False)
         report_layer("4bit, one launch per matrix", r1)
         extra["llama3_8b_4bit_per_matrix"] = r1
-    if args.sweep:
+    if not args.no_extra or args.sweep:
+        # The Qwen3-8B decode layer (65536-entry codebooks, larger than LDS)
+        # at 1, 4 and 16 tokens, with what the L2 counters of the same
+        # launches say about the gather path.
+        counters = load_counters()
         for M in (1, 4, 16):
             r5 = decode_layer(torch, fasq, pi, "qwen3_8b_sweep", max(10, args.steps // 2), 3, M=M)
-            log(f"[bench] qwen M={M}: kernel sum {r5['us_per_layer_kernel_sum']:.2f} us/layer "
-                f"({r5['gbs_kernel_sum']:.1f} GB/s); x36 layers {36 * r5['us_per_layer_kernel_sum'] / 1e3:.3f} ms")
+            report_layer(f"qwen3 M={M}", r5)
+            r5["l2"] = qwen_l2_summary(counters, M, r5)
+            log(f"[bench] qwen3 M={M}: kernel sum {r5['us_per_layer_kernel_sum']:.2f} us/layer "
+                f"({r5['gbs_kernel_sum']:.1f} GB/s); x36 layers {36 * r5['us_per_layer_kernel_sum'] / 1e3:.3f} ms"
+                + (f"; L2 requests {r5['l2']['requests_per_layer'] / 1e6:.1f} M per layer, request-rate floor "
+                   f"{r5['l2']['request_floor_us']:.1f} us" if r5["l2"] else ""))
             extra[f"qwen3_8b_M{M}"] = r5
 
+    if not args.no_extra:
+        extra["crossover"] = crossover(torch, fasq, pi)
     if args.sensitivity:
         extra["sensitivity"] = sensitivity(torch, fasq, pi)
+    elif not args.no_extra:
+        extra["sensitivity"] = sensitivity(torch, fasq, pi, core=True)
     if args.encode:
         extra["encode"] = encode_timing(torch, fasq, pi)
 

@@ -32,8 +32,10 @@
  *
  * Conventions:
  *   - Every call is asynchronous on `stream` (0 = the null stream).  The
- *     library keeps no pointer after returning, allocates no device memory,
- *     and uses no workspace, so the calls may be captured in a hipGraph.
+ *     library keeps no pointer after returning and allocates no device
+ *     memory, so the calls may be captured in a hipGraph.  The plain entry
+ *     points use no scratch memory; the _ex calls and the encoder take a
+ *     caller-owned workspace argument for theirs.
  *   - Argument checks run before any HIP call.  A bad argument returns
  *     FASQ_ERR_INVALID_ARG and launches nothing.  A failed launch returns
  *     FASQ_ERR_HIP.  fasq_last_error() then describes the failure (per calling
@@ -253,8 +255,11 @@ fasq_status fasq_pq_reconstruct(const void* idx, int64_t N, int64_t K, int idx_b
                                 hipStream_t stream);
 
 /*
- * Bytes of one packed index row: ceil((K / d) * idx_bits / 8).  Returns -1
- * when K < 1, d < 1, K % d != 0 or idx_bits is not 8, 12 or 16.  Host only.
+ * Bytes of one packed index row: ceil((K / d) * idx_bits / 8).  Each of the
+ * K / d sub-vectors of a row stores one codeword id of ceil(log2 K_s) bits
+ * (FASQ Sec. 3.2, the index term of the storage footprint); ids are packed
+ * as the bit stream described at the top of this file.  Returns -1 when
+ * K < 1, d < 1, K % d != 0 or idx_bits is not 8, 12 or 16.  Host only.
  */
 int64_t fasq_idx_row_bytes(int64_t K, int d, int idx_bits);
 

@@ -20,17 +20,44 @@ hipError_t launch_gemv_u8_m16(const Problem* ps, int count, const DeviceInfo& de
 hipError_t launch_gemv_u12_m16(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream);
 hipError_t launch_gemv_u16_m16(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream);
 
+namespace {
+
+hipError_t launch_gemv_m1_group(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream) {
+  switch (ps[0].idx_bits) {
+    case 8: return launch_gemv_u8_m1(ps, count, dev, stream);
+    case 12: return launch_gemv_u12_m1(ps, count, dev, stream);
+    default: return launch_gemv_u16_m1(ps, count, dev, stream);
+  }
+}
+
+// Whether the row-streaming kernel would take matrix p alone (nothing is
+// launched: the launcher runs in planning mode).
+bool m1_takes_alone(const Problem& p, const DeviceInfo& dev) {
+  Plan& pl = plan();
+  const Plan saved = pl;
+  pl.active = true;
+  const hipError_t e = launch_gemv_m1_group(&p, 1, dev, nullptr);
+  pl = saved;
+  return e == hipSuccess;
+}
+
+}  // namespace
+
 hipError_t launch_gemv_group(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream) {
   const Problem& p = ps[0];
   if (p.M < 1 || p.M > 16) return hipErrorNotSupported;
   if (p.M <= kM1MaxTokens) {  // the row-streaming kernel when its codebook placement allows
-    hipError_t e;
-    switch (p.idx_bits) {
-      case 8: e = launch_gemv_u8_m1(ps, count, dev, stream); break;
-      case 12: e = launch_gemv_u12_m1(ps, count, dev, stream); break;
-      default: e = launch_gemv_u16_m1(ps, count, dev, stream);
-    }
+    hipError_t e = launch_gemv_m1_group(ps, count, dev, stream);
     if (e != hipErrorNotSupported || p.M == 1) return e;
+    // Two tokens and a group the two-token kernel cannot take (a codebook
+    // too large for LDS).  A member that it would take alone must not run
+    // on the 16-row-tile kernel here: the two kernels add their fp32
+    // partials in different orders, and a grouped output has to equal the
+    // single call's bit for bit.  The caller then runs the matrices one by
+    // one.
+    if (count > 1)
+      for (int i = 0; i < count; ++i)
+        if (m1_takes_alone(ps[i], dev)) return hipErrorNotSupported;
   }
   switch (p.idx_bits) {
     case 8: return launch_gemv_u8_m16(ps, count, dev, stream);

@@ -54,26 +54,6 @@ __device__ __forceinline__ uint32_t load_id_bytes(const uint8_t* __restrict__ ro
   }
 }
 
-// Id j (0 <= j < ids per chunk) of a chunk held in registers.
-//   BITS 8 : 16 ids in 4 dwords, byte j
-//   BITS 16:  8 ids in 4 dwords, halfword j
-//   BITS 12:  8 ids in 3 dwords (96 bits), field j
-template <int BITS>
-__device__ __forceinline__ uint32_t chunk_id(const uint32_t* w, int j) {
-  if constexpr (BITS == 8) {
-    return __builtin_amdgcn_ubfe(w[j >> 2], (j & 3) * 8, 8);
-  } else if constexpr (BITS == 16) {
-    return __builtin_amdgcn_ubfe(w[j >> 1], (j & 1) * 16, 16);
-  } else {
-    const int bit = 12 * j;
-    const int word = bit >> 5;
-    const int sh = bit & 31;
-    if (sh <= 20) return __builtin_amdgcn_ubfe(w[word], sh, 12);
-    // field straddles two dwords: funnel-shift the pair, then mask
-    return __builtin_amdgcn_alignbit(w[word + 1], w[word], sh) & 0xFFFu;
-  }
-}
-
 // ---------------------------------------------------------------------------
 // Reductions (DPP within rows of 16 lanes)
 // ---------------------------------------------------------------------------

@@ -57,6 +57,9 @@ __all__ = [
     "signed_one_hot_codebook",
     "scaled_signed_one_hot_codebook",
     "ternary_x",
+    "subnormal_codebook",
+    "subnormal_x",
+    "FP16_SUBNORMAL_UNIT",
 ]
 
 SUPPORTED_IDX_BITS = (8, 12, 16)
@@ -290,6 +293,35 @@ def scaled_signed_one_hot_codebook(C: int, d: int, rng: np.random.Generator) -> 
 def ternary_x(rng: np.random.Generator, M: int, K: int) -> np.ndarray:
     """Activations drawn uniformly from {-1, 0, 1}, fp16."""
     return rng.integers(-1, 2, size=(M, K)).astype(np.float16)
+
+
+# The smallest positive fp16 subnormal, 2**-24.  Every fp16 subnormal is an
+# integer k (1 <= k <= 1023) times it.
+FP16_SUBNORMAL_UNIT = 2.0 ** -24
+
+
+def _signed_subnormal_bits(rng: np.random.Generator, shape, large_frac: float) -> np.ndarray:
+    """fp16 bit patterns of +-k * 2**-24 with k in {0, 1, 2, 3} (k = 0 gives
+    +0 or -0), a `large_frac` share of them replaced by k in {512, 1023} (the
+    largest subnormal).  Every value is an fp16 subnormal or a signed zero."""
+    k = rng.integers(0, 4, size=shape).astype(np.uint16)
+    if large_frac > 0.0:
+        big = rng.random(size=shape) < large_frac
+        k = np.where(big, rng.choice(np.array([512, 1023], np.uint16), size=shape), k)
+    sign = rng.integers(0, 2, size=shape).astype(np.uint16) << np.uint16(15)
+    return (k | sign).astype(np.uint16)
+
+
+def subnormal_codebook(rng: np.random.Generator, C: int, d: int, large_frac: float = 0.0) -> np.ndarray:
+    """A ``C x d`` fp16 codebook made only of subnormals and signed zeros
+    (+-k * 2**-24, see ``_signed_subnormal_bits``), for checking that no
+    kernel flushes fp16 subnormal codewords."""
+    return _signed_subnormal_bits(rng, (C, d), large_frac).view(np.float16)
+
+
+def subnormal_x(rng: np.random.Generator, M: int, K: int, large_frac: float = 0.0) -> np.ndarray:
+    """``M x K`` fp16 activations made only of subnormals and signed zeros."""
+    return _signed_subnormal_bits(rng, (M, K), large_frac).view(np.float16)
 
 
 # ---------------------------------------------------------------------------

@@ -151,6 +151,23 @@ def test_matches_scipy_kmeans_on_separated_clusters():
     assert np.all(np.abs(cb.astype(np.float64) - ref_cb) <= ulp)
 
 
+def test_objective_on_a_hand_worked_example():
+    """Three 2-D points, two codewords, worked by hand:
+    p0 = (1, 2)  -> c0 = (0, 0): 1^2 + 2^2     = 5
+    p1 = (3, -1) -> c1 = (1, 1): 2^2 + (-2)^2  = 8
+    p2 = (0.5, 0) -> c0:         0.5^2 + 0^2   = 0.25
+    sum of squared distances = 13.25 (an unsquared sum, 3 + 4 + 0.5 after
+    |.| per coordinate, gives 7.5; Euclidean lengths give sqrt(5) + sqrt(8)
+    + 0.5)."""
+    pts = np.array([[1.0, 2.0], [3.0, -1.0], [0.5, 0.0]], np.float16)
+    cb = np.array([[0.0, 0.0], [1.0, 1.0]], np.float16)
+    u = np.array([0, 1, 0])
+    assert enc.objective(pts, u, cb) == 13.25
+    # the nearest codewords move p0 to c1 ((1-1)^2 + (2-1)^2 = 1): 1 + 8 + 0.25
+    assert np.array_equal(enc.assign(pts, cb), [1, 1, 0])
+    assert enc.objective(pts, enc.assign(pts, cb), cb) == 9.25
+
+
 def test_objective_never_increases():
     rng = np.random.default_rng(4)
     w = pi.draw_weights(rng, 64, 256)

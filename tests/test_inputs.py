@@ -65,3 +65,22 @@ def test_draw_problem_validation():
         pi.draw_problem(rng, 1, 10, 4, 4, 16, 8)      # K % d != 0
     with pytest.raises(ValueError):
         pi.draw_problem(rng, 1, 8, 4, 2, 300, 8)      # C > 2^bits
+
+
+def test_subnormal_generators_draw_only_subnormals_and_signed_zeros():
+    """Every value is +-k * 2**-24 with k in {0, 1, 2, 3} (or 512, 1023 in
+    the wide variant): an fp16 exponent field of zero, both zero signs
+    present."""
+    rng = np.random.default_rng(0)
+    for arr in (pi.subnormal_codebook(rng, 4096, 4), pi.subnormal_x(rng, 3, 4096),
+                pi.subnormal_codebook(rng, 4096, 4, large_frac=0.05)):
+        bits = arr.view(np.uint16)
+        assert arr.dtype == np.float16
+        assert np.all((bits & 0x7C00) == 0)               # exponent field 0: subnormal or zero
+        k = bits & 0x03FF
+        assert set(np.unique(k).tolist()) <= {0, 1, 2, 3, 512, 1023}
+        assert np.any(bits == 0x8000) and np.any(bits == 0x0000)
+        units = arr.astype(np.float64) / pi.FP16_SUBNORMAL_UNIT
+        assert np.array_equal(np.abs(units), k.astype(np.float64))
+    wide = pi.subnormal_codebook(rng, 4096, 4, large_frac=0.05).view(np.uint16) & 0x03FF
+    assert np.any(wide == 1023) and np.any(wide == 512)

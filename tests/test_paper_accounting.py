@@ -37,7 +37,6 @@ def test_index_table_sizes():
 def test_layer_footprint_formula():
     # 4096 x 4096 at SZ=2, K_s=256: ids 8 MiB, per-subspace codebooks 2 MiB
     bits = pa.layer_footprint_bits(256, 2048, 2, 4096)
-    assert bits == 16 * 256 * 4096 + 8 * 2048 * 4096
     assert bits / 8 / MB == pytest.approx(10.0)
 
 
