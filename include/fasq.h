@@ -56,7 +56,7 @@
 extern "C" {
 #endif
 
-#define FASQ_ABI_VERSION 4
+#define FASQ_ABI_VERSION 5
 
 typedef enum {
   FASQ_OK = 0,
@@ -200,6 +200,38 @@ fasq_status fasq_pq_gemv_ex(const void* x, int64_t M, int64_t K, int64_t N,
  * K split of the GEMM fallback), 0 when none is used, -1 for invalid sizes. */
 int64_t fasq_pq_gemv_ex_workspace_bytes(int64_t M, int64_t K, int64_t N, int idx_bits, int d,
                                         int64_t C, int64_t cb_stride);
+
+/*
+ * fasq_pq_gemv_ex for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation).
+ * Same operation, arguments (minus the workspace), layouts and results as
+ * fasq_pq_gemv_ex: the scratch that call would take from a caller workspace
+ * (the per-subspace K split, or the K split of the GEMM fallback) comes from
+ * a static device array the library holds on every GPU it runs on, of
+ * fasq_noalloc_scratch_bytes() = FASQ_NOALLOC_SCRATCH_BYTES bytes, kept until
+ * the process ends.  The call allocates nothing: no hipMalloc, no allocating
+ * library routine.  Its device address is looked up once per device, on the
+ * first call made with that device current.
+ *
+ * Every call on one GPU shares that GPU's array, and the array keeps the last
+ * call's contents: calls that overlap on one GPU (concurrent streams or
+ * threads) race on it and must be serialised by the caller.  Calls on
+ * different GPUs do not interact.
+ *
+ * Returns FASQ_ERR_INVALID_ARG for the checks of fasq_pq_gemv_ex and when
+ * fasq_pq_gemv_ex_workspace_bytes() of these sizes exceeds the array
+ * (fasq_last_error() gives both figures; such calls need fasq_pq_gemv_ex
+ * with a workspace), FASQ_ERR_HIP when the array cannot be located or a
+ * launch fails.
+ */
+#define FASQ_NOALLOC_SCRATCH_BYTES (16 * 1024 * 1024)
+fasq_status fasq_pq_gemv_ex_noalloc(const void* x, int64_t M, int64_t K, int64_t N,
+                                    const void* idx, int idx_bits, int d,
+                                    const void* codebook, int64_t C, int64_t cb_stride,
+                                    void* y, hipStream_t stream);
+
+/* Bytes of the per-device scratch array of fasq_pq_gemv_ex_noalloc. */
+int64_t fasq_noalloc_scratch_bytes(void);
 
 /*
  * Calibration-free PQ encoding of one weight matrix (FASQ Sec. 3.1.1, Alg. 1):

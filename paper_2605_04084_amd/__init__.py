@@ -59,7 +59,7 @@ __all__ = [
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfasq.so")
 
-ABI_VERSION = 4  # FASQ_ABI_VERSION of include/fasq.h
+ABI_VERSION = 5  # FASQ_ABI_VERSION of include/fasq.h
 
 FASQ_OK = 0
 FASQ_ERR_INVALID_ARG = 1
@@ -83,6 +83,8 @@ EXPORTED_SYMBOLS = (
     "fasq_pq_gemm_lut",
     "fasq_pq_gemm_ex",
     "fasq_pq_gemm_ex_workspace_bytes",
+    "fasq_pq_gemv_ex_noalloc",
+    "fasq_noalloc_scratch_bytes",
 )
 
 
@@ -152,6 +154,11 @@ def lib() -> ctypes.CDLL:
         L.fasq_pq_gemm_ex.restype = _c_int
         L.fasq_pq_gemm_ex_workspace_bytes.argtypes = [_c_i64, _c_i64, _c_i64, _c_int, _c_int, _c_i64]
         L.fasq_pq_gemm_ex_workspace_bytes.restype = _c_i64
+        L.fasq_pq_gemv_ex_noalloc.argtypes = [_c_vp, _c_i64, _c_i64, _c_i64, _c_vp, _c_int, _c_int, _c_vp, _c_i64,
+                                              _c_i64, _c_vp, _c_vp]
+        L.fasq_pq_gemv_ex_noalloc.restype = _c_int
+        L.fasq_noalloc_scratch_bytes.argtypes = []
+        L.fasq_noalloc_scratch_bytes.restype = _c_i64
         _lib = L
         return L
 
@@ -406,6 +413,14 @@ def gemv_ex_workspace_bytes(M: int, K: int, N: int, idx_bits: int, d: int, C: in
 def gemv_ex_raw(x, M, K, N, idx, idx_bits, d, codebook, C, cb_stride, y, workspace, workspace_bytes, stream=0) -> int:
     return lib().fasq_pq_gemv_ex(x, M, K, N, idx, idx_bits, d, codebook, C, cb_stride, y, workspace,
                                  workspace_bytes, stream)
+
+
+def gemv_ex_noalloc_raw(x, M, K, N, idx, idx_bits, d, codebook, C, cb_stride, y, stream=0) -> int:
+    return lib().fasq_pq_gemv_ex_noalloc(x, M, K, N, idx, idx_bits, d, codebook, C, cb_stride, y, stream)
+
+
+def noalloc_scratch_bytes() -> int:
+    return lib().fasq_noalloc_scratch_bytes()
 
 
 def pq_gemv_ex(x, idx, idx_bits: int, d: int, codebook, out=None, workspace=None):

@@ -190,6 +190,8 @@ bool plan_record(const char* base, std::initializer_list<int> params) {
   return true;
 }
 
+void set_last_error(const std::string& msg) { t_last_error = msg; }
+
 bool force_generic() {
   const char* v = std::getenv("FASQ_FORCE_PATH");
   return v != nullptr && std::strcmp(v, "generic") == 0;

@@ -6,6 +6,7 @@
 
 #include <atomic>
 #include <initializer_list>
+#include <string>
 
 namespace fasq {
 
@@ -116,6 +117,9 @@ struct Plan {
 Plan& plan();
 // Record `base<params...>` as the planned kernel; returns true when planning.
 bool plan_record(const char* base, std::initializer_list<int> params);
+
+// Sets the calling thread's fasq_last_error() text.
+void set_last_error(const std::string& msg);
 
 // Environment overrides used by tests and ablations: FASQ_FORCE_PATH=generic
 // makes every call take the general kernel.
