@@ -885,24 +885,32 @@ def crossover(torch, fasq, pi, Ms=CROSSOVER_M, steps=5, short=2, long=10):
         cb = torch.from_numpy(p.codebook).to(dev)
         x_all = torch.from_numpy(p.x).to(dev)
         y = torch.empty((max(Ms), p.N), dtype=torch.float16, device=dev)
-        need_max = max(fasq.gemm_ex_workspace_bytes(M, p.K, p.N, p.idx_bits, p.d, p.C) for M in Ms)
+        need_max = max(max(fasq.gemm_ex_workspace_bytes(M, p.K, p.N, p.idx_bits, p.d, p.C),
+                           fasq.gemv_ex_workspace_bytes(M, p.K, p.N, p.idx_bits, p.d, p.C, 0)) for M in Ms)
         ws = torch.empty(max(need_max, 4), dtype=torch.uint8, device=dev)
         torch.cuda.synchronize()
         for M in Ms:
             x = x_all[:M]
             need = fasq.gemm_ex_workspace_bytes(M, p.K, p.N, p.idx_bits, p.d, p.C)
 
+            need_ex = fasq.gemv_ex_workspace_bytes(M, p.K, p.N, p.idx_bits, p.d, p.C, 0)
+            assert need_ex <= ws.numel()
+
             def call(regime, c):
                 if regime == "gemv":
                     st = fasq.gemv_raw(x.data_ptr(), M, p.K, p.N, idxs[c].data_ptr(), p.idx_bits, p.d, cb.data_ptr(),
                                        p.C, y.data_ptr(), stream.cuda_stream)
+                elif regime == "gemv_ex":
+                    st = fasq.gemv_ex_raw(x.data_ptr(), M, p.K, p.N, idxs[c].data_ptr(), p.idx_bits, p.d,
+                                          cb.data_ptr(), p.C, 0, y.data_ptr(), ws.data_ptr(), need_ex,
+                                          stream.cuda_stream)
                 else:
                     st = fasq.gemm_ex_raw(x.data_ptr(), M, p.K, p.N, idxs[c].data_ptr(), p.idx_bits, p.d,
                                           cb.data_ptr(), p.C, y.data_ptr(), ws.data_ptr(), need, stream.cuda_stream)
                 assert st == 0, fasq.last_error()
 
             row = dict(name=spec.name, N=p.N, K=p.K, M=M)
-            for regime in ("gemv", "gemm_ex"):
+            for regime in ("gemv", "gemv_ex", "gemm_ex"):
                 for c in range(copies):
                     call(regime, c)
 
@@ -921,10 +929,12 @@ def crossover(torch, fasq, pi, Ms=CROSSOVER_M, steps=5, short=2, long=10):
             row["gemv_kernel"] = fasq.plan("gemv", M, p.K, p.N, p.idx_bits, p.d, p.C)
             row["gemm_kernel"] = fasq.plan("gemm", M, p.K, p.N, p.idx_bits, p.d, p.C)
             row["gemm_k_split"] = need // (M * p.N * 4) if need else 1
+            row["gemv_ex_kernel"] = row["gemm_kernel"] if need_ex > 0 else row["gemv_kernel"]
             row["faster"] = "gemv" if row["gemv_us"] <= row["gemm_ex_us"] else "gemm_ex"
             out.append(row)
             log(f"[bench] crossover {spec.name:9s} M={M:3d}: fasq_pq_gemv {row['gemv_us']:7.2f} us "
-                f"({row['gemv_kernel']}), GEMM with K split {row['gemm_ex_us']:7.2f} us "
+                f"({row['gemv_kernel']}), fasq_pq_gemv_ex {row['gemv_ex_us']:7.2f} us "
+                f"({row['gemv_ex_kernel']}), GEMM with K split {row['gemm_ex_us']:7.2f} us "
                 f"(split {row['gemm_k_split']})")
         del idxs, cb, x_all, y, ws
         torch.cuda.empty_cache()

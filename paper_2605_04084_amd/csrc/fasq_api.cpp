@@ -45,7 +45,7 @@ bool m1_takes_alone(const Problem& p, const DeviceInfo& dev) {
 
 hipError_t launch_gemv_group(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream) {
   const Problem& p = ps[0];
-  if (p.M < 1 || p.M > 16) return hipErrorNotSupported;
+  if (p.M < 1 || p.M > kGemvMaxTokens) return hipErrorNotSupported;
   if (p.M <= kM1MaxTokens) {  // the row-streaming kernel when its codebook placement allows
     hipError_t e = launch_gemv_m1_group(ps, count, dev, stream);
     if (e != hipErrorNotSupported || p.M == 1) return e;
@@ -135,7 +135,10 @@ fasq_status run(const Problem& p, Regime regime, hipStream_t stream, void* works
   if (e != hipSuccess) return hip_fail("querying the current device", e);
   e = hipErrorNotSupported;
   if (!force_generic()) {
-    if (regime == Regime::kGemv) e = launch_gemv(p, dev, stream);
+    // a decode call with a workspace goes to the GEMM where that is faster
+    const bool to_gemm = regime == Regime::kGemv && workspace != nullptr && decode_prefers_gemm(p, dev) &&
+                         workspace_bytes >= gemm_workspace_bytes(p, dev);
+    if (regime == Regime::kGemv && !to_gemm) e = launch_gemv(p, dev, stream);
     if (e == hipErrorNotSupported) e = launch_gemm_mfma(p, dev, stream, workspace, workspace_bytes);
   }
   if (e == hipErrorNotSupported) e = launch_generic(p, stream);
@@ -308,8 +311,10 @@ int64_t fasq_pq_gemv_ex_workspace_bytes(int64_t M, int64_t K, int64_t N, int idx
   if (fasq::device_info(&dev) != hipSuccess) return -1;
   if (cb_stride != 0) return fasq::gemv_sub_workspace_bytes(p, dev);
   // one shared codebook: a workspace serves the GEMM when the decode kernels
-  // hand it the call (its K split)
-  if (std::strncmp(fasq_pq_plan(0, M, K, N, idx_bits, d, C), "k_gemm_mfma", 11) != 0) return 0;
+  // hand it the call, or when the GEMM with its K split is the faster one
+  if (std::strncmp(fasq_pq_plan(0, M, K, N, idx_bits, d, C), "k_gemm_mfma", 11) != 0 &&
+      !(fasq::decode_prefers_gemm(p, dev) && !fasq::force_generic()))
+    return 0;
   return fasq::gemm_workspace_bytes(p, dev);
 }
 

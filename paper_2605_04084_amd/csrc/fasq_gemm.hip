@@ -182,6 +182,21 @@ bool gemm_plan(const Problem& p, const DeviceInfo& dev, GemmPlan* out) {
   return true;
 }
 
+// Whether a decode call with a workspace runs faster on this GEMM: from 12
+// tokens on, when the decode kernel would have to stage x in slabs (rows of
+// x too long for LDS) and the GEMM splits K with its codebook in LDS.
+// Measured on the Llama-3-8B down_proj shape (4096 x 14336, d = 2, C = 256):
+// 12 tokens 31.3 us on the decode kernel against 26.1 us on the GEMM, 16
+// tokens 38.0 against 25.9 us; with x whole in LDS or registers, or a
+// codebook the GEMM has to gather from global memory (65536 entries), the
+// decode kernel is the faster one.
+bool decode_prefers_gemm(const Problem& p, const DeviceInfo& dev) {
+  if (p.M < kGemmFromTokens || p.M > kGemvMaxTokens || !gemv_x_slabbed(p)) return false;
+  GemmPlan pl;
+  if (!gemm_plan(p, dev, &pl)) return false;
+  return pl.ksplit > 1 && (pl.mode == CB_REPL || pl.mode == CB_LDS);
+}
+
 int64_t gemm_workspace_bytes(const Problem& p, const DeviceInfo& dev) {
   GemmPlan pl;
   if (!gemm_plan(p, dev, &pl) || pl.ksplit == 1) return 0;

@@ -43,7 +43,7 @@ struct GemvPart {
   int64_t N;           // rows of the part
   int64_t ldy;         // elements between the outputs of consecutive tokens
   int C;
-  int nsl;             // CB_SLICE: slices (passes over the rows)
+  int nsl;             // codebook slices; k_gemv takes one (the whole codebook)
 };
 
 constexpr int kGemvMaxParts = 8;  // parts one k_gemv launch can take
@@ -53,17 +53,20 @@ struct GemvArgs {
   int64_t M, K;
   int64_t R;   // bytes per row (= CH * chunk bytes)
   int64_t CH;  // chunks per row
+  int CHS;       // chunks per x slab (a multiple of 4; CH when x is staged whole)
+  int nslab;     // x slabs: ceil(CH / CHS)
   int P;         // waves per row (K split inside the workgroup)
   int TW;        // 16-row tiles per workgroup, a multiple of waves / P
   int cb_bytes;  // LDS bytes of the codebook (x follows)
   int xs;        // LDS bytes between rows of x
   int x_bytes;   // LDS bytes of x (partials follow)
-  int sl_shift;  // CB_SLICE: log2 of the entries per slice
+  int sl_shift;  // CB_SLICE: log2 of the entries of the one LDS slice (at least C)
   int head;      // CB_SPLIT: entries staged in LDS (the rest are read from global memory)
   GemvPart part[kGemvMaxParts];
 };
 
 constexpr int kGemvPipe = 8;      // load units per wave in the software pipeline
+constexpr int kGemvSlabPipe = 4;  // the same with x in slabs
 // Index loads each single-token wave keeps in flight.  Two per wave (32 KB
 // per CU at 16 waves) already saturate a CU's share of HBM; more only make
 // waves wait at the issue of loads that cannot enter the queue, where they
@@ -75,18 +78,28 @@ constexpr int kM1Window = 2;
 constexpr int kM1EarlyLoads = 2;
 static_assert(kM1Window <= kM1EarlyLoads && kM1EarlyLoads <= kGemvPipe, "early loads must cover the window");
 constexpr int kXWordsPerThread = 8;  // first-round x words (16 B) per thread for M > 1
+constexpr int kXSlabBatch = 4;       // x words (16 B) in flight per thread when a later slab is staged
 
-// MASK: some lanes of the last wave of a row see chunk columns past the end
-// of the row (the row is not a whole number of wave spans); their operands
-// are zeroed.
-template <int BITS, int D, int T, int MODE, int MR, bool MASK>
+// MR: token slots (16: one 16-row A tile of x per MFMA).
+// x slabs: when M rows of x are too long for LDS, K is walked in slabs of
+// CHS chunk columns; x is staged one slab at a time and every row's partial
+// sums are carried across the slabs in LDS (added in slab order by the same
+// lane, so the result stays deterministic).
+// MASK: some lanes see chunk columns past the end of their slab or row; their
+// operands are zeroed.  SLAB: x is staged in slabs (always with MASK); the
+// slab loop keeps more state live, so these variants run a shallower
+// pipeline (kGemvSlabPipe loads) to stay within the registers of 16 waves.
+template <int BITS, int D, int T, int MODE, int MR, bool MASK, bool SLAB>
 __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
   constexpr int G = Chunk<BITS>::G;      // ids per chunk
   constexpr int DW = Chunk<BITS>::DW;    // dwords per chunk
   constexpr int CBY = DW * 4;            // chunk bytes
   constexpr int SPC = G * D / 8;         // MFMA steps (8 K values each) per chunk
-  constexpr int L = kGemvPipe;
+  constexpr int XCB = G * D * 2;         // bytes of x per chunk column and token
+  constexpr int L = SLAB ? (T > kGemvSlabPipe ? T : kGemvSlabPipe) : kGemvPipe;
   static_assert(L % T == 0, "pipeline depth must be a multiple of T");
+  static_assert(MR == 16, "16 token slots");
+  static_assert(!SLAB || MASK, "slabs take the column checks");
 
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   uint8_t* xl = smem + a.cb_bytes;
@@ -110,25 +123,34 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
   const int nrt = a.TW / Q;                // row tiles of this wave
   const int nunits = nrt * T;
 
-  // chunk column of (t): raw value, and clamped into the row for loads
+  // chunk column of (t) within the slab: raw, and clamped for loads
   const int CH = (int)a.CH;
   auto ccol_raw = [&](int t) { return (p * T + t) * 4 + g; };
-  auto ccol = [&](int t) { const int c = ccol_raw(t); return c < CH ? c : CH - 1; };
 
-  // Units past the end of this wave's work load the first chunk of the table
-  // (one address for the whole wave: a single request) so that every
-  // iteration issues exactly one load and the waits stay exact.
+  // Units past the end of this wave's work, and rows past N, load the first
+  // chunk of the table (one address for the whole wave: a single request) so
+  // that every iteration issues exactly one load and the waits stay exact.
   // Byte offsets into the index table are 32-bit (the host checks that the
-  // table is below 4 GiB) from one uniform base.  Rows past N load the first
-  // chunk of the table (computed, never stored), as do units past the end.
+  // table is below 4 GiB) from one uniform base.
   auto tile_of = [&](int rt) { return (int64_t)blockIdx.x + (int64_t)(rt * Q + q) * gridDim.x; };
   const uint32_t lane_off0 = (uint32_t)(nl * a.R);
   const uint32_t tile_stride = (uint32_t)(16 * a.R);
   uint32_t buf[L][DW];
+  int c0 = 0, chs = CH;  // the slab: chunk columns [c0, c0 + chs)
+  // byte offset of the lane's chunk in column t of the slab within its row,
+  // or ~0 for columns past the slab (set per slab)
+  uint32_t col_off[T];
+  auto set_cols = [&]() {
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int c = ccol_raw(t);
+      col_off[t] = (!MASK || c < chs) ? (uint32_t)(c0 + c) * CBY : ~0u;
+    }
+  };
   auto load_unit = [&](int slot, int u, int t) {
     const int64_t tile = tile_of(u / T);
-    const bool live = u < nunits && tile * 16 + nl < pt.N;
-    const uint32_t off = (uint32_t)tile * tile_stride + lane_off0 + (uint32_t)ccol(t) * CBY;
+    const bool live = u < nunits && tile * 16 + nl < pt.N && (!MASK || col_off[t] != ~0u);
+    const uint32_t off = (uint32_t)tile * tile_stride + lane_off0 + col_off[t];
     load_chunk<BITS>(pt.idx + (live ? off : 0u), buf[slot]);
   };
 
@@ -137,56 +159,64 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
   // workgroup (the only one on its CU) issue their codebook and x loads,
   // meet at a barrier (which does not wait for memory), and only then issue
   // the first index loads: the codebook and x come back first while the
-  // index stream is already in flight.  CB_SLICE repeats everything from the
-  // codebook staging to the end of the row loop once per slice; x is staged
-  // once.
-  constexpr int XWT = MR == 1 ? 2 : kXWordsPerThread;
-  const int xw_row = (int)(a.K / 8);        // 16-byte words per row of x
-  const int xw_total = xw_row * M;
+  // index stream is already in flight.
   const uint32_t lane_off = repl_lane_off<D>(lane);
-  const int mrow = MR == 1 ? 0 : (nl < M ? nl : M - 1);  // x row this lane feeds to the A operand
-  const uint8_t* xrow = xl + mrow * a.xs;
-  // A operands (x) live in registers when they fit, loaded straight from
-  // global memory with the codebook (x takes no LDS then); else x is staged
-  // in LDS and read at every step.
+  // A operands (x) live in registers when they fit (x staged whole, no
+  // masked columns), loaded straight from global memory with the codebook
+  // (x takes no LDS then); else x is staged in LDS, a slab at a time, and
+  // read at every step.  Rows of A past M repeat a real row.
   constexpr bool kXInRegs = !MASK && T * SPC <= 8;
+  const int mrow = nl < M ? nl : M - 1;  // x row this lane feeds to the A operand
+  const uint8_t* xrow = xl + mrow * a.xs;
   half8_t xreg[kXInRegs ? T * SPC : 1];
-  const int nsl = MODE == CB_SLICE ? pt.nsl : 1;
+  Slice sl;
+  const half_t* scb = pt.cb;
+  int sC = pt.C;
+  if constexpr (MODE == CB_SLICE) {
+    sl.base = 0;
+    sl.mask = (1u << a.sl_shift) - 1u;
+  } else if constexpr (MODE == CB_SPLIT) {
+    sl.mask = (uint32_t)a.head - 1u;
+    sC = a.head;
+  }
+  constexpr bool kStageSlice = MODE == CB_SLICE || MODE == CB_SPLIT;
 
-  for (int si = 0; si < nsl; ++si) {
-    Slice sl;
-    const half_t* scb = pt.cb;
-    int sC = pt.C;
-    if constexpr (MODE == CB_SLICE) {
-      sl.base = (uint32_t)si << a.sl_shift;
-      sl.mask = (1u << a.sl_shift) - 1u;
-      scb = pt.cb + (size_t)sl.base * D;
-      sC = pt.C - (int)sl.base < (1 << a.sl_shift) ? pt.C - (int)sl.base : (1 << a.sl_shift);
-      if (si > 0) __syncthreads();  // every wave is done with the previous slice
-    } else if constexpr (MODE == CB_SPLIT) {
-      sl.mask = (uint32_t)a.head - 1u;
-      sC = a.head;
-    }
-    constexpr bool kStageSlice = MODE == CB_SLICE || MODE == CB_SPLIT;
+  // x words (16 B) of the current slab: token m, slab-local word w of wpr
+  auto x_word_src = [&](int w, int wpr) {
+    const int m = w / wpr;
+    return reinterpret_cast<const u32x4*>(a.x + (int64_t)m * a.K + (int64_t)c0 * (G * D)) + (w - m * wpr);
+  };
+  auto x_word_dst = [&](int w, int wpr) {
+    const int m = w / wpr;
+    return reinterpret_cast<u32x4*>(xl + m * a.xs + (w - m * wpr) * 16);
+  };
+
+
+  const int nslab = SLAB ? a.nslab : 1;
+  chs = CH < a.CHS ? CH : a.CHS;
+  set_cols();
+  {
+    // codebook and the first slab of x (or x in registers)
+    const int wpr = chs * XCB / 16;  // x words per token in this slab
+    const int xw_total = wpr * M;
     CbStage cst;
     if constexpr (kStageSlice) slice_fetch(scb, sC * D * 2 / 16, cst);
     else cb_fetch<D, MODE>(pt.cb, pt.C, cst);
-    u32x4 xst[kXInRegs ? 1 : XWT];
-    if (si == 0) {
-      if constexpr (kXInRegs) {
-        const half_t* xg = a.x + (int64_t)mrow * a.K;
+    u32x4 xst[kXInRegs ? 1 : kXWordsPerThread];
+    if constexpr (kXInRegs) {
+      const half_t* xg = a.x + (int64_t)mrow * a.K;
 #pragma unroll
-        for (int t = 0; t < T; ++t)
+      for (int t = 0; t < T; ++t) {
+        const int c = ccol_raw(t) < CH ? ccol_raw(t) : CH - 1;
 #pragma unroll
-          for (int s = 0; s < SPC; ++s)
-            xreg[t * SPC + s] = *reinterpret_cast<const half8_t*>(xg + ccol(t) * (G * D) + s * 8);
-      } else {
+        for (int s = 0; s < SPC; ++s) xreg[t * SPC + s] = *reinterpret_cast<const half8_t*>(xg + c * (G * D) + s * 8);
+      }
+    } else {
 #pragma unroll
-        for (int k = 0; k < XWT; ++k) {
-          int w = threadIdx.x + k * blockDim.x;
-          w = w < xw_total ? w : xw_total - 1;
-          xst[k] = reinterpret_cast<const u32x4*>(a.x)[w];
-        }
+      for (int k = 0; k < kXWordsPerThread; ++k) {
+        int w = threadIdx.x + k * blockDim.x;
+        w = w < xw_total ? w : xw_total - 1;
+        xst[k] = *x_word_src(w, wpr);
       }
     }
     __syncthreads();
@@ -195,21 +225,46 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
 
     if constexpr (kStageSlice) slice_store(smem, scb, sC * D * 2 / 16, cst);
     else cb_store<D, MODE>(smem, pt.cb, pt.C, cst);
-    if (!kXInRegs && si == 0) {
+    if constexpr (!kXInRegs) {
 #pragma unroll
-      for (int k = 0; k < XWT; ++k) {
+      for (int k = 0; k < kXWordsPerThread; ++k) {
         const int w = threadIdx.x + k * blockDim.x;
-        if (w < xw_total) {
-          const int m = w / xw_row;
-          *reinterpret_cast<u32x4*>(xl + m * a.xs + (w - m * xw_row) * 16) = xst[k];
-        }
+        if (w < xw_total) *x_word_dst(w, wpr) = xst[k];
       }
-      for (int w = threadIdx.x + XWT * blockDim.x; w < xw_total; w += blockDim.x) {
-        const int m = w / xw_row;
-        *reinterpret_cast<u32x4*>(xl + m * a.xs + (w - m * xw_row) * 16) = reinterpret_cast<const u32x4*>(a.x)[w];
-      }
+      for (int w = threadIdx.x + kXWordsPerThread * blockDim.x; w < xw_total; w += blockDim.x)
+        *x_word_dst(w, wpr) = *x_word_src(w, wpr);
     }
     __syncthreads();
+  }
+
+  for (int sb = 0; sb < nslab; ++sb) {
+    if (sb > 0) {
+      // the next slab: every wave is done with the previous slab's x; its
+      // first index loads go out, then x is staged in batches of
+      // kXSlabBatch words per thread
+      c0 = sb * a.CHS;
+      chs = CH - c0 < a.CHS ? CH - c0 : a.CHS;
+      set_cols();
+      const int wpr = chs * XCB / 16;
+      const int xw_total = wpr * M;
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < L - 1; ++i) load_unit(i, i, i % T);
+      for (int base = threadIdx.x; base < xw_total; base += kXSlabBatch * blockDim.x) {
+        u32x4 v[kXSlabBatch];
+#pragma unroll
+        for (int k = 0; k < kXSlabBatch; ++k) {
+          const int w = base + k * blockDim.x;
+          v[k] = *x_word_src(w < xw_total ? w : xw_total - 1, wpr);
+        }
+#pragma unroll
+        for (int k = 0; k < kXSlabBatch; ++k) {
+          const int w = base + k * blockDim.x;
+          if (w < xw_total) *x_word_dst(w, wpr) = v[k];
+        }
+      }
+      __syncthreads();
+    }
 
     float4_t acc0 = {0.f, 0.f, 0.f, 0.f};
     float4_t acc1 = {0.f, 0.f, 0.f, 0.f};
@@ -222,8 +277,9 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
         load_unit((i + L - 1) % L, u + L - 1, (i + L - 1) % T);
         if (u < nunits) {
           const uint32_t* w = buf[i];
-          const uint8_t* xa = xrow + ccol(t) * (G * D * 2);
-          const bool cval = !MASK || ccol_raw(t) < CH;
+          const int c = ccol_raw(t);
+          const bool cval = !MASK || c < chs;
+          const uint8_t* xa = xrow + (cval ? c : 0) * XCB;
 #pragma unroll
           for (int s = 0; s < SPC; ++s) {
             half8_t bop = gather8<BITS, D, MODE>(pt.cb, lane_off, w, s * (8 / D), sl);
@@ -239,14 +295,14 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
           }
           if (t == T - 1) {
             // lane l holds rows m = 4g .. 4g + 3 of column nl of the 16 x 16
-            // tile; slices of a row are summed in slice order by this lane
+            // tile; the slabs of a row are summed in slab order by this lane
             const int lrow = ((u / T) * Q + q) * 16 + nl;
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
               const int m = 4 * g + k;
               if (m < M) {
                 float* r = &red[(lrow * M + m) * P + p];
-                *r = (MODE == CB_SLICE && si > 0) ? *r + (acc0[k] + acc1[k]) : acc0[k] + acc1[k];
+                *r = sb > 0 ? *r + (acc0[k] + acc1[k]) : acc0[k] + acc1[k];
               }
             }
             acc0 = float4_t{0.f, 0.f, 0.f, 0.f};

@@ -68,7 +68,19 @@ inline int choose_part_cuts(const int64_t* units, int count, int64_t ncu, int ma
 
 template <int BITS, int D, int T, int MODE, int MR>
 hipError_t launch_gemv_variant(const GemvArgs& a, bool mask, int threads, dim3 blocks, int lds, hipStream_t stream) {
-  auto kern = mask ? k_gemv<BITS, D, T, MODE, MR, true> : k_gemv<BITS, D, T, MODE, MR, false>;
+  if (a.nslab > 1) {  // x in slabs (T up to 4): the plan name carries a trailing 1
+    if constexpr (T <= 4) {
+      if (plan_record("k_gemv", {BITS, D, T, MODE, MR, 1, 1})) return hipSuccess;
+      auto kern = k_gemv<BITS, D, T, MODE, MR, true, true>;
+      hipError_t e = prepare_kernel(kern);
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL(kern, blocks, dim3(threads), lds, stream, a);
+      return hipGetLastError();
+    } else {
+      return hipErrorNotSupported;
+    }
+  }
+  auto kern = mask ? k_gemv<BITS, D, T, MODE, MR, true, false> : k_gemv<BITS, D, T, MODE, MR, false, false>;
   if (plan_record("k_gemv", {BITS, D, T, MODE, MR, mask ? 1 : 0})) return hipSuccess;
   hipError_t e = prepare_kernel(kern);
   if (e != hipSuccess) return e;
@@ -103,10 +115,43 @@ hipError_t launch_gemv_mode(const GemvArgs& a, int mode, int T, bool mask, int t
   }
 }
 
-// 2 to 16 tokens, one launch over `count` <= kGemvMaxParts matrices that
-// share x, M, K, d and the id width: select T, P, Q, the codebook placement,
-// the parts and the 16-row tiles per workgroup, and launch;
-// hipErrorNotSupported when another kernel has to take the call.
+// x of the 16-row-tile kernel is staged whole when its rows take at most
+// kXWholeBytes of LDS, else in slabs of at most kXSlabBytes.  Both limits
+// depend on M and K alone, never on the codebooks, so a matrix computes in
+// the same order in a grouped launch and alone.
+constexpr int64_t kXWholeBytes = 136 * 1024;
+constexpr int64_t kXSlabBytes = 80 * 1024;
+
+// T chunk columns per lane and wave, P waves per row: the smallest T that
+// covers `cols` chunk columns with at most 16 waves (0: none does).
+inline int gemv_pick_t(int64_t cols) {
+  const int64_t qc = (cols + 3) / 4;  // chunk columns of the four K groups
+  for (int t : {1, 2, 4, 8})
+    if ((qc + t - 1) / t <= 16) return t;
+  return 0;
+}
+
+// Whether x goes to registers (whole rows, no masked columns), else to LDS,
+// whole or in slabs.
+inline bool gemv_x_in_regs(int64_t CH, int G, int d) {
+  const int T = gemv_pick_t(CH);
+  if (T == 0) return false;
+  const int64_t P0 = ((CH + 3) / 4 + T - 1) / T;
+  return P0 * T * 4 == CH && T * (G * d / 8) <= 8;
+}
+
+inline bool gemv_x_slabbed(const Problem& p) {
+  const int G = p.idx_bits == 8 ? 16 : 8;
+  if (p.S % G) return false;
+  const int64_t CH = p.S / G;
+  return !gemv_x_in_regs(CH, G, p.d) && p.M * (CH * G * p.d * 2 + 16) > kXWholeBytes;
+}
+
+// 2 to 16 tokens, one launch over
+// `count` <= kGemvMaxParts matrices that share x, M, K, d and the id width:
+// select the x slabs, T, P, Q, the codebook placement, the parts and the
+// 16-row tiles per workgroup, and launch; hipErrorNotSupported when another
+// kernel has to take the call.
 template <int BITS, int MR>
 hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream) {
   constexpr int G = Chunk<BITS>::G;
@@ -114,7 +159,8 @@ hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev,
   if (count < 1 || count > kGemvMaxParts) return hipErrorNotSupported;
   const Problem& p = ps[0];
   const int d = p.d;
-  if (MR == 1 ? p.M != 1 : (p.M < 2 || p.M > 16)) return hipErrorNotSupported;
+  static_assert(MR == 16, "16 token slots");
+  if (p.M < 2 || p.M > 16) return hipErrorNotSupported;
   if (!(d == 1 || d == 2 || d == 4 || d == 8)) return hipErrorNotSupported;
   if (p.S % G || p.K % 8) return hipErrorNotSupported;
   const int64_t CH = p.S / G;
@@ -133,23 +179,31 @@ hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev,
     tiles_of[i] = (pi.N + 15) / 16;
   }
 
-  const int64_t QC = (CH + 3) / 4;  // chunk columns of the four K groups
-  int T = 0;
-  for (int t : {1, 2, 4, 8}) {
-    if ((QC + t - 1) / t <= 16) { T = t; break; }
+  const int XCB = G * d * 2;  // bytes of x per chunk column and token
+  // x in registers (whole rows, no masked columns) needs no LDS
+  const bool x_in_regs = gemv_x_in_regs(CH, G, d);
+  int64_t CHS = CH;  // chunk columns per x slab
+  if (!x_in_regs && p.M * (CH * XCB + 16) > kXWholeBytes) {
+    // at most 64 chunk columns of each K group per slab (T <= 4)
+    const int64_t cmax = std::min<int64_t>(((kXSlabBytes / p.M - 16) / XCB) / 4 * 4, 256);
+    if (cmax < 4) return hipErrorNotSupported;
+    const int64_t ns = (CH + cmax - 1) / cmax;
+    CHS = ((CH + ns - 1) / ns + 3) / 4 * 4;  // near-equal slabs, whole K groups
   }
+  const int nslab = (int)((CH + CHS - 1) / CHS);
+  const int T = gemv_pick_t(CHS);
   if (T == 0) return hipErrorNotSupported;
-  const int P = (int)((QC + T - 1) / T);
+  const int P = (int)(((CHS + 3) / 4 + T - 1) / T);
   const int Q = 16 / P;
-  const bool mask = (int64_t)P * T * 4 != CH;  // the last wave sees columns past the row end
+  // lanes past the slab's (or the row's) last chunk column; slabbed x is
+  // always read with the column checks (and never from registers)
+  const bool mask = (int64_t)P * T * 4 != CHS || nslab > 1;
   const int threads = P * Q * kWave;
 
   // One codebook placement for the launch: the largest codebook decides it.
   int mode = choose_cb_mode(maxC, d);
   if (mode == CB_REPL && (total_rows + dev.num_cus - 1) / dev.num_cus * p.S < kReplMinIdsPerEntry * maxC) mode = CB_LDS;
-  const int xs = (int)(p.M == 1 ? p.K * 2 : p.K * 2 + 16);
-  // x in registers (loaded from global memory by each lane) needs no LDS
-  const bool x_in_regs = !mask && T * (G * d / 8) <= 8;
+  const int xs = (int)(CHS * XCB + 16);
   const int64_t x_bytes = x_in_regs ? 0 : p.M * (int64_t)xs;
   // The replicated table (up to 64 KB) gives way to one copy when it leaves
   // too little room beside x for one row group's partials.
@@ -216,6 +270,8 @@ hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev,
   a.K = p.K;
   a.R = p.R;
   a.CH = CH;
+  a.CHS = (int)CHS;
+  a.nslab = nslab;
   a.P = P;
   a.TW = (int)tw;
   a.cb_bytes = cb_bytes;
@@ -236,7 +292,7 @@ hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev,
       pt.N = rows;
       pt.ldy = ps[i].N;
       pt.C = (int)ps[i].C;
-      pt.nsl = mode == CB_SLICE ? (int)((ps[i].C + (int64_t(1) << sl_shift) - 1) >> sl_shift) : 1;
+      pt.nsl = 1;
       row += rows;
     }
   }

@@ -37,18 +37,19 @@ hipError_t device_info(DeviceInfo* out);
 hipError_t launch_reconstruct(const Problem& p, void* w, hipStream_t stream);
 hipError_t launch_generic(const Problem& p, hipStream_t stream);
 
-// Tuned decode kernel for M <= 16.  Returns hipErrorNotSupported (without
-// launching) when no tuned variant applies.
+// Tuned decode kernel for M <= kGemvMaxTokens.  Returns hipErrorNotSupported
+// (without launching) when no tuned variant applies.
 hipError_t launch_gemv(const Problem& p, const DeviceInfo& dev, hipStream_t stream);
 
 // Tuned decode kernels over one to kMaxBatchLaunch matrices in one launch,
-// all with the same M <= 16, x, K, d and id width: the row-streaming kernel
+// all with the same M <= kGemvMaxTokens, x, K, d and id width: the row-streaming kernel
 // for M <= kM1MaxTokens where its codebook placement allows, else the
 // 16-row-tile kernel.  hipErrorNotSupported (without launching) when
 // neither applies.
 hipError_t launch_gemv_group(const Problem* ps, int count, const DeviceInfo& dev, hipStream_t stream);
 constexpr int kMaxBatchLaunch = 8;  // matrices per grouped launch
 constexpr int kM1MaxTokens = 2;     // tokens the row-streaming decode kernel takes at once
+constexpr int kGemvMaxTokens = 16;  // tokens the 16-row-tile decode kernel takes at once
 
 // Tuned MFMA prefill kernel.  hipErrorNotSupported when no variant applies.
 // With a workspace of at least gemm_workspace_bytes() a grid too small for
@@ -57,6 +58,13 @@ constexpr int kM1MaxTokens = 2;     // tokens the row-streaming decode kernel ta
 hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t stream, void* workspace = nullptr,
                             int64_t workspace_bytes = 0);
 int64_t gemm_workspace_bytes(const Problem& p, const DeviceInfo& dev);
+
+// Whether the 16-row-tile decode kernel would stage x in slabs for p.
+bool gemv_x_slabbed(const Problem& p);
+// Whether a decode call that has a workspace is faster on the prefill GEMM
+// with its K split (the measured crossover); see fasq_gemm.hip.
+constexpr int kGemmFromTokens = 12;
+bool decode_prefers_gemm(const Problem& p, const DeviceInfo& dev);
 
 // The paper's lookup-table GEMM (Alg. 3), kept for comparison with the MFMA
 // GEMM.  hipErrorNotSupported when its tables do not fit in LDS.

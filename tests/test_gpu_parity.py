@@ -720,3 +720,92 @@ def test_split_codebook_random_against_oracle(case):
     p = pi.draw_problem(rng, M, K, N, d, C, bits)
     y = run("gemv", p)
     assert_close(y, orc.pq_linear(p.x, p.idx, bits, d, p.codebook), f"split codebook {case}")
+
+
+# ---------------------------------------------------------------------------
+# The 16-row-tile decode kernel with x staged in K slabs (rows of x too long
+# for LDS)
+# ---------------------------------------------------------------------------
+
+SLAB_DECODE = [
+    # M, K, N, d, C, bits
+    (8, 14336, 300, 2, 256, 8),        # down_proj rows at 8 tokens
+    (16, 12288, 200, 4, 65536, 16),    # Qwen3-8B down_proj rows at 16 tokens, codebook head in LDS
+    (12, 14336 + 128, 70, 2, 256, 8),  # slabs of unequal length
+    (6, 28672, 90, 2, 256, 8),
+    (16, 14336, 130, 4, 4096, 12),
+    (10, 16384, 64, 1, 256, 8),
+]
+
+
+@pytest.mark.parametrize("case", SLAB_DECODE)
+def test_decode_kernel_x_slabs(case):
+    M, K, N, d, C, bits = case
+    print(f"[case] gemv x slabs {case}", flush=True)
+    assert fasq.plan("gemv", M, K, N, bits, d, C).startswith("k_gemv<"), fasq.plan("gemv", M, K, N, bits, d, C)
+    rng = np.random.default_rng(71 + sum(case))
+    p = pi.draw_problem(rng, M, K, N, d, C, bits)
+    y = run("gemv", p)
+    assert np.isfinite(y).all()
+    assert_close(y, orc.pq_linear(p.x, p.idx, bits, d, p.codebook), f"x slabs {case}")
+
+
+@pytest.mark.parametrize("case", SLAB_DECODE)
+def test_decode_kernel_x_slabs_one_hot_bit_exact(case):
+    """Exact small-integer results: a slab summed twice or skipped shows as
+    an exact mismatch."""
+    M, K, N, d, C, bits = case
+    print(f"[case] gemv x slabs one-hot {case}", flush=True)
+    rng = np.random.default_rng(73 + sum(case))
+    cb = pi.signed_one_hot_codebook(C, d, rng)
+    ids = rng.integers(0, C, size=(N, K // d))
+    x = pi.ternary_x(rng, M, K)
+    idx = pi.pack_indices(ids, bits)
+    ref = orc.pq_linear(x, idx, bits, d, cb)
+    assert np.abs(ref).max() <= 2048
+    y = to_np(fasq.pq_gemv(to_dev(x), to_dev(idx), bits, d, to_dev(cb))).astype(np.float64)
+    assert np.array_equal(y, ref)
+
+
+@pytest.mark.parametrize("M", [8, 12, 16])
+def test_batched_x_slabs(M):
+    """Grouped launches with x in slabs equal single calls bit for bit."""
+    rng = np.random.default_rng(79 + M)
+    K, d, bits = 14336, 2, 8
+    probs = [pi.draw_problem(rng, M, K, N, d, C, bits) for N, C in ((500, 256), (130, 256), (33, 200))]
+    x = probs[0].x
+    got = _batched(x, probs, bits, d)
+    for i, p in enumerate(probs):
+        single = to_np(fasq.pq_gemv(to_dev(x), to_dev(p.idx), bits, d, to_dev(p.codebook)))
+        assert np.array_equal(got[i].view(np.uint16), single.view(np.uint16)), f"matrix {i}"
+        assert_close(got[i].astype(np.float64), orc.pq_linear(x, p.idx, bits, d, p.codebook), f"batched M={M} {i}")
+
+
+@pytest.mark.parametrize("case", [(12, 14336, 300, 2, 256, 8), (16, 14336, 130, 4, 4096, 12)])
+def test_decode_with_workspace_takes_the_gemm_past_the_crossover(case):
+    """From 12 tokens on, a decode call whose x needs slabs goes to the GEMM
+    with its K split when it has a workspace (the measured crossover); it
+    then equals fasq_pq_gemm_ex bit for bit, while fasq_pq_gemv (no
+    workspace) keeps the decode kernel."""
+    M, K, N, d, C, bits = case
+    print(f"[case] crossover dispatch {case}", flush=True)
+    assert fasq.plan("gemv", M, K, N, bits, d, C).startswith("k_gemv<")
+    need = fasq.gemv_ex_workspace_bytes(M, K, N, bits, d, C, 0)
+    assert need > 0 and need == fasq.gemm_ex_workspace_bytes(M, K, N, bits, d, C)
+    rng = np.random.default_rng(83 + sum(case))
+    p = pi.draw_problem(rng, M, K, N, d, C, bits)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda:0")
+    y_ex = to_np(fasq.pq_gemv_ex(to_dev(p.x), to_dev(p.idx), bits, d, to_dev(p.codebook), workspace=ws))
+    y_gemm, _ = _gemm_ex(p.x, p.idx, bits, d, p.codebook)
+    assert np.array_equal(y_ex.view(np.uint16), y_gemm.view(np.uint16))
+    ref = orc.pq_linear(p.x, p.idx, bits, d, p.codebook)
+    assert_close(y_ex.astype(np.float64), ref, f"gemv_ex past the crossover {case}")
+    assert_close(run("gemv", p), ref, f"gemv below the crossover {case}")
+
+
+def test_decode_with_workspace_keeps_the_decode_kernel_elsewhere():
+    # x whole in registers (q_proj rows at 16 tokens), and a codebook the GEMM
+    # would gather from global memory (Qwen3-8B down_proj rows at 16 tokens)
+    assert fasq.gemv_ex_workspace_bytes(16, 4096, 4096, 8, 2, 256, 0) == 0
+    assert fasq.gemv_ex_workspace_bytes(16, 12288, 4096, 16, 4, 65536, 0) == 0
+    assert fasq.gemv_ex_workspace_bytes(8, 14336, 4096, 8, 2, 256, 0) == 0   # below 12 tokens
