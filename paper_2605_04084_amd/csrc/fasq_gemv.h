@@ -361,6 +361,13 @@ struct GemvM1Part {
 
 constexpr int kM1MaxParts = 8;   // parts one row-streaming launch can take
 
+// Products of the row-streaming kernels: packed fp16 dot products on the
+// vector ALU (1), or the diagonal of a 16 x 16 MFMA per token (0).
+#ifndef FASQ_DECODE_DOT
+#define FASQ_DECODE_DOT 1
+#endif
+constexpr bool kDecodeDot = FASQ_DECODE_DOT != 0;
+
 struct GemvM1Args {
   const half_t* x;  // shared by every matrix of the launch
   int64_t K;
@@ -526,9 +533,15 @@ __device__ __forceinline__ void gemv_rows_body(const GemvM1Args& a) {
       }
     }
 
-    float4_t acc0[MT], acc1[MT];
+    // per token: two fp32 partial sums of the lane's products (even and odd
+    // steps), or the two diagonal-MFMA accumulators
+    float dacc0[MT], dacc1[MT];
+    float4_t acc0[kDecodeDot ? 1 : MT], acc1[kDecodeDot ? 1 : MT];
 #pragma unroll
-    for (int m = 0; m < MT; ++m) acc0[m] = acc1[m] = float4_t{0.f, 0.f, 0.f, 0.f};
+    for (int m = 0; m < MT; ++m) {
+      dacc0[m] = dacc1[m] = 0.f;
+      if constexpr (!kDecodeDot) acc0[m] = acc1[m] = float4_t{0.f, 0.f, 0.f, 0.f};
+    }
     auto compute_unit = [&](int slot, int u, int t) {
       const uint32_t* w = buf[slot];
       const bool cval = !MASK || ccol_raw(t) < CH;
@@ -542,16 +555,31 @@ __device__ __forceinline__ void gemv_rows_body(const GemvM1Args& a) {
           if constexpr (kXInRegs) bop = xreg[(m * T + t) * SPC + s];
           else bop = *reinterpret_cast<const half8_t*>(xl + m * xtok + ccol(t) * (G * D * 2) + s * 16);
           if (MASK && !cval) bop = half8_t{};
-          if (s & 1) acc1[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc1[m], 0, 0, 0);
-          else acc0[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc0[m], 0, 0, 0);
+          if constexpr (kDecodeDot) {
+            // eight K values: four packed fp16 products-and-adds into fp32
+            const u32x4 av = __builtin_bit_cast(u32x4, aop), bv = __builtin_bit_cast(u32x4, bop);
+            float& d = (s & 1) ? dacc1[m] : dacc0[m];
+            d = dot2(av[0], bv[0], d);
+            d = dot2(av[1], bv[1], d);
+            d = dot2(av[2], bv[2], d);
+            d = dot2(av[3], bv[3], d);
+          } else {
+            if (s & 1) acc1[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc1[m], 0, 0, 0);
+            else acc0[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, acc0[m], 0, 0, 0);
+          }
         }
       }
       if (t == T - 1) {
 #pragma unroll
         for (int m = 0; m < MT; ++m) {
-          const float4_t acc = acc0[m] + acc1[m];
-          float v = diag_reg == 0 ? acc[0] : diag_reg == 1 ? acc[1] : diag_reg == 2 ? acc[2] : acc[3];
-          v = on_diag ? v : 0.f;
+          float v;
+          if constexpr (kDecodeDot) {
+            v = dacc0[m] + dacc1[m];
+          } else {
+            const float4_t acc = acc0[m] + acc1[m];
+            v = diag_reg == 0 ? acc[0] : diag_reg == 1 ? acc[1] : diag_reg == 2 ? acc[2] : acc[3];
+            v = on_diag ? v : 0.f;
+          }
           v = group_sum<16>(v);
           // the four rows of 16 lanes hold partial sums: combine in a fixed order
           const float sum = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0)) +
@@ -563,8 +591,11 @@ __device__ __forceinline__ void gemv_rows_body(const GemvM1Args& a) {
             float* r = &red[(((u / T) * Q + q) * MT + m) * P + p];
             *r = (MODE == CB_SLICE && si > 0) ? *r + sum : sum;
           }
-          acc0[m] = float4_t{0.f, 0.f, 0.f, 0.f};
-          acc1[m] = float4_t{0.f, 0.f, 0.f, 0.f};
+          dacc0[m] = dacc1[m] = 0.f;
+          if constexpr (!kDecodeDot) {
+            acc0[m] = float4_t{0.f, 0.f, 0.f, 0.f};
+            acc1[m] = float4_t{0.f, 0.f, 0.f, 0.f};
+          }
         }
       }
     };
