@@ -278,6 +278,8 @@ def source_hash():
 
 PMC_REPS = 4
 COUNTERS_PATH = os.path.join(ROOT, "profiles", "counters.json")
+# variant builds (python -m paper_2605_04084_amd._build -D ... --out LIB) by library file name
+VARIANT_DEFINES = {"libfasq_decode_mfma.so": ["FASQ_DECODE_DOT=0"]}
 
 # rocprofv3 --pmc groups, one run each (within the per-block limits: at most
 # 8 SQ, 4 TCC, 4 TCP, 2 GRBM counters per run).
@@ -353,7 +355,8 @@ def pmc_pass(torch, fasq, pi, manifest_path):
         del x, idx, cb, y, ws
     torch.cuda.empty_cache()
     with open(manifest_path, "w") as f:
-        json.dump(dict(source_hash=source_hash(), calibration_bytes=CALIBRATION_BYTES, launches=seq), f, indent=1)
+        json.dump(dict(source_hash=source_hash(), calibration_bytes=CALIBRATION_BYTES, launches=seq,
+                       lib=os.path.relpath(fasq.LIB_PATH, ROOT)), f, indent=1)
     log(f"[bench] pmc pass: {len(seq)} launches x {PMC_REPS}, manifest {manifest_path}")
 
 
@@ -453,8 +456,11 @@ def pmc_report(manifest_path, out_dir, pass_dirs):
             if k in c:
                 der[f"{name}_per_id"] = c[k] / L["ids"]
         L["derived"] = der
-    out = dict(source_hash=man["source_hash"], calibration_factors=factors, reps=PMC_REPS,
-               launches={f"{L['set']}/{L['name']}": L for L in launches})
+    lib = man.get("lib", "paper_2605_04084_amd/libfasq.so")
+    defines = [] if lib == "paper_2605_04084_amd/libfasq.so" else VARIANT_DEFINES.get(os.path.basename(lib), [])
+    groups = [g for g, cs in PMC_GROUPS.items() if any(c in L["counters"] for L in launches for c in cs)]
+    out = dict(source_hash=man["source_hash"], calibration_factors=factors, reps=PMC_REPS, lib=lib,
+               defines=defines, groups=groups, launches={f"{L['set']}/{L['name']}": L for L in launches})
     os.makedirs(out_dir, exist_ok=True)
     with open(os.path.join(out_dir, "counters.json"), "w") as f:
         json.dump(out, f, indent=1)
@@ -492,20 +498,32 @@ PMC_MD_DERIVED = (
 )
 
 
-def pmc_markdown(counters_path, out_dir):
+def pmc_markdown(counters_path, out_dir, variant=None):
+    """One Markdown summary per counter family.  `variant` names a variant
+    build (bench.py --lib) whose counters these are: its summaries go to
+    files tagged with it."""
     with open(counters_path) as f:
         data = json.load(f)
+    groups_run = PMC_GROUPS if variant is None else {g: PMC_GROUPS[g] for g in data.get("groups", PMC_GROUPS)}
+    lib = "" if variant is None else f" --lib {data.get('lib', 'LIB')}"
+    build = "" if variant is None else (f"python3 -m paper_2605_04084_amd._build {' '.join('-D ' + d for d in data.get('defines', []))} "
+                                        f"--out {data.get('lib', 'LIB')}\n")
     groups = "\n".join(f"timeout -s KILL 300 rocprofv3 --pmc {' '.join(cs)} --output-format csv -d gpurun_out/pmc_{g} "
-                       f"-o run -- \\\n    python3 bench.py --pmc-pass gpurun_out/pmc_manifest.json"
-                       for g, cs in PMC_GROUPS.items())
+                       f"-o run -- \\\n    python3 bench.py{lib} --pmc-pass gpurun_out/pmc_manifest.json"
+                       for g, cs in groups_run.items())
+    groups = build + groups
     report = ("python3 bench.py --pmc-report gpurun_out/pmc_manifest.json gpurun_out/counters " +
-              " ".join(f"gpurun_out/pmc_{g}" for g in PMC_GROUPS) +
-              f"\npython3 bench.py --pmc-markdown gpurun_out/counters/counters.json profiles")
+              " ".join(f"gpurun_out/pmc_{g}" for g in groups_run) +
+              f"\npython3 bench.py --pmc-markdown gpurun_out/counters/counters.json profiles" +
+              ("" if variant is None else f" {variant}"))
     fac = data.get("calibration_factors", {})
     for fname, sets, title in PMC_MD_FILES:
         rows = [(k, e) for k, e in data["launches"].items() if e["set"] in sets]
         if not rows:
             continue
+        if variant is not None:
+            fname = fname.replace("_counters.md", f"_{variant}_counters.md")
+            title = f"{title}, variant build {variant} ({', '.join(data.get('defines', []))})"
         lines = [f"# {title}: rocprofv3 counters", "",
                  "Commands (from the repository root on one MI355X; one `rocprofv3 --pmc` run per counter group, "
                  "each over the same fixed launch sequence):", "", "```", "export TMPDIR=/tmp", groups, report, "```",
@@ -609,6 +627,11 @@ def trace_markdown(trace_dir, bench_json, out_path):
         for j, m in enumerate(tab):
             lines.append(f"| {m['name']} | {'+'.join(str(n) for n in m['N'])} × {m['K']} | "
                          f"{np.median(D[:, j]):.2f} | {m['us_median']:.2f} |")
+        dj = [j for j, m in enumerate(tab) if m["kernel"] == dom]
+        if dj:
+            lines += ["", f"The dominant kernel over its launches in this layer ({', '.join(tab[j]['name'] for j in dj)}): "
+                      f"rocprofv3 {np.mean([np.median(D[:, j]) for j in dj]):.3f} µs per launch (mean of the "
+                      f"per-launch medians) against bench.py's {rl['us_per_launch']:.3f} µs."]
         # gaps between consecutive kernels inside the timed graph replays
         starts = np.array([int(r["Start_Timestamp"]) for r in g[:nlay * nl]], dtype=np.float64)
         ends = np.array([int(r["End_Timestamp"]) for r in g[:nlay * nl]], dtype=np.float64)
@@ -1126,9 +1149,11 @@ def cpu_baseline(pi, frac=1.0):
                        f"{blas} BLAS threads; {len(os.sched_getaffinity(0))} cores in the affinity mask")
 
 
-# L2 (TCC) request rate of MI355X: 8 XCDs x 16 channels, one 128-byte tag
-# lookup per channel and clock, at the 2.4 GHz peak engine clock.
-L2_REQ_PER_S = 8 * 16 * 2.4e9
+# L2 (TCC) requests per second that random 8-byte gathers from a 512 KB
+# table (L2-resident) reach on MI355X: 278 G gathers/s measured at 0.94
+# TCC_REQ per gather.  (8 XCDs x 16 channels x one tag lookup per clock would
+# be 307 G/s at 2.4 GHz; the measured rate corresponds to about 2.04 GHz.)
+L2_REQ_PER_S = 261e9
 
 
 def qwen_l2_summary(counters, M, res):
@@ -1147,7 +1172,7 @@ def qwen_l2_summary(counters, M, res):
         hits += c.get("TCC_HIT_sum", 0.0)
         misses += c.get("TCC_MISS_sum", 0.0)
     return dict(requests_per_layer=reqs, l2_hit_pct=100.0 * hits / max(hits + misses, 1.0),
-                request_floor_us=reqs / L2_REQ_PER_S * 1e6, request_rate_assumed_per_s=L2_REQ_PER_S,
+                request_floor_us=reqs / L2_REQ_PER_S * 1e6, request_rate_measured_per_s=L2_REQ_PER_S,
                 source="profiles/counters.json (rocprofv3 --pmc TCC_REQ_sum, TCC_HIT_sum, TCC_MISS_sum)")
 
 
@@ -1174,6 +1199,8 @@ def main():
     ap.add_argument("--sensitivity", action="store_true",
                     help="add the codebook-size, sub-vector, batch and prefill-length sweeps on one 4096x4096 layer")
     ap.add_argument("--out", default=None, help="also write the JSON record to this file")
+    ap.add_argument("--lib", default=None,
+                    help="load this libfasq.so instead of the in-tree one (a variant build, for A/B runs)")
     ap.add_argument("--pmc-pass", metavar="MANIFEST", default=None,
                     help="run the short launch sequence for a rocprofv3 --pmc pass and write its manifest")
     ap.add_argument("--pmc-groups", action="store_true",
@@ -1182,8 +1209,8 @@ def main():
                     help="MANIFEST OUT_DIR PASS_DIR...: turn --pmc passes into counters.json")
     ap.add_argument("--trace-markdown", nargs=3, metavar=("TRACE_DIR", "BENCH_JSON", "OUT_MD"), default=None,
                     help="write the kernel-statistics summary of a rocprofv3 --kernel-trace --stats run")
-    ap.add_argument("--pmc-markdown", nargs=2, metavar=("COUNTERS_JSON", "OUT_DIR"), default=None,
-                    help="write the Markdown counter summaries of a counters.json")
+    ap.add_argument("--pmc-markdown", nargs="+", metavar="ARG", default=None,
+                    help="COUNTERS_JSON OUT_DIR [VARIANT]: write the Markdown counter summaries of a counters.json")
     args = ap.parse_args()
 
     if args.pmc_groups:
@@ -1194,6 +1221,8 @@ def main():
         trace_markdown(*args.trace_markdown)
         return
     if args.pmc_markdown:
+        if len(args.pmc_markdown) not in (2, 3):
+            ap.error("--pmc-markdown needs COUNTERS_JSON OUT_DIR [VARIANT]")
         pmc_markdown(*args.pmc_markdown)
         return
     if args.pmc_report:
@@ -1212,7 +1241,9 @@ def main():
     import paper_2605_04084_amd as fasq
     import pq_inputs as pi
 
-    if not os.path.exists(fasq.LIB_PATH):
+    if args.lib:
+        fasq.LIB_PATH = os.path.abspath(args.lib)
+    elif not os.path.exists(fasq.LIB_PATH):
         import __graft_entry__
 
         __graft_entry__.build()

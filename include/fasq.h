@@ -185,9 +185,11 @@ fasq_status fasq_pq_gemm_lut(const void* x, int64_t M, int64_t K, int64_t N,
  * books and M = 1 the tuned kernel splits K over workgroups whose books fit
  * in LDS and adds the partials in a fixed order (deterministic); other shapes,
  * or a workspace that is too small, take the general kernel.  With one shared
- * codebook the call is fasq_pq_gemv, except that when the decode kernels hand
- * it to the prefill GEMM (M > 16, or rows of x too long for LDS) the GEMM may
- * split K with the workspace as fasq_pq_gemm_ex does.
+ * codebook the call is fasq_pq_gemv, except that the workspace lets the
+ * prefill GEMM split K as fasq_pq_gemm_ex does where the GEMM takes the call:
+ * beyond 16 tokens, where no decode kernel applies, and, from 12 tokens on,
+ * where the decode kernel would stage x in slabs and the GEMM keeps its
+ * codebook in LDS (the measured crossover of Sec. 4.4's batch-size trade-off).
  */
 fasq_status fasq_pq_gemv_ex(const void* x, int64_t M, int64_t K, int64_t N,
                             const void* idx, int idx_bits, int d,

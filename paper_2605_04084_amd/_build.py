@@ -13,7 +13,7 @@ import os
 import shutil
 import subprocess
 import sys
-from typing import List, Optional
+from typing import List, Optional, Sequence
 
 PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 REPO_DIR = os.path.dirname(PKG_DIR)
@@ -46,9 +46,9 @@ def sources() -> List[str]:
     return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith((".hip", ".cpp")))
 
 
-def _compile(src: str, verbose: bool) -> str:
-    obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    cmd = [hipcc(), *COMMON_FLAGS, "-c", src, "-o", obj]
+def _compile(src: str, verbose: bool, build_dir: str = BUILD_DIR, defines: Sequence[str] = ()) -> str:
+    obj = os.path.join(build_dir, os.path.basename(src) + ".o")
+    cmd = [hipcc(), *COMMON_FLAGS, *(f"-D{d}" for d in defines), "-c", src, "-o", obj]
     if src.endswith(".cpp"):
         cmd[1:1] = ["-x", "hip"]
     if verbose:
@@ -62,23 +62,41 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
-def build(verbose: bool = False, jobs: Optional[int] = None) -> str:
-    """Compile every source and link ``libfasq.so``; returns the library path."""
-    os.makedirs(BUILD_DIR, exist_ok=True)
+def build(verbose: bool = False, jobs: Optional[int] = None, defines: Sequence[str] = (),
+          lib_path: str = LIB_PATH) -> str:
+    """Compile every source and link ``libfasq.so``; returns the library path.
+
+    ``defines`` (``NAME=VALUE`` strings) select compile-time variants, for
+    example ``FASQ_DECODE_DOT=0`` (the one- and two-token decode kernels on
+    the diagonal MFMA); such builds go to ``lib_path`` with their objects in
+    a build directory of their own."""
+    build_dir = BUILD_DIR if not defines else os.path.join(BUILD_DIR, "variant_" + "_".join(defines).replace("=", "-"))
+    os.makedirs(build_dir, exist_ok=True)
+    os.makedirs(os.path.dirname(os.path.abspath(lib_path)), exist_ok=True)
     srcs = sources()
     jobs = jobs or min(len(srcs), max(1, min(16, os.cpu_count() or 1)))
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), srcs))
-    tmp = LIB_PATH + ".tmp"
+        objs = list(ex.map(lambda s: _compile(s, verbose, build_dir, defines), srcs))
+    tmp = lib_path + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"linking libfasq.so failed:\n{r.stderr}")
-    os.replace(tmp, LIB_PATH)
-    return LIB_PATH
+    os.replace(tmp, lib_path)
+    return lib_path
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    import argparse
+
+    ap = argparse.ArgumentParser(description="build libfasq.so for gfx950")
+    ap.add_argument("-v", "--verbose", action="store_true")
+    ap.add_argument("-D", dest="defines", action="append", default=[], metavar="NAME=VALUE",
+                    help="compile-time variant (needs --out)")
+    ap.add_argument("--out", default=LIB_PATH, help="library path (default: the in-tree libfasq.so)")
+    a = ap.parse_args()
+    if a.defines and os.path.abspath(a.out) == os.path.abspath(LIB_PATH):
+        ap.error("a variant build needs --out: the in-tree library is the default build")
+    print(build(verbose=a.verbose, defines=a.defines, lib_path=a.out))
