@@ -16,7 +16,11 @@ namespace fasq {
 //              an id contributes only in the pass of its own slice.
 //   CB_SPLIT : the first entries in LDS, as many as fit, the rest gathered
 //              from global memory (codebooks larger than LDS, one pass).
-enum CbMode { CB_REPL = 0, CB_LDS = 1, CB_GLOBAL = 2, CB_SLICE = 3, CB_SPLIT = 4 };
+//   CB_HALF  : LDS, each entry replicated over a 128-byte row (half of
+//              CB_REPL's), for a tile whose ring leaves no room for the full
+//              table: with 8-byte codewords two lanes of an LDS cycle share
+//              each copy, so a gather costs at most two cycles.
+enum CbMode { CB_REPL = 0, CB_LDS = 1, CB_GLOBAL = 2, CB_SLICE = 3, CB_SPLIT = 4, CB_HALF = 5 };
 
 // One lane's unit of the packed index stream.
 template <int BITS>
@@ -75,10 +79,20 @@ struct Repl {
   static constexpr int WPE = COPIES * ESZ / 16;  // 16-byte words staged per row
 };
 
+// The half-row layout (CB_HALF): entry e owns the 128-byte row at e << 7,
+// filled with 128 / ESZ copies; lane l reads copy l % HCOPIES.
+template <int D>
+struct ReplHalf {
+  static constexpr int ESZ = Repl<D>::ESZ;
+  static constexpr int STRIDE = 128;
+  static constexpr int COPIES = STRIDE / ESZ;
+  static constexpr int WPE = STRIDE / 16;
+};
+
 // LDS bytes a codebook of C entries takes in a given placement.
 // (CB_SLICE: the slice size is chosen by the launcher, not given by C.)
 __host__ __device__ constexpr int64_t cb_lds_bytes(int mode, int64_t C, int d) {
-  return mode == CB_REPL ? C * 256 : mode == CB_LDS ? C * d * 2 : 0;
+  return mode == CB_REPL ? C * 256 : mode == CB_HALF ? C * 128 : mode == CB_LDS ? C * d * 2 : 0;
 }
 
 // ---------------------------------------------------------------------------
@@ -89,6 +103,7 @@ __host__ __device__ constexpr int64_t cb_lds_bytes(int mode, int64_t C, int d) {
 //   CB_REPL: word w holds copies of entry e = w / WPE and is stored at
 //            (e << 8) + 16 (w % WPE); the thread loads the entry itself (the
 //            loads of one wave touch one or two cache lines).
+//   CB_HALF: as CB_REPL with 128-byte rows: (e << 7) + 16 (w % 8).
 // The fetch phase issues the global loads and the store phase writes LDS, so
 // that a kernel can issue its index-stream loads in between without waiting
 // on them here.
@@ -108,12 +123,14 @@ struct CbStage {
 
 template <int D, int MODE>
 __device__ __forceinline__ int cb_words(int C) {
-  return MODE == CB_REPL ? C * Repl<D>::WPE : C * D * 2 / 16;
+  return MODE == CB_REPL ? C * Repl<D>::WPE : MODE == CB_HALF ? C * ReplHalf<D>::WPE : C * D * 2 / 16;
 }
 
 template <int D, int MODE>
 __device__ __forceinline__ uint32_t cb_word_addr(int w) {
   if constexpr (MODE == CB_REPL) return ((uint32_t)(w / Repl<D>::WPE) << 8) + (uint32_t)(w % Repl<D>::WPE) * 16;
+  else if constexpr (MODE == CB_HALF)
+    return ((uint32_t)(w / ReplHalf<D>::WPE) << 7) + (uint32_t)(w % ReplHalf<D>::WPE) * 16;
   else return (uint32_t)w * 16;
 }
 
@@ -122,7 +139,7 @@ __device__ __forceinline__ u32x4 cb_word(const half_t* __restrict__ cb, int w) {
   if constexpr (MODE == CB_LDS) {
     return reinterpret_cast<const u32x4*>(cb)[w];
   } else {
-    const int e = w / Repl<D>::WPE;
+    const int e = w / (MODE == CB_HALF ? ReplHalf<D>::WPE : Repl<D>::WPE);
     if constexpr (D == 1) {
       const uint32_t h = reinterpret_cast<const uint16_t*>(cb)[e];
       return u32x4{h, h, h, h};
@@ -277,6 +294,8 @@ __device__ __forceinline__ void gather(const half_t* __restrict__ gcb, uint32_t 
                                        uint32_t* out, Slice sl = Slice()) {
   if constexpr (MODE == CB_REPL) {
     read_codeword_lds<D>((u << 8) | lane_off, out);
+  } else if constexpr (MODE == CB_HALF) {
+    read_codeword_lds<D>((u << 7) | lane_off, out);
   } else if constexpr (MODE == CB_LDS) {
     read_codeword_lds<D>(u * (2 * D), out);
   } else if constexpr (MODE == CB_SLICE) {
@@ -295,6 +314,13 @@ __device__ __forceinline__ void gather(const half_t* __restrict__ gcb, uint32_t 
 template <int D>
 __device__ __forceinline__ uint32_t repl_lane_off(int lane) {
   return (uint32_t)(lane % Repl<D>::COPIES) * Repl<D>::ESZ;
+}
+
+// The lane's copy offset in the placement MODE (0 for a single copy).
+template <int D, int MODE>
+__device__ __forceinline__ uint32_t cb_lane_off(int lane) {
+  if constexpr (MODE == CB_HALF) return (uint32_t)(lane % ReplHalf<D>::COPIES) * ReplHalf<D>::ESZ;
+  else return repl_lane_off<D>(lane);
 }
 
 // Gather the codeword of id i of chunk w[].  For 8-bit ids in the replicated

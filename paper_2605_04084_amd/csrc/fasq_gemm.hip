@@ -24,13 +24,21 @@ hipError_t launch_gemm_variant(const GemmArgs& a, int lds, hipStream_t stream) {
 // takes the largest tile whose grid covers at least 3/4 of the CUs, else the
 // smallest.  A 128 x 64 wave tile reads 0.75 KB of LDS operands per MFMA
 // against 1 KB for 64 x 64, which lifts the LDS-bound MFMA loop; its ring
-// leaves no room for the replicated codebook, so it gathers from one copy.
+// leaves no room for the replicated codebook, so it gathers from the
+// half-row table (CB_HALF) where that fits, else from one copy.
 // The 64-row tiles (small grids) also split K over KG groups of waves inside
 // the workgroup, with a shallower ring per group.
 struct GemmTileShape {
   int bm, bn, ns;
 };
-constexpr GemmTileShape kGemmTiles[] = {{256, 256, 3}, {128, 256, 4}, {128, 128, 4}, {64, 128, 8}, {64, 64, 8}};
+#ifndef FASQ_GEMM_BIG_NS
+#define FASQ_GEMM_BIG_NS 3
+#endif
+#ifndef FASQ_GEMM_HALF
+#define FASQ_GEMM_HALF 1
+#endif
+constexpr GemmTileShape kGemmTiles[] = {
+    {256, 256, FASQ_GEMM_BIG_NS}, {128, 256, 4}, {128, 128, 4}, {64, 128, 8}, {64, 64, 8}};
 constexpr int kGemmNumTiles = 5;
 // K groups tried for the 64-row tiles, in order.  Two groups (two waves per
 // SIMD) with the replicated codebook measured best; four groups only fit
@@ -84,6 +92,10 @@ hipError_t launch_gemm_mode(const GemmArgs& a, int mode, int tile, int kg, int l
   switch (mode) {
     case CB_REPL: return launch_gemm_tile<BITS, D, CB_REPL>(a, tile, kg, lds, stream);
     case CB_LDS: return launch_gemm_tile<BITS, D, CB_LDS>(a, tile, kg, lds, stream);
+    case CB_HALF:  // the 256 x 256 tile only
+      if constexpr (gemm_big_tile_fits(BITS, D))
+        return launch_gemm_variant<BITS, D, CB_HALF, 256, 256, 2, 4, kGemmTiles[0].ns, 1>(a, lds, stream);
+      else return hipErrorNotSupported;
     default: return launch_gemm_tile<BITS, D, CB_GLOBAL>(a, tile, kg, lds, stream);
   }
 }
@@ -140,10 +152,13 @@ bool gemm_plan(const Problem& p, const DeviceInfo& dev, GemmPlan* out) {
   auto tiles_of = [&](int t) {
     return ((p.M + kGemmTiles[t].bm - 1) / kGemmTiles[t].bm) * ((p.N + kGemmTiles[t].bn - 1) / kGemmTiles[t].bn);
   };
-  // The codebook placement of tile t: the call's, or one LDS copy when only
-  // that fits beside the tile's ring (-1: neither fits).
+  // The codebook placement of tile t: the call's; else, for the replicated
+  // table, the half-row table (256 x 256 tile) or one LDS copy, whichever
+  // fits beside the tile's ring first (-1: none fits).
   auto mode_of = [&](int t) {
     if (lds_of(t, 1, mode) <= dev.lds_per_block) return mode;
+    if (FASQ_GEMM_HALF && mode == CB_REPL && t == 0 && lds_of(t, 1, CB_HALF) <= dev.lds_per_block)
+      return (int)CB_HALF;
     if (mode == CB_REPL && lds_of(t, 1, CB_LDS) <= dev.lds_per_block) return (int)CB_LDS;
     return -1;
   };
@@ -194,7 +209,7 @@ bool decode_prefers_gemm(const Problem& p, const DeviceInfo& dev) {
   if (p.M < kGemmFromTokens || p.M > kGemvMaxTokens || !gemv_x_slabbed(p)) return false;
   GemmPlan pl;
   if (!gemm_plan(p, dev, &pl)) return false;
-  return pl.ksplit > 1 && (pl.mode == CB_REPL || pl.mode == CB_LDS);
+  return pl.ksplit > 1 && (pl.mode == CB_REPL || pl.mode == CB_HALF || pl.mode == CB_LDS);
 }
 
 int64_t gemm_workspace_bytes(const Problem& p, const DeviceInfo& dev) {

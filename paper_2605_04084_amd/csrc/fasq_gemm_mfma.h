@@ -170,7 +170,7 @@ __global__ __launch_bounds__(WGM * WGN * KG * 64) void k_gemm_mfma(GemmArgs a) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[fm][fn][i] = 0.f;
 
-  const uint32_t lane_off = repl_lane_off<D>(lane);
+  const uint32_t lane_off = cb_lane_off<D, MODE>(lane);
 
   // Operands of one k-step: FM A fragments from the X tile, FN B fragments
   // gathered from the codebook.

@@ -151,14 +151,17 @@ WIDE_TILE = [
     (1030, 384, 16400, 4, 4096, 12),
     (1100, 256, 16500, 4, 65536, 16),
     (1025, 128, 16390, 8, 256, 8),
-    (1030, 320, 16400, 4, 256, 8),      # the 256 x 256 tile (one codebook copy)
+    (1030, 320, 16400, 4, 256, 8),      # the 256 x 256 tile (half-row codebook, 16 copies)
 ]
 
 
 def test_gemm_tile_choice():
-    """Enough 256 x 256 tiles to fill the CUs: the big tile with one codebook
-    copy; fewer: 128 x 256 with the replicated codebook."""
-    assert fasq.plan("gemm", 2048, 4096, 14336, 8, 4, 256).startswith("k_gemm_mfma<8, 4, 1, 256, 256, 2, 4, ")
+    """Enough 256 x 256 tiles to fill the CUs: the big tile with the half-row
+    codebook (one copy for 4096 entries); fewer: 128 x 256 with the
+    replicated codebook."""
+    assert fasq.plan("gemm", 2048, 4096, 14336, 8, 4, 256).startswith("k_gemm_mfma<8, 4, 5, 256, 256, 2, 4, ")
+    assert fasq.plan("gemm", 2048, 4096, 14336, 8, 8, 256).startswith("k_gemm_mfma<8, 8, 5, 256, 256, 2, 4, ")
+    assert fasq.plan("gemm", 2048, 4096, 14336, 12, 4, 4096).startswith("k_gemm_mfma<12, 4, 1, 256, 256, 2, 4, ")
     assert fasq.plan("gemm", 2048, 4096, 4096, 8, 4, 256).startswith("k_gemm_mfma<8, 4, 0, 128, 256, 2, 4, ")
     assert fasq.plan("gemm", 512, 4096, 14336, 8, 4, 256).startswith("k_gemm_mfma<8, 4, 0, 128, 256, 2, 4, ")
     # sub-vectors of 1 or 2, or 16-bit ids, would spill in the big tile

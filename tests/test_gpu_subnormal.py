@@ -128,7 +128,8 @@ def test_gemv_paths(path, kind):
 
 # fasq_pq_gemm tiles: (rows, columns) of the output tile, (M, K, N, d, C, bits)
 GEMM_PATHS = [
-    ((256, 256), (777, 448, 12345, 4, 256, 8)),
+    ((256, 256), (777, 448, 12345, 4, 256, 8)),   # half-row codebook
+    ((256, 256), (600, 256, 16400, 4, 4096, 12)),  # one codebook copy
     ((128, 256), (1030, 256, 16400, 2, 256, 8)),
     ((128, 128), (1000, 256, 3000, 4, 256, 8)),
     ((64, 128), (500, 256, 3000, 4, 256, 8)),
