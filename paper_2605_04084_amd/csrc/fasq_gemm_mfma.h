@@ -20,7 +20,7 @@
 //     (allowed: the contraction is a sum over K), so that lane half h reads
 //     one contiguous run of 32/d ids per chunk.
 //   * Software pipeline: each wave reads the A and B operands of k-step
-//     t + 2 from LDS while the matrix cores work on step t.
+//     t + 1 from LDS while the matrix cores work on step t.
 //   * Synchronisation: one workgroup barrier per chunk, in the middle of it
 //     (after an explicit wait for this wave's copies of the next chunk):
 //     every wave's copies of the next chunk are in, and every wave is done
@@ -78,6 +78,11 @@ template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt out of range");
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// s_waitcnt with only the LDS/scalar counter constrained, to zero.
+__device__ __forceinline__ void wait_lgkmcnt0() {
+  __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (0x7 << 4) | (0 << 8));
 }
 
 // KG > 1 splits K inside the workgroup: KG groups of WGM x WGN waves, each
@@ -198,46 +203,69 @@ __global__ __launch_bounds__(WGM * WGN * KG * 64) void k_gemm_mfma(GemmArgs a) {
       o.a[fm] = *reinterpret_cast<const half8_t*>(xb + r * 128 + slot * 16);
     }
   };
+  // Four-wave tiles (one wave per SIMD, or two K groups) pin the order: the
+  // reads of the next step stay ahead of this step's MFMAs (scheduling
+  // barriers on both sides), and each step starts with an explicit wait for
+  // the reads of the step before.  Two steps of reads (16 with d = 4) are
+  // more than the LDS counter can name, so the compiler's own wait, placed
+  // after the next step's reads, would wait for those as well.  The
+  // eight-wave tiles measured faster with the compiler's interleaving (the
+  // other wave of the SIMD covers the waits).
+  constexpr bool kPinSteps = WAVES == 4;
+  auto step_reads = [&](Ops& o, int stage, const uint32_t (&ids)[FN][HB / 4], int t) {
+    if constexpr (kPinSteps) {
+      __builtin_amdgcn_sched_barrier(0);
+      wait_lgkmcnt0();
+    }
+    read_ops(o, stage, ids, t);
+  };
   auto mfma_step = [&](const Ops& o, bool valid) {
+    if constexpr (kPinSteps) __builtin_amdgcn_sched_barrier(0);
     if (KG > 1 && !valid) return;  // a group's last chunk past K
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
       for (int fn = 0; fn < FN; ++fn)
         acc[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x16_f16(o.a[fm], o.b[fn], acc[fm][fn], 0, 0, 0);
+    if constexpr (kPinSteps) __builtin_amdgcn_sched_barrier(0);
   };
 
-  // Software pipeline: the operands of k-step t + 2 are read while the
-  // matrix cores work on step t, across chunk boundaries too (step t's
-  // operands live in o[t % 4]).  The workgroup barrier sits in the middle
-  // of a chunk: at chunk c's third step every wave has finished chunk c - 1
+  // Software pipeline: the operands of k-step t + 1 are read while the
+  // matrix cores work on step t, across chunk boundaries too.  One step
+  // ahead keeps at most one step's LDS reads (plus the next ids) in flight,
+  // few enough for the 4-bit LDS counter, so each wait names exactly the
+  // reads it needs.  The control flow is the same in every chunk (the last
+  // one reads and copies a clamped chunk it does not use), so no join point
+  // makes the compiler wait for every read in flight.  The workgroup barrier
+  // sits after the chunk's first step: every wave has finished chunk c - 1
   // (its stage can be refilled) and, after waiting for its own copies,
   // chunk c + 1 is in LDS (its ids and first operands can be read).
   wait_vmcnt<LPC * (NS - 2)>();  // this wave's copies of chunk 0
   __builtin_amdgcn_s_barrier();  // everyone's
-  uint32_t idc[FN][HB / 4];
+  uint32_t idc[FN][HB / 4], idn[FN][HB / 4];
   read_ids(0, idc);
-  Ops o0, o1, o2, o3;
-  read_ops(o0, 0, idc, 0);
-  read_ops(o1, 0, idc, 1);
+  Ops oa, ob;
+  read_ops(oa, 0, idc, 0);
   for (int c = 0; c < niter; ++c) {
     const int stage = c % NS;
-    const bool more = c + 1 < niter;
+    const int nstage = (c + 1) % NS;
     const bool valid = c * KG + kg < nchunks;
-    read_ops(o2, stage, idc, 2);
-    mfma_step(o0, valid);
-    read_ops(o3, stage, idc, 3);
-    mfma_step(o1, valid);
-    if (more) {
-      wait_vmcnt<LPC * (NS - 3)>();  // this wave's copies of chunk c + 1
-      __builtin_amdgcn_s_barrier();  // everyone's; nobody reads chunk c - 1 any more
-      issue(chunk_of(c + NS - 1 < niter ? c + NS - 1 : niter - 1), (c + NS - 1) % NS);
-      read_ids((c + 1) % NS, idc);
-      read_ops(o0, (c + 1) % NS, idc, 0);
-    }
-    mfma_step(o2, valid);
-    if (more) read_ops(o1, (c + 1) % NS, idc, 1);
-    mfma_step(o3, valid);
+    step_reads(ob, stage, idc, 1);
+    mfma_step(oa, valid);
+    wait_vmcnt<LPC * (NS - 3)>();  // this wave's copies of chunk c + 1
+    __builtin_amdgcn_s_barrier();  // everyone's; nobody reads chunk c - 1 any more
+    issue(chunk_of(c + NS - 1 < niter ? c + NS - 1 : niter - 1), (c + NS - 1) % NS);
+    read_ids(nstage, idn);
+    step_reads(oa, stage, idc, 2);
+    mfma_step(ob, valid);
+    step_reads(ob, stage, idc, 3);
+    mfma_step(oa, valid);
+    step_reads(oa, nstage, idn, 0);
+    mfma_step(ob, valid);
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn)
+#pragma unroll
+      for (int w = 0; w < HB / 4; ++w) idc[fn][w] = idn[fn][w];
   }
   wait_vmcnt<0>();  // drain the clamped copies issued past the last chunk
 
