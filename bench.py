@@ -755,29 +755,29 @@ def time_single(torch, fasq, p, regime, steps=10):
     return t, kernel
 
 
-def time_per_subspace(torch, fasq, pi, rng, d=2, C=256, bits=8, steps=10, short=2, long=10):
+def time_per_subspace(torch, fasq, pi, rng, d=2, C=256, bits=8, M=1, steps=10, short=2, long=10):
     """fasq_pq_gemv_ex with one codebook per subspace (the paper's general
-    form; its sensitivity layer is 4096 x 4096 at d = 2, K_s = 256) at M = 1,
-    over rotated cold copies; the call is two kernels (the K-split partials and
-    their sum)."""
+    form; its sensitivity layer is 4096 x 4096 at d = 2, K_s = 256) at M
+    tokens, over rotated cold copies; the call is two kernels (the K-split
+    partials and their sum)."""
     S = SENS_K // d
     books = pi.draw_codebook(rng, S * C, d).reshape(S, C, d)
     ids = pi.draw_ids(rng, SENS_N, S, C)
     idx = pi.pack_indices(ids, bits)
-    x = pi.draw_x(rng, 1, SENS_K)
+    x = pi.draw_x(rng, M, SENS_K)
     dev = torch.device("cuda:0")
-    nbytes = idx.nbytes + books.nbytes + x.nbytes + SENS_N * 2
+    nbytes = idx.nbytes + books.nbytes + x.nbytes + M * SENS_N * 2
     copies = max(short + long, math.ceil(ROTATION_BYTES / nbytes) + 1)
-    ws_bytes = fasq.gemv_ex_workspace_bytes(1, SENS_K, SENS_N, bits, d, C, C * d)
+    ws_bytes = fasq.gemv_ex_workspace_bytes(M, SENS_K, SENS_N, bits, d, C, C * d)
     base = [torch.from_numpy(a).to(dev) for a in (x, idx, books)]
-    sets = [[t.clone() for t in base] + [torch.empty((1, SENS_N), dtype=torch.float16, device=dev),
+    sets = [[t.clone() for t in base] + [torch.empty((M, SENS_N), dtype=torch.float16, device=dev),
                                          torch.zeros(max(ws_bytes, 4), dtype=torch.uint8, device=dev)]
             for _ in range(copies)]
     stream = torch.cuda.current_stream()
 
     def launch(c):
         xs, ids_d, bk, y, ws = sets[c]
-        st = fasq.gemv_ex_raw(xs.data_ptr(), 1, SENS_K, SENS_N, ids_d.data_ptr(), bits, d, bk.data_ptr(), C, C * d,
+        st = fasq.gemv_ex_raw(xs.data_ptr(), M, SENS_K, SENS_N, ids_d.data_ptr(), bits, d, bk.data_ptr(), C, C * d,
                               y.data_ptr(), ws.data_ptr(), ws_bytes, stream.cuda_stream)
         assert st == 0, fasq.last_error()
 
@@ -798,10 +798,12 @@ def time_per_subspace(torch, fasq, pi, rng, d=2, C=256, bits=8, steps=10, short=
     t = max(float(np.median([(batch(0, long) - batch(long, short)) / (long - short) for _ in range(steps)])), 1e-7)
     del sets, base
     torch.cuda.empty_cache()
-    log(f"[bench] sensitivity per-subspace codebooks (4096 x 4096, d={d}, C={C}): {t * 1e6:.2f} us, "
+    log(f"[bench] sensitivity per-subspace codebooks (4096 x 4096, d={d}, C={C}, M={M}): {t * 1e6:.2f} us, "
         f"{nbytes / t / 1e9:.0f} GB/s (ids + books)")
-    return dict(d=d, C=C, idx_bits=bits, us=t * 1e6, bytes=nbytes, gbs=nbytes / t / 1e9,
-                workspace_bytes=ws_bytes, paper_rtx3090_us=32.0)
+    r = dict(d=d, C=C, idx_bits=bits, M=M, us=t * 1e6, bytes=nbytes, gbs=nbytes / t / 1e9, workspace_bytes=ws_bytes)
+    if M == 1:
+        r["paper_rtx3090_us"] = 32.0
+    return r
 
 
 def time_dense(torch, M, K, N, steps=10, short=2, long=10):
@@ -848,6 +850,7 @@ def sensitivity(torch, fasq, pi, core=False):
                     tflops=2.0 * M * SENS_N * SENS_K / t / 1e12, kernel=kern)
 
     out["per_subspace"] = time_per_subspace(torch, fasq, pi, rng)
+    out["per_subspace_tokens"] = [time_per_subspace(torch, fasq, pi, rng, M=M) for M in (4, 16)]
     dense1 = time_dense(torch, 1, SENS_K, SENS_N)
     out["dense_fp16_gemv_us"] = dense1 * 1e6
     log(f"[bench] sensitivity: dense fp16 GEMV (torch.matmul, M=1) {dense1 * 1e6:.2f} us")

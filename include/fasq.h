@@ -182,9 +182,11 @@ fasq_status fasq_pq_gemm_lut(const void* x, int64_t M, int64_t K, int64_t N,
  *              partial sums of the K split; contents are overwritten
  *
  * Other arguments, layouts and errors as fasq_pq_gemv.  With per-subspace
- * books and M = 1 the tuned kernel splits K over workgroups whose books fit
- * in LDS and adds the partials in a fixed order (deterministic); other shapes,
- * or a workspace that is too small, take the general kernel.  With one shared
+ * books and M <= 16 the tuned kernel splits K over workgroups whose books fit
+ * in LDS and adds the partials in a fixed order (deterministic; each token's
+ * output has the bits a call with that token alone gives); for M > 1 it needs
+ * d <= 4 and x 16-byte aligned with K * 2 a multiple of 16.  Other shapes, or
+ * a workspace that is too small, take the general kernel.  With one shared
  * codebook the call is fasq_pq_gemv, except that the workspace lets the
  * prefill GEMM split K as fasq_pq_gemm_ex does where the GEMM takes the call:
  * beyond 16 tokens, where no decode kernel applies, and, from 12 tokens on,

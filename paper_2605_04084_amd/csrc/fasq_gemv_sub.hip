@@ -1,8 +1,8 @@
 // Decode GEMV with one codebook per subspace (FASQ Sec. 3.1.1, Eq.
 // lut-accumulate with its per-subspace tables; Sec. 4.1 splits the subspaces
-// over blocks the same way), one token (M = 1).
+// over blocks the same way), for M <= 16 tokens.
 //
-//   y[n] = sum_s dot(x[s*d : (s+1)*d], codebook_s[u(n, s)])
+//   y[m, n] = sum_s dot(x[m, s*d : (s+1)*d], codebook_s[u(n, s)])
 //
 // The books of all subspaces (S x C x d fp16, 2 MB for a 4096-wide layer at
 // d = 2, C = 256) do not fit in LDS, so K is split over workgroups: workgroup
@@ -15,6 +15,11 @@
 // of a row sum their partials (DPP), and the row's fp32 partial for this
 // segment goes to the workspace.  A second kernel adds the segments of every
 // row in segment order and rounds to fp16 once: deterministic, no atomics.
+// One token keeps the lane's x slice in registers.  Several tokens (d <= 4)
+// stage the segment's slice of every row of x in LDS after the books; the
+// lane gathers its G codewords once per chunk and takes the dot products
+// with each token's slice in turn, so the ids and the gathers are shared by
+// all tokens.
 #include "fasq_codebook.h"
 #include "fasq_device.h"
 #include "fasq_internal.h"
@@ -26,9 +31,12 @@ namespace {
 constexpr int kSubThreads = 1024;               // 16 waves
 constexpr int kSubBookBytes = 144 * 1024;       // LDS for the books of one segment
 constexpr int kSubMaxNch = 16;                  // chunks per row segment (lanes per row)
+constexpr int kSubMaxTokens = 16;               // tokens of the multi-token kernel
 
 struct SubArgs {
   const half_t* x;
+  int64_t M, K;       // tokens, row length of x
+  int x_off;          // several tokens: LDS byte offset of the staged x slices
   int64_t N;
   const uint8_t* idx;
   int64_t R;          // bytes per id row
@@ -37,7 +45,7 @@ struct SubArgs {
   int C;
   int KS;             // segments
   int64_t rows_per_block;
-  float* ws;          // [KS x N] fp32 partials
+  float* ws;          // [KS x M x N] fp32 partials
 };
 
 // Codeword of book b (LDS byte address base + (b * C + u) * 2D) dotted with
@@ -57,14 +65,17 @@ __device__ __forceinline__ float dot_codeword(uint32_t addr, const uint32_t* xv,
   }
 }
 
-template <int BITS, int D, int NCH>
+// XL: several tokens, x slices staged in LDS (see the file comment).
+template <int BITS, int D, int NCH, bool XL>
 __global__ __launch_bounds__(kSubThreads) void k_gemv_sub(SubArgs a) {
   constexpr int G = Chunk<BITS>::G;
   constexpr int DW = Chunk<BITS>::DW;
   constexpr int CBY = DW * 4;
   constexpr int RPL = kWave / NCH;             // rows per wave-wide load
   constexpr int XW = D == 1 ? 1 : D / 2;       // dwords of x per id (D == 1: the low half)
+  constexpr int XSB = G * D * 2;               // bytes of one chunk's x slice (one token)
   static_assert(kWave % NCH == 0 && NCH <= kSubMaxNch, "NCH must divide the wave");
+  static_assert(!XL || (D <= 4 && XSB % 16 == 0), "the multi-token kernel takes d <= 4");
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
   const int ks = (int)(blockIdx.x % a.KS);
@@ -110,9 +121,23 @@ __global__ __launch_bounds__(kSubThreads) void k_gemv_sub(SubArgs a) {
       }
     }
   }
-  // x of the lane's chunk: G * D halves
-  uint32_t xv[G][XW];
-  {
+  // several tokens: the segment's slice of every row of x (NCH chunks of G
+  // ids, zeros past the row) after the books, 16-byte words
+  if constexpr (XL) {
+    constexpr int WPS = NCH * XSB / 16;  // words per token
+    const int words = (int)a.M * WPS;
+    const int64_t seg0 = (int64_t)ks * NCH * G * D;  // first x element of the segment
+    for (int w = threadIdx.x; w < words; w += blockDim.x) {
+      const int m = w / WPS, k = w - m * WPS;
+      const int64_t ch_w = (int64_t)ks * NCH + (k * 16) / XSB;  // chunk of the word
+      u32x4 v = u32x4{0u, 0u, 0u, 0u};
+      if (ch_w < a.CH) v = *reinterpret_cast<const u32x4*>(a.x + (int64_t)m * a.K + seg0 + (int64_t)k * 8);
+      *reinterpret_cast<u32x4*>(smem + a.x_off + (uint32_t)w * 16) = v;
+    }
+  }
+  // one token: x of the lane's chunk, G * D halves, in registers
+  uint32_t xv[XL ? 1 : G][XW];
+  if constexpr (!XL) {
     const uint16_t* xs = reinterpret_cast<const uint16_t*>(a.x) + (cval ? ch : 0) * G * D;
 #pragma unroll
     for (int i = 0; i < G; ++i) {
@@ -128,15 +153,50 @@ __global__ __launch_bounds__(kSubThreads) void k_gemv_sub(SubArgs a) {
 
   const uint32_t book0 = (uint32_t)c * G;  // first book of the lane's chunk
   auto compute = [&](const uint32_t* w, int k) {
-    float acc = 0.f;
-    if (cval) {  // a chunk past the row end (last segment) has no staged books
-#pragma unroll
-      for (int i = 0; i < G; ++i)
-        acc = dot_codeword<D>(((book0 + i) * (uint32_t)a.C + stream_id<BITS>(w, i)) * (2 * D), xv[i], acc);
-    }
-    acc = group_sum<NCH>(acc);
     const int64_t row = r0 + (int64_t)(wave + k * waves) * RPL + rl;
-    if (c == 0 && row < r1) a.ws[(int64_t)ks * a.N + row] = acc;
+    if constexpr (XL) {
+      // the chunk's G codewords (zeros past the row end: no staged books)
+      uint32_t cw[G][XW];
+#pragma unroll
+      for (int i = 0; i < G; ++i) {
+#pragma unroll
+        for (int q = 0; q < XW; ++q) cw[i][q] = 0u;
+        if (cval) read_codeword_lds<D>(((book0 + i) * (uint32_t)a.C + stream_id<BITS>(w, i)) * (2 * D), cw[i]);
+      }
+      const uint32_t xs0 = (uint32_t)a.x_off + (uint32_t)c * XSB;
+      for (int m = 0; m < (int)a.M; ++m) {
+        uint32_t xs[G * D / 2 > 0 ? G * D / 2 : 1];
+#pragma unroll
+        for (int q = 0; q < XSB / 16; ++q) {
+          const u32x4 v = *lds_at<u32x4>(xs0 + (uint32_t)m * (NCH * XSB) + (uint32_t)q * 16);
+          xs[4 * q] = v[0]; xs[4 * q + 1] = v[1]; xs[4 * q + 2] = v[2]; xs[4 * q + 3] = v[3];
+        }
+        float acc = 0.f;
+#pragma unroll
+        for (int i = 0; i < G; ++i) {
+          if constexpr (D == 1) {
+            const uint16_t xh = (uint16_t)(xs[i / 2] >> (16 * (i % 2)));
+            const half_t xf = __builtin_bit_cast(half_t, xh);
+            const half_t cf = __builtin_bit_cast(half_t, (uint16_t)(cw[i][0] & 0xFFFFu));
+            acc = __builtin_fmaf(static_cast<float>(xf), static_cast<float>(cf), acc);
+          } else {
+#pragma unroll
+            for (int q = 0; q < XW; ++q) acc = dot2(xs[i * XW + q], cw[i][q], acc);
+          }
+        }
+        acc = group_sum<NCH>(acc);
+        if (c == 0 && row < r1) a.ws[((int64_t)ks * a.M + m) * a.N + row] = acc;
+      }
+    } else {
+      float acc = 0.f;
+      if (cval) {  // a chunk past the row end (last segment) has no staged books
+#pragma unroll
+        for (int i = 0; i < G; ++i)
+          acc = dot_codeword<D>(((book0 + i) * (uint32_t)a.C + stream_id<BITS>(w, i)) * (2 * D), xv[i], acc);
+      }
+      acc = group_sum<NCH>(acc);
+      if (c == 0 && row < r1) a.ws[(int64_t)ks * a.N + row] = acc;
+    }
   };
   for (int k = 0; k < mine; k += 2) {
     compute(buf0, k);
@@ -148,12 +208,12 @@ __global__ __launch_bounds__(kSubThreads) void k_gemv_sub(SubArgs a) {
   }
 }
 
-// y[n] = fp16(sum over segments, in segment order, of ws[ks][n])
-__global__ void k_sub_reduce(const float* __restrict__ ws, int64_t N, int KS, half_t* __restrict__ y) {
-  for (int64_t n = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; n < N; n += (int64_t)gridDim.x * blockDim.x) {
+// y[m, n] = fp16(sum over segments, in segment order, of ws[ks][m][n])
+__global__ void k_sub_reduce(const float* __restrict__ ws, int64_t MN, int KS, half_t* __restrict__ y) {
+  for (int64_t o = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; o < MN; o += (int64_t)gridDim.x * blockDim.x) {
     float s = 0.f;
-    for (int k = 0; k < KS; ++k) s += ws[(int64_t)k * N + n];
-    y[n] = static_cast<half_t>(s);
+    for (int k = 0; k < KS; ++k) s += ws[(int64_t)k * MN + o];
+    y[o] = static_cast<half_t>(s);
   }
 }
 
@@ -165,9 +225,10 @@ struct SubPlan {
 };
 
 bool sub_plan(const Problem& p, const DeviceInfo& dev, SubPlan* out) {
-  if (p.M != 1 || p.cb_stride != p.C * p.d) return false;
+  if (p.M < 1 || p.M > kSubMaxTokens || p.cb_stride != p.C * p.d) return false;
   const int d = p.d;
   if (!(d == 1 || d == 2 || d == 4 || d == 8)) return false;
+  if (p.M > 1 && (d > 4 || (reinterpret_cast<uintptr_t>(p.x) & 15) || (p.K * 2) % 16)) return false;
   const int G = p.idx_bits == 8 ? 16 : 8;
   const int CBY = p.idx_bits == 12 ? 12 : 16;
   if (p.S % G || p.R != p.S / G * CBY) return false;
@@ -177,9 +238,10 @@ bool sub_plan(const Problem& p, const DeviceInfo& dev, SubPlan* out) {
     return false;
   if ((p.N + kWave) * p.R >= (int64_t(1) << 32)) return false;  // loads read up to one load past N
   const int64_t per_chunk = (int64_t)G * p.C * d * 2;  // book bytes per chunk of ids
+  const int64_t x_chunk = p.M > 1 ? p.M * G * d * 2 : 0;  // staged x bytes per chunk (several tokens)
   int nch = kSubMaxNch;
-  while (nch > 1 && nch * per_chunk > kSubBookBytes) nch /= 2;
-  if (per_chunk > kSubBookBytes) return false;
+  while (nch > 1 && (nch * per_chunk > kSubBookBytes || nch * (per_chunk + x_chunk) > dev.lds_per_block)) nch /= 2;
+  if (per_chunk > kSubBookBytes || per_chunk + x_chunk > dev.lds_per_block) return false;
   const int64_t CH = p.S / G;
   const int64_t ks = (CH + nch - 1) / nch;
   // row blocks: about one workgroup per CU in all, each with whole loads
@@ -200,8 +262,12 @@ bool sub_plan(const Problem& p, const DeviceInfo& dev, SubPlan* out) {
 
 template <int BITS, int D, int NCH>
 hipError_t launch_sub(const SubArgs& a, int blocks, int lds, hipStream_t stream) {
-  auto kern = k_gemv_sub<BITS, D, NCH>;
-  if (plan_record("k_gemv_sub", {BITS, D, NCH})) return hipSuccess;
+  const bool xl = a.M > 1;
+  if constexpr (D > 4) {
+    if (xl) return hipErrorNotSupported;
+  }
+  auto kern = xl ? k_gemv_sub<BITS, D, NCH, D <= 4> : k_gemv_sub<BITS, D, NCH, false>;
+  if (plan_record("k_gemv_sub", {BITS, D, NCH, xl ? 1 : 0})) return hipSuccess;
   hipError_t e = prepare_kernel(kern);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, dim3(blocks), dim3(kSubThreads), lds, stream, a);
@@ -234,19 +300,23 @@ hipError_t launch_sub_d(const SubArgs& a, int d, int nch, int blocks, int lds, h
 int64_t gemv_sub_workspace_bytes(const Problem& p, const DeviceInfo& dev) {
   SubPlan sp;
   if (!sub_plan(p, dev, &sp)) return 0;
-  return (int64_t)sp.ks * p.N * 4;
+  return (int64_t)sp.ks * p.M * p.N * 4;
 }
 
 hipError_t launch_gemv_sub(const Problem& p, void* workspace, int64_t workspace_bytes, const DeviceInfo& dev,
                            hipStream_t stream) {
   SubPlan sp;
   if (!sub_plan(p, dev, &sp)) return hipErrorNotSupported;
-  if (workspace == nullptr || workspace_bytes < (int64_t)sp.ks * p.N * 4 ||
+  if (workspace == nullptr || workspace_bytes < (int64_t)sp.ks * p.M * p.N * 4 ||
       (reinterpret_cast<uintptr_t>(workspace) & 3))
     return hipErrorNotSupported;
   const int G = p.idx_bits == 8 ? 16 : 8;
+  const int books = (int)((int64_t)sp.nch * G * p.C * p.d * 2);
   SubArgs a;
   a.x = static_cast<const half_t*>(p.x);
+  a.M = p.M;
+  a.K = p.K;
+  a.x_off = books;
   a.N = p.N;
   a.idx = static_cast<const uint8_t*>(p.idx);
   a.R = p.R;
@@ -256,7 +326,7 @@ hipError_t launch_gemv_sub(const Problem& p, void* workspace, int64_t workspace_
   a.KS = sp.ks;
   a.rows_per_block = sp.rows;
   a.ws = static_cast<float*>(workspace);
-  const int lds = (int)((int64_t)sp.nch * G * p.C * p.d * 2);
+  const int lds = books + (p.M > 1 ? (int)(p.M * sp.nch * G * p.d * 2) : 0);
   const int blocks = (int)(sp.rb * sp.ks);
   hipError_t e;
   switch (p.idx_bits) {
@@ -265,9 +335,9 @@ hipError_t launch_gemv_sub(const Problem& p, void* workspace, int64_t workspace_
     default: e = launch_sub_d<16>(a, p.d, sp.nch, blocks, lds, stream); break;
   }
   if (e != hipSuccess || plan().active) return e;
-  const int64_t rblocks = (p.N + 255) / 256;
+  const int64_t rblocks = (p.M * p.N + 255) / 256;
   hipLaunchKernelGGL(k_sub_reduce, dim3((unsigned)(rblocks < 65536 ? rblocks : 65536)), dim3(256), 0, stream,
-                     static_cast<const float*>(workspace), p.N, sp.ks, static_cast<half_t*>(p.y));
+                     static_cast<const float*>(workspace), p.M * p.N, sp.ks, static_cast<half_t*>(p.y));
   return hipGetLastError();
 }
 

@@ -171,10 +171,12 @@ def test_gemm_k_split(case, kind):
 
 
 @pytest.mark.parametrize("kind", KINDS)
-@pytest.mark.parametrize("case", [(1, 4096, 300, 2, 256, 8), (1, 768, 70, 4, 1024, 12)])
+@pytest.mark.parametrize("case", [(1, 4096, 300, 2, 256, 8), (1, 768, 70, 4, 1024, 12),
+                                  (4, 1024, 300, 2, 256, 8), (16, 768, 70, 4, 1024, 12)])
 def test_per_subspace_books(case, kind):
     """fasq_pq_gemv_ex with one codebook per subspace (the K-split kernel
-    with its books in LDS and v_dot2 products)."""
+    with its books in LDS and v_dot2 products; several tokens with their x
+    slices staged in LDS)."""
     M, K, N, d, C, bits = case
     S = K // d
     label = f"gemv_ex per-subspace {case} {kind}"

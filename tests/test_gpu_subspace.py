@@ -45,7 +45,16 @@ CASES = [
     (1, 512, 64, 1, 16, 8),
     (1, 768, 70, 4, 1024, 12),
     (1, 512, 50, 8, 256, 16),
-    (3, 256, 40, 2, 256, 8),          # M > 1: general kernel
+    (3, 256, 40, 2, 256, 8),          # several tokens: x slices staged in LDS
+    (2, 4096, 300, 2, 256, 8),
+    (4, 4096 + 128, 200, 2, 256, 8),  # several tokens, last segment half empty
+    (16, 2048, 130, 2, 256, 8),       # the most tokens the tuned kernel takes
+    (5, 1024, 100, 4, 256, 8),
+    (3, 512, 64, 1, 16, 8),
+    (7, 768, 70, 4, 1024, 12),
+    (2, 512, 50, 2, 256, 16),
+    (2, 512, 50, 8, 256, 16),         # several tokens at d = 8: general kernel
+    (17, 256, 40, 2, 256, 8),         # more than 16 tokens: general kernel
     (1, 36, 5, 4, 9, 12),             # odd 12-bit rows: general kernel
 ]
 
@@ -60,15 +69,20 @@ def test_per_subspace_books_match_oracle(case):
     assert_close(y, reference(x, books, idx, bits), f"per-subspace {case}")
 
 
-def test_tuned_path_is_taken_for_one_token():
-    # fp32 partials of 16 segments
+def test_tuned_path_takes_up_to_16_tokens():
+    # fp32 partials of 16 segments per token
     assert fasq.gemv_ex_workspace_bytes(1, 4096, 4096, 8, 2, 256, 512) == 16 * 4096 * 4
-    assert fasq.gemv_ex_workspace_bytes(3, 4096, 4096, 8, 2, 256, 512) == 0
+    assert fasq.gemv_ex_workspace_bytes(3, 4096, 4096, 8, 2, 256, 512) == 16 * 3 * 4096 * 4
+    assert fasq.gemv_ex_workspace_bytes(16, 4096, 4096, 8, 2, 256, 512) == 16 * 16 * 4096 * 4
+    # more tokens, or several tokens at d = 8: the general kernel, no workspace
+    assert fasq.gemv_ex_workspace_bytes(17, 4096, 4096, 8, 2, 256, 512) == 0
+    assert fasq.gemv_ex_workspace_bytes(2, 4096, 4096, 8, 8, 256, 2048) == 0
     assert fasq.gemv_ex_workspace_bytes(1, 4096, 4096, 8, 2, 256, 0) == 0
     assert fasq.gemv_ex_workspace_bytes(1, 4096, 4096, 8, 2, 256, 7) == -1
 
 
-@pytest.mark.parametrize("case", [(1, 2048, 128, 2, 256, 8), (1, 1024, 96, 4, 4096, 12)])
+@pytest.mark.parametrize("case", [(1, 2048, 128, 2, 256, 8), (1, 1024, 96, 4, 4096, 12),
+                                  (4, 2048, 128, 2, 256, 8), (3, 1024, 96, 4, 4096, 12), (16, 512, 64, 1, 16, 8)])
 def test_per_subspace_one_hot_is_bit_exact(case):
     M, K, N, d, C, bits = case
     rng = np.random.default_rng(3 + sum(case))
@@ -121,6 +135,19 @@ def test_one_workspace_serves_consecutive_calls_of_different_shapes():
             x, books, ids, idx = draw(rng, 1, K, N, 2, 256, 8)
             y = fasq.pq_gemv_ex(to_dev(x), to_dev(idx), 8, 2, to_dev(books), workspace=ws)
             assert_close(to_np(y).astype(np.float64), reference(x, books, idx, 8), f"reuse {rep} {K}x{N}")
+
+
+def test_several_tokens_match_single_token_calls():
+    """Each token of a multi-token call gives the bits of a call with that
+    token alone: the same segments, added in the same order."""
+    rng = np.random.default_rng(13)
+    M, K, N = 6, 4096, 700
+    x, books, ids, idx = draw(rng, M, K, N, 2, 256, 8)
+    idd, bd = to_dev(idx), to_dev(books)
+    y = fasq.pq_gemv_ex(to_dev(x), idd, 8, 2, bd)
+    for m in range(M):
+        ym = fasq.pq_gemv_ex(to_dev(np.ascontiguousarray(x[m:m + 1])), idd, 8, 2, bd)
+        assert torch.equal(y[m:m + 1].view(torch.int16), ym.view(torch.int16)), m
 
 
 def test_paper_layer_4096_2_256_sampled():

@@ -71,6 +71,8 @@ def _run_both(x, books, idx, M, K, N, d, C, bits, per_subspace):
 CASES = [
     ("per-subspace books, K split over workgroups", True,
      (1, 4096, 4096, 2, 256, 8), (1, 1024, 300, 2, 256, 8)),
+    ("per-subspace books, several tokens", True,
+     (8, 2048, 1000, 2, 256, 8), (3, 1024, 300, 2, 256, 8)),
     ("shared codebook, GEMM fallback with K split", False,
      (20, 2048, 300, 4, 256, 8), (17, 1024, 100, 4, 256, 8)),
     ("shared codebook, decode kernel (no scratch)", False,
