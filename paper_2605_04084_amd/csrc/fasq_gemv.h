@@ -360,6 +360,10 @@ struct GemvM1Part {
 };
 
 constexpr int kM1MaxParts = 8;   // parts one row-streaming launch can take
+#ifndef FASQ_M1_DIRECT_STORE
+#define FASQ_M1_DIRECT_STORE 1
+#endif
+constexpr bool kM1DirectStore = FASQ_M1_DIRECT_STORE != 0;
 
 // Products of the row-streaming kernels: packed fp16 dot products on the
 // vector ALU (1), or the diagonal of a 16 x 16 MFMA per token (0).
@@ -428,6 +432,13 @@ __device__ __forceinline__ void gemv_rows_body(const GemvM1Args& a) {
   const int g = lane >> 4;   // K group of the lane's chunk
   const int CH = (int)a.CH;
   const int nunits = a.NRW * T;
+  // One token, one wave per row (P = 1), one pass and at most two rows per
+  // wave (the small launches): the wave that sums a row stores it at once
+  // (its lane 0) instead of meeting the slowest wave at a final barrier.
+  // Otherwise the P waves' partials meet in LDS and are summed in a fixed
+  // order at the end: with many rows per wave (lm_head) or two tokens the
+  // scattered stores during the stream measured slower.
+  const bool direct = kM1DirectStore && MODE != CB_SLICE && MT == 1 && P == 1 && a.NRW <= 2;
 
   // chunk of this lane in unit t of its row part
   auto ccol_raw = [&](int t) { return (p * T + t) * 64 + lane; };
@@ -588,8 +599,14 @@ __device__ __forceinline__ void gemv_rows_body(const GemvM1Args& a) {
                             __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
           // slices of a row are summed in slice order, each by the same lane
           if (lane == 0) {
-            float* r = &red[(((u / T) * Q + q) * MT + m) * P + p];
-            *r = (MODE == CB_SLICE && si > 0) ? *r + sum : sum;
+            const int rl = (u / T) * Q + q;  // local row
+            if (direct) {
+              const int64_t n = (int64_t)wg + (int64_t)rl * nwg;
+              if (n < N && m < a.M) y[(int64_t)m * pt.ldy + n] = static_cast<half_t>(sum);
+            } else {
+              float* r = &red[(rl * MT + m) * P + p];
+              *r = (MODE == CB_SLICE && si > 0) ? *r + sum : sum;
+            }
           }
           dacc0[m] = dacc1[m] = 0.f;
           if constexpr (!kDecodeDot) {
@@ -647,6 +664,7 @@ __device__ __forceinline__ void gemv_rows_body(const GemvM1Args& a) {
       default: break;
     }
   }
+  if (direct) return;
   __syncthreads();
 
   // fixed-order sum over the P waves of each row, one fp16 rounding
