@@ -678,6 +678,28 @@ def load_traffic(kernel, set_name, names):
     return float(np.mean(vals))
 
 
+def decode_roofline(res, set_name):
+    """The HBM roofline of a decode layer's dominant kernel: the
+    instantiation with the largest share of the layer's kernel time
+    (launches that map to the same instantiation are pooled), algorithmic
+    bytes per launch over its mean launch time, and the counter traffic of
+    the same launches (counter set `set_name`) when the counters match the
+    sources."""
+    pools = {}
+    for r in res["launch_table"]:
+        g = pools.setdefault(r["kernel"], dict(us=0.0, bytes=0, n=0, names=[]))
+        g["us"] += r["us_median"]
+        g["bytes"] += r["bytes"]
+        g["n"] += 1
+        g["names"].append(r["name"])
+    dom_kernel, dom = max(pools.items(), key=lambda kv: kv[1]["us"])
+    achieved = (dom["bytes"] / dom["n"]) / (dom["us"] / dom["n"] * 1e-6) / 1e9
+    return dict(bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s", frac=achieved / HBM_PEAK_GBS,
+                traffic=None if set_name is None else load_traffic(dom_kernel, set_name, dom["names"]),
+                kernel=f"{dom_kernel} on {', '.join(dom['names'])}",
+                bytes_per_launch=dom["bytes"] / dom["n"], us_per_launch=dom["us"] / dom["n"])
+
+
 # ---------------------------------------------------------------------------
 # Workload runners
 # ---------------------------------------------------------------------------
@@ -1261,33 +1283,19 @@ def main():
 
     main_res = decode_layer(torch, fasq, pi, "llama3_8b_4bit", args.steps, args.warmup)
     report_layer("4bit", main_res)
-
-    # dominant kernel: the instantiation with the largest share of the layer's kernel time
-    # (launches that map to the same instantiation are pooled).
-    pools = {}
-    for r in main_res["launch_table"]:
-        g = pools.setdefault(r["kernel"], dict(us=0.0, bytes=0, n=0, names=[]))
-        g["us"] += r["us_median"]
-        g["bytes"] += r["bytes"]
-        g["n"] += 1
-        g["names"].append(r["name"])
-    dom_kernel, dom = max(pools.items(), key=lambda kv: kv[1]["us"])
-    achieved = (dom["bytes"] / dom["n"]) / (dom["us"] / dom["n"] * 1e-6) / 1e9
-    roofline = dict(bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
-                    frac=achieved / HBM_PEAK_GBS,
-                    traffic=load_traffic(dom_kernel, "llama3_8b_4bit", dom["names"]),
-                    kernel=f"{dom_kernel} on {', '.join(dom['names'])}",
-                    bytes_per_launch=dom["bytes"] / dom["n"], us_per_launch=dom["us"] / dom["n"])
+    roofline = decode_roofline(main_res, "llama3_8b_4bit")
 
     extra = {}
     if not args.no_extra:
         r3 = decode_layer(torch, fasq, pi, "llama3_8b_3bit", max(10, args.steps // 2), 3)
         report_layer("3bit", r3)
+        r3["roofline"] = decode_roofline(r3, "llama3_8b_3bit")
         extra["llama3_8b_3bit"] = r3
         extra["prefill"] = prefill(torch, fasq, pi, (128, 512, 2048), 10)
         extra["tiny"] = tiny_latency(torch, fasq, pi)
         r2 = decode_layer(torch, fasq, pi, "llama3_8b_4bit", max(10, args.steps // 2), 3, M=2)
         report_layer("4bit, M=2", r2)
+        r2["roofline"] = decode_roofline(r2, None)
         extra["llama3_8b_4bit_M2"] = r2
     if args.per_matrix:
         r1 = decode_layer(torch, fasq, pi, "llama3_8b_4bit", max(10, args.steps // 2), 3, grouped=False)
@@ -1302,6 +1310,7 @@ def main():
             r5 = decode_layer(torch, fasq, pi, "qwen3_8b_sweep", max(10, args.steps // 2), 3, M=M)
             report_layer(f"qwen3 M={M}", r5)
             r5["l2"] = qwen_l2_summary(counters, M, r5)
+            r5["roofline"] = decode_roofline(r5, f"qwen3_8b_M{M}")
             log(f"[bench] qwen3 M={M}: kernel sum {r5['us_per_layer_kernel_sum']:.2f} us/layer "
                 f"({r5['gbs_kernel_sum']:.1f} GB/s); x36 layers {36 * r5['us_per_layer_kernel_sum'] / 1e3:.3f} ms"
                 + (f"; L2 requests {r5['l2']['requests_per_layer'] / 1e6:.1f} M per layer, request-rate floor "
