@@ -360,6 +360,10 @@ struct GemvM1Part {
 };
 
 constexpr int kM1MaxParts = 8;   // parts one row-streaming launch can take
+// x slices (16-byte words per lane) the one-token row-streaming kernel keeps
+// in registers; more are read from LDS at every unit.  The two-token kernel
+// keeps up to twice as many (it then has no other large state).
+constexpr int kRowsXRegs = 8;
 #ifndef FASQ_M1_DIRECT_STORE
 #define FASQ_M1_DIRECT_STORE 1
 #endif
@@ -402,7 +406,7 @@ __device__ __forceinline__ void gemv_rows_body(const GemvM1Args& a) {
   // otherwise spill), the others a full pipeline's worth
   constexpr int L = MODE == CB_SLICE ? (T > 4 ? T : 4) : kGemvPipe;
   static_assert(L % T == 0, "pipeline depth must be a multiple of T");
-  constexpr bool kXInRegs = MT * T * SPC <= 8;
+  constexpr bool kXInRegs = MT * T * SPC <= kRowsXRegs * (MT > 1 ? 2 : 1);
 
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 

@@ -100,6 +100,7 @@ GEMV_PATHS = [
     ("k_gemv_m1", 3, (1, 2048, 100, 2, 65536, 16)),
     ("k_gemv_m1", 0, (1, 4096 + 512, 600, 2, 256, 8)),   # masked chunk tail
     ("k_gemv_mt", None, (2, 4096, 1000, 2, 256, 8)),
+    ("k_gemv_mt", 0, (2, 4096, 16500, 2, 256, 8)),        # many rows per CU: two loads per row part, x in registers
     ("k_gemv_mt", 1, (2, 1536, 260, 4, 4096, 12)),
     ("k_gemv", 0, (4, 4096, 500, 2, 256, 8)),
     ("k_gemv", 1, (8, 1024, 200, 4, 4096, 12)),
