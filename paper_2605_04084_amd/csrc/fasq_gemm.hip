@@ -31,6 +31,10 @@ hipError_t launch_gemm_variant(const GemmArgs& a, int lds, hipStream_t stream) {
 struct GemmTileShape {
   int bm, bn, ns;
 };
+// Build-time switches for measuring variants against each other (the
+// defaults are the measured choices): the ring depth of the 256 x 256 tile
+// (4 fits only with one codebook copy), and whether that tile may use the
+// half-row table (0: one copy).
 #ifndef FASQ_GEMM_BIG_NS
 #define FASQ_GEMM_BIG_NS 3
 #endif

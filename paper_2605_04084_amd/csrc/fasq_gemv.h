@@ -364,6 +364,9 @@ constexpr int kM1MaxParts = 8;   // parts one row-streaming launch can take
 // in registers; more are read from LDS at every unit.  The two-token kernel
 // keeps up to twice as many (it then has no other large state).
 constexpr int kRowsXRegs = 8;
+// Small one-token launches store each row sum from the wave that computed
+// it (1), or all through LDS after a final barrier (0): a build-time switch
+// for measuring the two against each other.
 #ifndef FASQ_M1_DIRECT_STORE
 #define FASQ_M1_DIRECT_STORE 1
 #endif
