@@ -39,6 +39,7 @@ import hashlib
 import json
 import math
 import os
+import re
 import sys
 import time
 
@@ -582,7 +583,14 @@ def trace_markdown(trace_dir, bench_json, out_path):
         bt = json.load(f)
 
     def short(name):
-        return name.replace("void fasq::", "").split("(")[0].replace("false", "0").replace("true", "1")
+        """Kernel name without namespaces and arguments; plain (mangled)
+        names of non-template kernels are cut down to their identifier."""
+        m = re.match(r"_ZN4fasq(?:12_GLOBAL__N_1)?(\d+)", name)
+        if m:
+            n = int(m.group(1))
+            return name[m.end():m.end() + n]
+        name = name.replace("void ", "").replace("fasq::", "").replace("(anonymous namespace)::", "")
+        return name.split("(")[0].replace("false", "0").replace("true", "1")
 
     lines = ["# libfasq kernels: rocprofv3 kernel statistics of the default bench.py run", "",
              "Command (from the repository root, on one MI355X):", "", "```", "export TMPDIR=/tmp",
@@ -597,7 +605,7 @@ def trace_markdown(trace_dir, bench_json, out_path):
              "| Kernel | Calls | Average µs | Min µs | Max µs |", "|---|---:|---:|---:|---:|"]
     avg = {}
     for r in stats:
-        if "fasq::" not in r["Name"]:
+        if "fasq::" not in r["Name"] and not r["Name"].startswith("_ZN4fasq"):
             continue
         avg[short(r["Name"])] = float(r["AverageNs"]) / 1e3
         lines.append(f"| `{short(r['Name'])}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.3f} | "

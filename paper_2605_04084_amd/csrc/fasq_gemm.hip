@@ -255,9 +255,16 @@ hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t
   }
   if (e != hipSuccess || a.ksplit == 1 || plan().active) return e;
   const int64_t mn = p.M * p.N;
-  const int64_t blocks = (mn + 255) / 256;
-  hipLaunchKernelGGL(k_gemm_split_reduce, dim3((unsigned)(blocks < 65536 ? blocks : 65536)), dim3(256), 0, stream,
-                     static_cast<const float*>(workspace), mn, a.ksplit, a.y);
+  const bool vec = mn % 4 == 0 && (reinterpret_cast<uintptr_t>(workspace) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(p.y) & 7) == 0;
+  const int64_t blocks = ((vec ? mn / 4 : mn) + 255) / 256;
+  const dim3 grid((unsigned)(blocks < 65536 ? blocks : 65536));
+  if (vec)
+    hipLaunchKernelGGL(k_gemm_split_reduce<true>, grid, dim3(256), 0, stream, static_cast<const float*>(workspace),
+                       mn, a.ksplit, a.y);
+  else
+    hipLaunchKernelGGL(k_gemm_split_reduce<false>, grid, dim3(256), 0, stream, static_cast<const float*>(workspace),
+                       mn, a.ksplit, a.y);
   return hipGetLastError();
 }
 

@@ -324,11 +324,29 @@ __global__ __launch_bounds__(WGM * WGN * KG * 64) void k_gemm_mfma(GemmArgs a) {
 }
 
 // y = fp16(sum over the K ranges, in range order, of the fp32 partials)
+// y = fp16(sum over the K ranges, in range order, of the fp32 partials).
+// VEC: four outputs per thread (16-byte partial loads, one 8-byte store),
+// taken when MN is a multiple of 4 and the buffers are aligned for it.
+template <bool VEC>
 __global__ void k_gemm_split_reduce(const float* __restrict__ ws, int64_t MN, int ksplit, half_t* __restrict__ y) {
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < MN; i += (int64_t)gridDim.x * blockDim.x) {
-    float s = 0.f;
-    for (int k = 0; k < ksplit; ++k) s += ws[(int64_t)k * MN + i];
-    y[i] = static_cast<half_t>(s);
+  if constexpr (VEC) {
+    const int64_t n4 = MN / 4;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n4; i += (int64_t)gridDim.x * blockDim.x) {
+      float4_t s = float4_t{0.f, 0.f, 0.f, 0.f};
+      for (int k = 0; k < ksplit; ++k) s += reinterpret_cast<const float4_t*>(ws + (int64_t)k * MN)[i];
+      half4_t h;
+      h[0] = static_cast<half_t>(s[0]);
+      h[1] = static_cast<half_t>(s[1]);
+      h[2] = static_cast<half_t>(s[2]);
+      h[3] = static_cast<half_t>(s[3]);
+      reinterpret_cast<half4_t*>(y)[i] = h;
+    }
+  } else {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < MN; i += (int64_t)gridDim.x * blockDim.x) {
+      float s = 0.f;
+      for (int k = 0; k < ksplit; ++k) s += ws[(int64_t)k * MN + i];
+      y[i] = static_cast<half_t>(s);
+    }
   }
 }
 

@@ -155,7 +155,8 @@ def test_gemm_tiles(path, kind):
 
 
 @pytest.mark.parametrize("kind", KINDS)
-@pytest.mark.parametrize("case", [(128, 4096, 4096, 4, 256, 8), (40, 14336, 200, 4, 4096, 12)])
+@pytest.mark.parametrize("case", [(128, 4096, 4096, 4, 256, 8), (40, 14336, 200, 4, 4096, 12),
+                                  (37, 8192, 211, 4, 256, 8)])  # M * N odd: the scalar reduce
 def test_gemm_k_split(case, kind):
     """fasq_pq_gemm_ex splitting K over workgroups (fp32 partials in the
     workspace, then the fixed-order sum)."""
