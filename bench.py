@@ -735,11 +735,18 @@ def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None, gro
     # copies w .. w + lpg - 1): every copy the timed loop reads was last read
     # at least copies - 1 layers earlier, far more than the 256 MB MALL holds.
     start = ((warmup - 1) % ms.copies + lpg) % ms.copies if warmup > 0 else 0
+    # Events on the replay stream beside the wall clock: their difference
+    # shows how much of the wall time is the host's launch of the graph.
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
+    ev0.record(stream)
     for r in range(steps // lpg):
         graphs[(start + r * lpg) % ms.copies].replay()
+    ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    gpu_graph = ev0.elapsed_time(ev1) * 1e-3
     del graphs
     per = ms.time_kernels(max(steps // 2, 10))
     med = [max(float(np.median(v)), 1e-7) for v in per]
@@ -755,6 +762,7 @@ def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None, gro
     res = dict(workload=wl_name, M=M, bytes_per_layer=step_bytes, copies=ms.copies, launches=len(rows),
                layers_per_graph=lpg,
                wall_s=wall, steps=steps, us_per_layer_graph=wall / steps * 1e6,
+               us_per_layer_graph_events=gpu_graph / steps * 1e6,
                us_per_layer_kernel_sum=sum(med) * 1e6, launch_table=rows)
     res["gbs_graph"] = step_bytes * steps / wall / 1e9
     res["gbs_kernel_sum"] = step_bytes / sum(med) / 1e9
@@ -1214,8 +1222,8 @@ def report_layer(tag, res):
         log(f"[bench] {tag} {r['name']:26s} K={r['K']:6d}: {r['us_median']:7.2f} us "
             f"{r['gbs']:7.1f} GB/s ({r['pct_hbm']:.1f}% of HBM peak) {r['kernel']}")
     log(f"[bench] {tag} layer: graph {res['us_per_layer_graph']:.2f} us/layer "
-        f"({res['gbs_graph']:.1f} GB/s), kernel sum {res['us_per_layer_kernel_sum']:.2f} us "
-        f"({res['gbs_kernel_sum']:.1f} GB/s)")
+        f"({res['gbs_graph']:.1f} GB/s; {res['us_per_layer_graph_events']:.2f} us between events on the stream), "
+        f"kernel sum {res['us_per_layer_kernel_sum']:.2f} us ({res['gbs_kernel_sum']:.1f} GB/s)")
 
 
 def main():
@@ -1365,6 +1373,7 @@ def main():
         },
         "pct_of_hbm_peak": 100.0 * value / HBM_PEAK_GBS,
         "us_per_layer": main_res["us_per_layer_graph"],
+        "us_per_layer_graph_events": main_res["us_per_layer_graph_events"],
         "us_per_layer_kernel_sum": main_res["us_per_layer_kernel_sum"],
         "gbs_kernel_sum": main_res["gbs_kernel_sum"],
         "launch_table": main_res["launch_table"],
