@@ -748,6 +748,18 @@ def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None, gro
     wall = time.perf_counter() - t0
     gpu_graph = ev0.elapsed_time(ev1) * 1e-3
     del graphs
+    # The same layers launched eagerly, back to back behind a spin kernel
+    # (the host's launches run ahead of the GPU): the GPU time without the
+    # graph, from events on the stream.  Reported beside the graph figure.
+    ev2, ev3 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    eager_layers = min(steps, ms.copies)
+    torch.cuda._sleep(SPACER_CYCLES * 4)
+    ev2.record(stream)
+    for k in range(eager_layers):
+        ms.launch_all((start + k) % ms.copies, stream.cuda_stream)
+    ev3.record(stream)
+    torch.cuda.synchronize()
+    eager = ev2.elapsed_time(ev3) * 1e-3 / eager_layers
     per = ms.time_kernels(max(steps // 2, 10))
     med = [max(float(np.median(v)), 1e-7) for v in per]
     mean = [max(float(np.mean(v)), 1e-7) for v in per]
@@ -762,7 +774,7 @@ def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None, gro
     res = dict(workload=wl_name, M=M, bytes_per_layer=step_bytes, copies=ms.copies, launches=len(rows),
                layers_per_graph=lpg,
                wall_s=wall, steps=steps, us_per_layer_graph=wall / steps * 1e6,
-               us_per_layer_graph_events=gpu_graph / steps * 1e6,
+               us_per_layer_graph_events=gpu_graph / steps * 1e6, us_per_layer_eager_events=eager * 1e6,
                us_per_layer_kernel_sum=sum(med) * 1e6, launch_table=rows)
     res["gbs_graph"] = step_bytes * steps / wall / 1e9
     res["gbs_kernel_sum"] = step_bytes / sum(med) / 1e9
@@ -1223,6 +1235,7 @@ def report_layer(tag, res):
             f"{r['gbs']:7.1f} GB/s ({r['pct_hbm']:.1f}% of HBM peak) {r['kernel']}")
     log(f"[bench] {tag} layer: graph {res['us_per_layer_graph']:.2f} us/layer "
         f"({res['gbs_graph']:.1f} GB/s; {res['us_per_layer_graph_events']:.2f} us between events on the stream), "
+        f"eager {res['us_per_layer_eager_events']:.2f} us/layer, "
         f"kernel sum {res['us_per_layer_kernel_sum']:.2f} us ({res['gbs_kernel_sum']:.1f} GB/s)")
 
 
@@ -1374,6 +1387,7 @@ def main():
         "pct_of_hbm_peak": 100.0 * value / HBM_PEAK_GBS,
         "us_per_layer": main_res["us_per_layer_graph"],
         "us_per_layer_graph_events": main_res["us_per_layer_graph_events"],
+        "us_per_layer_eager_events": main_res["us_per_layer_eager_events"],
         "us_per_layer_kernel_sum": main_res["us_per_layer_kernel_sum"],
         "gbs_kernel_sum": main_res["gbs_kernel_sum"],
         "launch_table": main_res["launch_table"],
