@@ -6,11 +6,14 @@ One step = one Llama-3-8B decoder layer of decode GEMVs at effective 4 bits
 read cold from HBM: the inputs are rotated over enough distinct copies
 (>= 1 GiB) that the 256 MB Infinity Cache cannot serve them.
 
-The timed region replays HIP graphs holding several consecutive layers each
-(a decode step replays the whole model from one graph); each layer is four
-launches, as deployed, since matrices that read the same activations go out as one
+The timed region runs one launch list of `steps` consecutive layers
+(fasq_launch_list_*: the launches are recorded once through the library
+calls, then queued by the library with one hipLaunchKernel each, as a
+serving loop would replay a decode step); each layer is four launches, as
+deployed, since matrices that read the same activations go out as one
 grouped call (q + k + v and gate + up through fasq_pq_gemv_batched; o and
-down alone).  Separately, per-launch durations come from HIP events on the
+down alone).  The same layers replayed from HIP graphs (several consecutive
+layers per graph) are timed beside it and reported as us_per_layer_graph.  Separately, per-launch durations come from HIP events on the
 launch stream around back-to-back launches of one group on distinct cold
 copies (behind a spin kernel, so that host launch latency does not enter the
 measurement): the difference between a 10-launch and a 2-launch batch,
@@ -620,7 +623,7 @@ def trace_markdown(trace_dir, bench_json, out_path):
               "same instantiation)", ""]
     tab = bt["launch_table"]
     nl = len(tab)
-    lpg = int(bt["config"]["timed_region"].split("HIP graph replays, ")[1].split(" ")[0])
+    lpg = int(bt["layers_per_graph"])
     kern = {r["kernel"] for r in tab}
     g = [r for r in trace if short(r["Kernel_Name"]) in kern]
     dur = np.array([(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in g])
@@ -653,6 +656,18 @@ def trace_markdown(trace_dir, bench_json, out_path):
             lines += ["", f"Gap between the end of one kernel and the start of the next inside the timed graph "
                       f"replays ({gaps.size} gaps): median {np.median(gaps):.2f} µs, mean {gaps.mean():.2f} µs, "
                       f"max {gaps.max():.2f} µs."]
+        # and inside the timed launch-list run (after a warm-up list of
+        # max(warmup, 1) layers)
+        a = nlay * nl + max(bt["warmup"], 1) * nl
+        b = a + bt["steps"] * nl
+        if len(g) >= b:
+            st = np.array([int(r["Start_Timestamp"]) for r in g[a:b]], dtype=np.float64)
+            en = np.array([int(r["End_Timestamp"]) for r in g[a:b]], dtype=np.float64)
+            lg = (st[1:] - en[:-1]) / 1e3
+            lines += ["", f"Gap between consecutive kernels inside the timed launch-list run ({lg.size} gaps): "
+                      f"median {np.median(lg):.2f} µs, mean {lg.mean():.2f} µs, max {lg.max():.2f} µs; the run "
+                      f"spans {(en[-1] - st[0]) / 1e3 / bt['steps']:.2f} µs per layer from the first kernel's start "
+                      f"to the last kernel's end."]
     with open(out_path, "w") as f:
         f.write("\n".join(lines) + "\n")
     log(f"[bench] wrote {out_path}")
@@ -748,6 +763,33 @@ def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None, gro
     wall = time.perf_counter() - t0
     gpu_graph = ev0.elapsed_time(ev1) * 1e-3
     del graphs
+    # The same layers queued from launch lists (fasq_launch_list_*): the
+    # launches recorded once through the same calls, then queued by the
+    # library with one hipLaunchKernel each, no HIP graph.  A warm-up list of
+    # max(warmup, 1) layers, then the timed list of `steps` layers, both on
+    # copies read at least copies - 1 layers earlier.
+    def record(first, count):
+        lst = fasq.LaunchList()
+        with lst:
+            for k in range(count):
+                ms.launch_all((first + k) % ms.copies, stream.cuda_stream)
+        return lst
+
+    lwarm = max(warmup, 1)
+    lstart = (start + steps) % ms.copies
+    warm_list, timed_list = record(lstart, lwarm), record(lstart + lwarm, steps)
+    warm_list.run(stream)
+    torch.cuda.synchronize()
+    ev4, ev5 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev4.record(stream)
+    timed_list.run(stream)
+    ev5.record(stream)
+    torch.cuda.synchronize()
+    wall_list = time.perf_counter() - t0
+    gpu_list = ev4.elapsed_time(ev5) * 1e-3
+    warm_list.close()
+    timed_list.close()
     # The same layers launched eagerly, back to back behind a spin kernel
     # (the host's launches run ahead of the GPU): the GPU time without the
     # graph, from events on the stream.  Reported beside the graph figure.
@@ -773,9 +815,12 @@ def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None, gro
     step_bytes = sum(r["bytes"] for r in rows)
     res = dict(workload=wl_name, M=M, bytes_per_layer=step_bytes, copies=ms.copies, launches=len(rows),
                layers_per_graph=lpg,
-               wall_s=wall, steps=steps, us_per_layer_graph=wall / steps * 1e6,
+               wall_s=wall_list, steps=steps, us_per_layer_list=wall_list / steps * 1e6,
+               us_per_layer_list_events=gpu_list / steps * 1e6,
+               wall_graph_s=wall, us_per_layer_graph=wall / steps * 1e6,
                us_per_layer_graph_events=gpu_graph / steps * 1e6, us_per_layer_eager_events=eager * 1e6,
                us_per_layer_kernel_sum=sum(med) * 1e6, launch_table=rows)
+    res["gbs_list"] = step_bytes * steps / wall_list / 1e9
     res["gbs_graph"] = step_bytes * steps / wall / 1e9
     res["gbs_kernel_sum"] = step_bytes / sum(med) / 1e9
     del ms
@@ -1233,7 +1278,9 @@ def report_layer(tag, res):
     for r in res["launch_table"]:
         log(f"[bench] {tag} {r['name']:26s} K={r['K']:6d}: {r['us_median']:7.2f} us "
             f"{r['gbs']:7.1f} GB/s ({r['pct_hbm']:.1f}% of HBM peak) {r['kernel']}")
-    log(f"[bench] {tag} layer: graph {res['us_per_layer_graph']:.2f} us/layer "
+    log(f"[bench] {tag} layer: launch list {res['us_per_layer_list']:.2f} us/layer ({res['gbs_list']:.1f} GB/s; "
+        f"{res['us_per_layer_list_events']:.2f} us between events), "
+        f"graph {res['us_per_layer_graph']:.2f} us/layer "
         f"({res['gbs_graph']:.1f} GB/s; {res['us_per_layer_graph_events']:.2f} us between events on the stream), "
         f"eager {res['us_per_layer_eager_events']:.2f} us/layer, "
         f"kernel sum {res['us_per_layer_kernel_sum']:.2f} us ({res['gbs_kernel_sum']:.1f} GB/s)")
@@ -1362,7 +1409,7 @@ def main():
         log(f"[bench] oracle: {cpu['value'] * 1e3:.2f} MB/s over {cpu['seconds']:.1f} s")
 
     ms_per_step = main_res["wall_s"] / args.steps * 1e3
-    value = main_res["gbs_graph"]
+    value = main_res["gbs_list"]
     record = {
         "metric": METRIC,
         "value": value,
@@ -1381,11 +1428,16 @@ def main():
                         "M=1, d=2, C=256, 8-bit ids, one fp16 codebook per matrix, uniform ids, seed 0",
             "bytes_per_step": main_res["bytes_per_layer"],
             "rotation_copies": main_res["copies"],
-            "timed_region": f"HIP graph replays, {main_res['layers_per_graph']} consecutive layers per graph, "
-                            "4 launches per layer (q+k+v and gate+up grouped, o, down), inputs cold in HBM",
+            "timed_region": f"one launch-list run of {args.steps} consecutive layers (fasq_launch_list_run: the "
+                            "launches recorded once through the library calls, queued with one hipLaunchKernel "
+                            "each), 4 launches per layer (q+k+v and gate+up grouped, o, down), inputs cold in HBM",
         },
+        "layers_per_graph": main_res["layers_per_graph"],
         "pct_of_hbm_peak": 100.0 * value / HBM_PEAK_GBS,
-        "us_per_layer": main_res["us_per_layer_graph"],
+        "us_per_layer": main_res["us_per_layer_list"],
+        "us_per_layer_list_events": main_res["us_per_layer_list_events"],
+        "us_per_layer_graph": main_res["us_per_layer_graph"],
+        "gbs_graph": main_res["gbs_graph"],
         "us_per_layer_graph_events": main_res["us_per_layer_graph_events"],
         "us_per_layer_eager_events": main_res["us_per_layer_eager_events"],
         "us_per_layer_kernel_sum": main_res["us_per_layer_kernel_sum"],

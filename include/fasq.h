@@ -32,8 +32,9 @@
  *
  * Conventions:
  *   - Every call is asynchronous on `stream` (0 = the null stream).  The
- *     library keeps no pointer after returning and allocates no device
- *     memory, so the calls may be captured in a hipGraph.  The plain entry
+ *     library allocates no device memory and, outside launch lists (below),
+ *     keeps no pointer after returning, so the calls may be captured in a
+ *     hipGraph.  The plain entry
  *     points use no scratch memory; the _ex calls and the encoder take a
  *     caller-owned workspace argument for theirs.
  *   - Argument checks run before any HIP call.  A bad argument returns
@@ -56,13 +57,14 @@
 extern "C" {
 #endif
 
-#define FASQ_ABI_VERSION 5
+#define FASQ_ABI_VERSION 6
 
 typedef enum {
   FASQ_OK = 0,
   FASQ_ERR_INVALID_ARG = 1, /* a size, pointer or format argument is invalid */
   FASQ_ERR_UNSUPPORTED = 2, /* valid, but no kernel handles this combination */
-  FASQ_ERR_HIP = 3          /* the HIP runtime reported an error */
+  FASQ_ERR_HIP = 3,         /* the HIP runtime reported an error */
+  FASQ_ERR_HOST_MEMORY = 4  /* host memory for a launch list could not be allocated */
 } fasq_status;
 
 /*
@@ -278,6 +280,61 @@ fasq_status fasq_pq_encode(const void* w, int64_t N, int64_t K, int d, int64_t C
 /* Workspace bytes fasq_pq_encode needs for these sizes; -1 if they are invalid
  * (N, K < 1; d does not divide K; C outside [1, 65536]). */
 int64_t fasq_pq_encode_workspace_bytes(int64_t N, int64_t K, int d, int64_t C);
+
+/*
+ * Launch lists: the kernel launches of a sequence of library calls, recorded
+ * once and queued again as often as needed, for callers that issue the same
+ * calls with the same buffers at every step (a serving loop's decode step, a
+ * benchmark) and want to pay only for the launches: no argument checks, no
+ * kernel selection, no HIP graph.  Between fasq_launch_list_begin and
+ * fasq_launch_list_end, every fasq_* compute call made on the calling thread
+ * (fasq_pq_gemv, _batched, _ex, _ex_noalloc, fasq_pq_gemm, _ex, _lut,
+ * fasq_pq_reconstruct, fasq_pq_encode) validates its arguments and chooses its
+ * kernels as usual, then appends its launches (kernel, grid, block, LDS bytes
+ * and a copy of the argument values) to the list instead of queueing them; its
+ * `stream` argument is ignored.  fasq_launch_list_run queues every recorded
+ * launch, in recording order, on `stream`.  A run computes what the recorded
+ * calls would have computed at that point of the stream, bit for bit.
+ *
+ * The list holds the device addresses the calls were given (inputs, outputs,
+ * workspaces, the static array of fasq_pq_gemv_ex_noalloc): they must stay
+ * valid while the list may run, and a run reads and writes their contents as
+ * they are when it executes.  A list records for the device current at
+ * fasq_launch_list_begin and runs only with that device current (its
+ * recorded launches from later begin/end pairs are appended and must be on
+ * the same device).  A call that fails while recording returns its error and
+ * may leave part of its launches in the list: destroy such a list.
+ *
+ *   fasq_launch_list_create   *list = a new, empty list.  FASQ_ERR_INVALID_ARG
+ *                             (list is NULL), FASQ_ERR_HOST_MEMORY.
+ *   fasq_launch_list_begin    the calling thread records into `list`.
+ *                             FASQ_ERR_INVALID_ARG when list is NULL, the
+ *                             thread already records a list, the list records
+ *                             on another thread, or it holds launches for
+ *                             another device; FASQ_ERR_HIP when no device is
+ *                             current.
+ *   fasq_launch_list_end      stop recording.  FASQ_ERR_INVALID_ARG when
+ *                             `list` does not record on the calling thread.
+ *   fasq_launch_list_run      queue the launches on `stream` (asynchronous).
+ *                             FASQ_ERR_INVALID_ARG when list is NULL, it
+ *                             records, the calling thread records a list, or
+ *                             another device is current; FASQ_ERR_HIP when a
+ *                             launch fails (fasq_last_error() names which;
+ *                             the launches before it are queued).  An empty
+ *                             list queues nothing.  Runs from several threads
+ *                             may share a list.
+ *   fasq_launch_list_size     launches recorded, -1 for a NULL list.
+ *   fasq_launch_list_destroy  free the list (and stop recording into it on the
+ *                             calling thread); NULL is ignored.  Launches
+ *                             already queued are not affected.
+ */
+typedef struct fasq_launch_list fasq_launch_list;
+fasq_status fasq_launch_list_create(fasq_launch_list** list);
+fasq_status fasq_launch_list_begin(fasq_launch_list* list);
+fasq_status fasq_launch_list_end(fasq_launch_list* list);
+fasq_status fasq_launch_list_run(const fasq_launch_list* list, hipStream_t stream);
+int64_t fasq_launch_list_size(const fasq_launch_list* list);
+void fasq_launch_list_destroy(fasq_launch_list* list);
 
 /*
  * Decode W_hat explicitly (the reconstruction the paper's reconstruction-free

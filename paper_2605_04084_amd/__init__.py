@@ -53,18 +53,21 @@ __all__ = [
     "FASQ_ERR_INVALID_ARG",
     "FASQ_ERR_UNSUPPORTED",
     "FASQ_ERR_HIP",
+    "FASQ_ERR_HOST_MEMORY",
+    "LaunchList",
     "EXPORTED_SYMBOLS",
     "ABI_VERSION",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfasq.so")
 
-ABI_VERSION = 5  # FASQ_ABI_VERSION of include/fasq.h
+ABI_VERSION = 6  # FASQ_ABI_VERSION of include/fasq.h
 
 FASQ_OK = 0
 FASQ_ERR_INVALID_ARG = 1
 FASQ_ERR_UNSUPPORTED = 2
 FASQ_ERR_HIP = 3
+FASQ_ERR_HOST_MEMORY = 4
 
 EXPORTED_SYMBOLS = (
     "fasq_pq_gemv",
@@ -85,6 +88,12 @@ EXPORTED_SYMBOLS = (
     "fasq_pq_gemm_ex_workspace_bytes",
     "fasq_pq_gemv_ex_noalloc",
     "fasq_noalloc_scratch_bytes",
+    "fasq_launch_list_create",
+    "fasq_launch_list_begin",
+    "fasq_launch_list_end",
+    "fasq_launch_list_run",
+    "fasq_launch_list_size",
+    "fasq_launch_list_destroy",
 )
 
 
@@ -159,6 +168,17 @@ def lib() -> ctypes.CDLL:
         L.fasq_pq_gemv_ex_noalloc.restype = _c_int
         L.fasq_noalloc_scratch_bytes.argtypes = []
         L.fasq_noalloc_scratch_bytes.restype = _c_i64
+        L.fasq_launch_list_create.argtypes = [ctypes.POINTER(_c_vp)]
+        L.fasq_launch_list_create.restype = _c_int
+        for name in ("fasq_launch_list_begin", "fasq_launch_list_end"):
+            getattr(L, name).argtypes = [_c_vp]
+            getattr(L, name).restype = _c_int
+        L.fasq_launch_list_run.argtypes = [_c_vp, _c_vp]
+        L.fasq_launch_list_run.restype = _c_int
+        L.fasq_launch_list_size.argtypes = [_c_vp]
+        L.fasq_launch_list_size.restype = _c_i64
+        L.fasq_launch_list_destroy.argtypes = [_c_vp]
+        L.fasq_launch_list_destroy.restype = None
         _lib = L
         return L
 
@@ -498,3 +518,69 @@ def pq_gemm_ex(x, idx, idx_bits: int, d: int, codebook, out=None, workspace=None
         return lib().fasq_pq_gemm_ex(xp, M_, K_, N_, ip, bits, dd, cp, C_, yp, ws_ptr, ws_bytes, stream)
 
     return _matmul(call, x, idx, idx_bits, d, codebook, out)
+
+
+# ---------------------------------------------------------------------------
+# Launch lists
+# ---------------------------------------------------------------------------
+
+class LaunchList:
+    """The kernel launches of a sequence of fasq calls, recorded once and
+    queued again with :meth:`run` (``fasq_launch_list_*``).
+
+    Calls made on this thread inside ``with lst:`` (or between :meth:`begin`
+    and :meth:`end`) are checked and planned as usual but only recorded; the
+    buffers they name must stay alive while the list may run.
+    """
+
+    def __init__(self):
+        h = _c_vp()
+        _check(lib().fasq_launch_list_create(ctypes.byref(h)))
+        self._h = h
+
+    @property
+    def handle(self) -> int:
+        """The ``fasq_launch_list*`` (0 once closed)."""
+        return (self._h.value or 0) if self._h is not None else 0
+
+    def begin(self) -> None:
+        _check(lib().fasq_launch_list_begin(self._live()))
+
+    def end(self) -> None:
+        _check(lib().fasq_launch_list_end(self._live()))
+
+    def __enter__(self) -> "LaunchList":
+        self.begin()
+        return self
+
+    def __exit__(self, *exc) -> bool:
+        self.end()
+        return False
+
+    def run(self, stream=None) -> None:
+        """Queue the recorded launches on ``stream`` (an integer HIP stream
+        handle, a torch stream, or None for torch's current stream)."""
+        if stream is None:
+            stream = _torch().cuda.current_stream().cuda_stream
+        elif not isinstance(stream, int):
+            stream = stream.cuda_stream
+        _check(lib().fasq_launch_list_run(self._live(), stream))
+
+    def __len__(self) -> int:
+        return int(lib().fasq_launch_list_size(self._live()))
+
+    def close(self) -> None:
+        if self._h is not None and self._h.value:
+            lib().fasq_launch_list_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _live(self):
+        if self._h is None or not self._h.value:
+            raise ValueError("the launch list is closed")
+        return self._h

@@ -292,6 +292,7 @@ const char* fasq_status_string(fasq_status s) {
     case FASQ_ERR_INVALID_ARG: return "FASQ_ERR_INVALID_ARG";
     case FASQ_ERR_UNSUPPORTED: return "FASQ_ERR_UNSUPPORTED";
     case FASQ_ERR_HIP: return "FASQ_ERR_HIP";
+    case FASQ_ERR_HOST_MEMORY: return "FASQ_ERR_HOST_MEMORY";
   }
   return "FASQ_UNKNOWN_STATUS";
 }

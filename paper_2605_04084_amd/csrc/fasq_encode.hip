@@ -238,9 +238,8 @@ hipError_t launch_assign_d(const half_t* w, int64_t P, int d, const half_t* cb, 
   auto go = [&](auto kern) {
     hipError_t e = prepare_kernel(kern);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kEncThreads), lds, stream, w, P, d, cb, C, assign, sums,
-                       counts);
-    return hipGetLastError();
+    return launch_kernel(kern, dim3((unsigned)blocks), dim3(kEncThreads), lds, stream, w, P, d, cb, C, assign, sums,
+                         counts);
   };
   if (!accum) return go(k_enc_assign<D, false, false>);
   return agg ? go(k_enc_assign<D, true, true>) : go(k_enc_assign<D, true, false>);
@@ -279,17 +278,17 @@ hipError_t launch_encode(const EncodeProblem& e, const DeviceInfo& dev, hipStrea
   const int64_t cbn = (int64_t)C * d;
   hipError_t err;
   if (e.init != e.codebook) {
-    hipLaunchKernelGGL(k_enc_copy, dim3(grid_for(cbn, 256)), dim3(256), 0, stream,
-                       static_cast<const uint16_t*>(e.init), cb, cbn);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
+    err = launch_kernel(k_enc_copy, dim3(grid_for(cbn, 256)), dim3(256), 0, stream,
+                        static_cast<const uint16_t*>(e.init), cb, cbn);
+    if (err != hipSuccess) return err;
   }
   for (int it = 0; it < e.iters; ++it) {
-    hipLaunchKernelGGL(k_enc_zero, dim3(grid_for(cbn + C, 256)), dim3(256), 0, stream, sums, cbn + C);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
+    err = launch_kernel(k_enc_zero, dim3(grid_for(cbn + C, 256)), dim3(256), 0, stream, sums, cbn + C);
+    if (err != hipSuccess) return err;
     err = launch_assign(w, P, d, reinterpret_cast<const half_t*>(cb), C, assign, sums, counts, true, dev, stream);
     if (err != hipSuccess) return err;
-    hipLaunchKernelGGL(k_enc_update, dim3(grid_for(cbn, 256)), dim3(256), 0, stream, cb, sums, counts, C, d);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
+    err = launch_kernel(k_enc_update, dim3(grid_for(cbn, 256)), dim3(256), 0, stream, cb, sums, counts, C, d);
+    if (err != hipSuccess) return err;
   }
   err = launch_assign(w, P, d, reinterpret_cast<const half_t*>(cb), C, assign, sums, counts, false, dev, stream);
   if (err != hipSuccess) return err;
@@ -297,11 +296,10 @@ hipError_t launch_encode(const EncodeProblem& e, const DeviceInfo& dev, hipStrea
   const unsigned g = grid_for(e.N * per_row, 256);
   uint8_t* idx = static_cast<uint8_t*>(e.idx);
   switch (e.idx_bits) {
-    case 8: hipLaunchKernelGGL(k_enc_pack<8>, dim3(g), dim3(256), 0, stream, assign, e.N, S, e.R, idx); break;
-    case 12: hipLaunchKernelGGL(k_enc_pack<12>, dim3(g), dim3(256), 0, stream, assign, e.N, S, e.R, idx); break;
-    default: hipLaunchKernelGGL(k_enc_pack<16>, dim3(g), dim3(256), 0, stream, assign, e.N, S, e.R, idx); break;
+    case 8: return launch_kernel(k_enc_pack<8>, dim3(g), dim3(256), 0, stream, assign, e.N, S, e.R, idx);
+    case 12: return launch_kernel(k_enc_pack<12>, dim3(g), dim3(256), 0, stream, assign, e.N, S, e.R, idx);
+    default: return launch_kernel(k_enc_pack<16>, dim3(g), dim3(256), 0, stream, assign, e.N, S, e.R, idx);
   }
-  return hipGetLastError();
 }
 
 }  // namespace fasq

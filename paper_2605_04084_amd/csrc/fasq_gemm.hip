@@ -14,8 +14,7 @@ hipError_t launch_gemm_variant(const GemmArgs& a, int lds, hipStream_t stream) {
   hipError_t e = prepare_kernel(kern);
   if (e != hipSuccess) return e;
   dim3 grid((unsigned)((a.N + BN - 1) / BN), (unsigned)((a.M + BM - 1) / BM), (unsigned)a.ksplit);
-  hipLaunchKernelGGL(kern, grid, dim3(WGM * WGN * KG * kWave), lds, stream, a);
-  return hipGetLastError();
+  return launch_kernel(kern, grid, dim3(WGM * WGN * KG * kWave), lds, stream, a);
 }
 
 // Tile shapes, largest first: 256 x 256 and 128 x 256 on 2 x 4 waves (two
@@ -260,12 +259,10 @@ hipError_t launch_gemm_mfma(const Problem& p, const DeviceInfo& dev, hipStream_t
   const int64_t blocks = ((vec ? mn / 4 : mn) + 255) / 256;
   const dim3 grid((unsigned)(blocks < 65536 ? blocks : 65536));
   if (vec)
-    hipLaunchKernelGGL(k_gemm_split_reduce<true>, grid, dim3(256), 0, stream, static_cast<const float*>(workspace),
+    return launch_kernel(k_gemm_split_reduce<true>, grid, dim3(256), 0, stream, static_cast<const float*>(workspace),
+                         mn, a.ksplit, a.y);
+  return launch_kernel(k_gemm_split_reduce<false>, grid, dim3(256), 0, stream, static_cast<const float*>(workspace),
                        mn, a.ksplit, a.y);
-  else
-    hipLaunchKernelGGL(k_gemm_split_reduce<false>, grid, dim3(256), 0, stream, static_cast<const float*>(workspace),
-                       mn, a.ksplit, a.y);
-  return hipGetLastError();
 }
 
 }  // namespace fasq

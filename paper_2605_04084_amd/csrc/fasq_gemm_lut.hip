@@ -148,8 +148,7 @@ hipError_t launch_lut(const LutArgs& a, hipStream_t stream) {
   if (e != hipSuccess) return e;
   const int lds = (2 * SB * kLutTokens * a.C + 2 * kLutTokens * SB * D) * 4;
   dim3 grid((unsigned)((a.N + kLutThreads - 1) / kLutThreads), (unsigned)((a.M + kLutTokens - 1) / kLutTokens));
-  hipLaunchKernelGGL(kern, grid, dim3(kLutThreads), lds, stream, a);
-  return hipGetLastError();
+  return launch_kernel(kern, grid, dim3(kLutThreads), lds, stream, a);
 }
 
 template <int BITS, int D>

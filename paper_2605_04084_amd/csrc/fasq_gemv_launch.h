@@ -75,8 +75,7 @@ hipError_t launch_gemv_variant(const GemvArgs& a, bool mask, int threads, dim3 b
       auto kern = k_gemv<BITS, D, T, MODE, MR, true, true>;
       hipError_t e = prepare_kernel(kern);
       if (e != hipSuccess) return e;
-      hipLaunchKernelGGL(kern, blocks, dim3(threads), lds, stream, a);
-      return hipGetLastError();
+      return launch_kernel(kern, blocks, dim3(threads), lds, stream, a);
     } else {
       return hipErrorNotSupported;
     }
@@ -85,8 +84,7 @@ hipError_t launch_gemv_variant(const GemvArgs& a, bool mask, int threads, dim3 b
   if (plan_record("k_gemv", {BITS, D, T, MODE, MR, mask ? 1 : 0})) return hipSuccess;
   hipError_t e = prepare_kernel(kern);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, blocks, dim3(threads), lds, stream, a);
-  return hipGetLastError();
+  return launch_kernel(kern, blocks, dim3(threads), lds, stream, a);
 }
 
 template <int BITS, int MR, int D, int MODE>
@@ -314,8 +312,7 @@ template <typename K>
 hipError_t launch_rows_kernel(K kern, const GemvM1Args& a, int threads, dim3 grid, int lds, hipStream_t stream) {
   hipError_t e = prepare_kernel(kern);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, grid, dim3(threads), lds, stream, a);
-  return hipGetLastError();
+  return launch_kernel(kern, grid, dim3(threads), lds, stream, a);
 }
 
 // mt: token slots (1 or 2); two tokens only with the codebook in LDS.

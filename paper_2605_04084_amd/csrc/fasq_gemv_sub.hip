@@ -270,8 +270,7 @@ hipError_t launch_sub(const SubArgs& a, int blocks, int lds, hipStream_t stream)
   if (plan_record("k_gemv_sub", {BITS, D, NCH, xl ? 1 : 0})) return hipSuccess;
   hipError_t e = prepare_kernel(kern);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3(blocks), dim3(kSubThreads), lds, stream, a);
-  return hipGetLastError();
+  return launch_kernel(kern, dim3(blocks), dim3(kSubThreads), lds, stream, a);
 }
 
 template <int BITS, int D>
@@ -336,9 +335,8 @@ hipError_t launch_gemv_sub(const Problem& p, void* workspace, int64_t workspace_
   }
   if (e != hipSuccess || plan().active) return e;
   const int64_t rblocks = (p.M * p.N + 255) / 256;
-  hipLaunchKernelGGL(k_sub_reduce, dim3((unsigned)(rblocks < 65536 ? rblocks : 65536)), dim3(256), 0, stream,
-                     static_cast<const float*>(workspace), p.M * p.N, sp.ks, static_cast<half_t*>(p.y));
-  return hipGetLastError();
+  return launch_kernel(k_sub_reduce, dim3((unsigned)(rblocks < 65536 ? rblocks : 65536)), dim3(256), 0, stream,
+                       static_cast<const float*>(workspace), p.M * p.N, sp.ks, static_cast<half_t*>(p.y));
 }
 
 }  // namespace fasq

@@ -84,11 +84,10 @@ hipError_t launch_reconstruct(const Problem& p, void* w, hipStream_t stream) {
   const uint16_t* cb = static_cast<const uint16_t*>(p.codebook);
   uint16_t* out = static_cast<uint16_t*>(w);
   switch (p.idx_bits) {
-    case 8: hipLaunchKernelGGL(k_reconstruct<8>, dim3(blocks), dim3(256), 0, stream, idx, p.N, S, p.R, p.d, cb, p.cb_stride, out); break;
-    case 12: hipLaunchKernelGGL(k_reconstruct<12>, dim3(blocks), dim3(256), 0, stream, idx, p.N, S, p.R, p.d, cb, p.cb_stride, out); break;
-    default: hipLaunchKernelGGL(k_reconstruct<16>, dim3(blocks), dim3(256), 0, stream, idx, p.N, S, p.R, p.d, cb, p.cb_stride, out); break;
+    case 8: return launch_kernel(k_reconstruct<8>, dim3(blocks), dim3(256), 0, stream, idx, p.N, S, p.R, p.d, cb, p.cb_stride, out);
+    case 12: return launch_kernel(k_reconstruct<12>, dim3(blocks), dim3(256), 0, stream, idx, p.N, S, p.R, p.d, cb, p.cb_stride, out);
+    default: return launch_kernel(k_reconstruct<16>, dim3(blocks), dim3(256), 0, stream, idx, p.N, S, p.R, p.d, cb, p.cb_stride, out);
   }
-  return hipGetLastError();
 }
 
 hipError_t launch_generic(const Problem& p, hipStream_t stream) {
@@ -99,11 +98,10 @@ hipError_t launch_generic(const Problem& p, hipStream_t stream) {
   const half_t* cb = static_cast<const half_t*>(p.codebook);
   half_t* y = static_cast<half_t*>(p.y);
   switch (p.idx_bits) {
-    case 8: hipLaunchKernelGGL(k_pq_generic<8>, dim3(blocks), dim3(256), 0, stream, x, p.M, p.K, p.N, idx, p.R, p.d, cb, p.cb_stride, y); break;
-    case 12: hipLaunchKernelGGL(k_pq_generic<12>, dim3(blocks), dim3(256), 0, stream, x, p.M, p.K, p.N, idx, p.R, p.d, cb, p.cb_stride, y); break;
-    default: hipLaunchKernelGGL(k_pq_generic<16>, dim3(blocks), dim3(256), 0, stream, x, p.M, p.K, p.N, idx, p.R, p.d, cb, p.cb_stride, y); break;
+    case 8: return launch_kernel(k_pq_generic<8>, dim3(blocks), dim3(256), 0, stream, x, p.M, p.K, p.N, idx, p.R, p.d, cb, p.cb_stride, y);
+    case 12: return launch_kernel(k_pq_generic<12>, dim3(blocks), dim3(256), 0, stream, x, p.M, p.K, p.N, idx, p.R, p.d, cb, p.cb_stride, y);
+    default: return launch_kernel(k_pq_generic<16>, dim3(blocks), dim3(256), 0, stream, x, p.M, p.K, p.N, idx, p.R, p.d, cb, p.cb_stride, y);
   }
-  return hipGetLastError();
 }
 
 }  // namespace fasq

@@ -6,7 +6,11 @@
 
 #include <atomic>
 #include <initializer_list>
+#include <memory>
 #include <string>
+#include <tuple>
+#include <utility>
+#include <vector>
 
 namespace fasq {
 
@@ -125,6 +129,65 @@ struct Plan {
 Plan& plan();
 // Record `base<params...>` as the planned kernel; returns true when planning.
 bool plan_record(const char* base, std::initializer_list<int> params);
+
+// ---------------------------------------------------------------------------
+// Launch recording (fasq_launch_list_*).  While a list records on the calling
+// thread, every kernel launch of the library is appended to it (kernel, grid,
+// block, dynamic LDS bytes and a copy of the argument values) instead of
+// being queued; fasq_launch_list_run queues the recorded launches later.
+// ---------------------------------------------------------------------------
+struct LaunchArgs {
+  virtual ~LaunchArgs() = default;
+  virtual void** pointers() = 0;  // one pointer per kernel parameter, as hipLaunchKernel takes them
+};
+
+// The argument values of one launch, held with the kernel's own parameter
+// types (so each pointer addresses exactly the bytes of its parameter).
+template <typename... T>
+struct LaunchArgsOf final : LaunchArgs {
+  std::tuple<T...> values;
+  void* ptrs[sizeof...(T) > 0 ? sizeof...(T) : 1];
+  explicit LaunchArgsOf(T... v) : values(v...) { point(std::index_sequence_for<T...>{}); }
+  LaunchArgsOf(const LaunchArgsOf&) = delete;
+  LaunchArgsOf& operator=(const LaunchArgsOf&) = delete;
+  void** pointers() override { return ptrs; }
+
+ private:
+  template <size_t... I>
+  void point(std::index_sequence<I...>) {
+    ((ptrs[I] = static_cast<void*>(&std::get<I>(values))), ...);
+  }
+};
+
+struct RecordedLaunch {
+  const void* kernel;  // host-side handle of the __global__ function
+  dim3 grid, block;
+  size_t lds;
+  std::unique_ptr<LaunchArgs> args;
+};
+
+// The launches the calling thread records into (nullptr: launches are queued).
+std::vector<RecordedLaunch>*& recording_into();
+
+// Queue kernel `kern` on `stream`, or record the launch when the calling
+// thread records a launch list.  Returns the launch error (hipSuccess when
+// recorded; hipErrorOutOfMemory when the host cannot hold the record).
+template <typename... KArgs, typename... Args>
+hipError_t launch_kernel(void (*kern)(KArgs...), dim3 grid, dim3 block, size_t lds, hipStream_t stream,
+                         Args&&... args) {
+  static_assert(sizeof...(KArgs) == sizeof...(Args), "one value per kernel parameter");
+  if (std::vector<RecordedLaunch>* out = recording_into()) {
+    try {
+      out->push_back(RecordedLaunch{reinterpret_cast<const void*>(kern), grid, block, lds,
+                                    std::make_unique<LaunchArgsOf<KArgs...>>(static_cast<KArgs>(args)...)});
+    } catch (...) {
+      return hipErrorOutOfMemory;
+    }
+    return hipSuccess;
+  }
+  hipLaunchKernelGGL(kern, grid, block, lds, stream, std::forward<Args>(args)...);
+  return hipGetLastError();
+}
 
 // Sets the calling thread's fasq_last_error() text.
 void set_last_error(const std::string& msg);

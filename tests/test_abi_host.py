@@ -49,6 +49,7 @@ def test_status_strings(L):
     assert fasq.status_string(1) == "FASQ_ERR_INVALID_ARG"
     assert fasq.status_string(2) == "FASQ_ERR_UNSUPPORTED"
     assert fasq.status_string(3) == "FASQ_ERR_HIP"
+    assert fasq.status_string(4) == "FASQ_ERR_HOST_MEMORY"
     assert fasq.status_string(99) == "FASQ_UNKNOWN_STATUS"
 
 
@@ -213,3 +214,34 @@ def test_gemm_ex_workspace_bytes_invalid_sizes(L):
     assert fasq.gemm_ex_workspace_bytes(0, 16, 4, 8, 2, 256) == -1
     assert fasq.gemm_ex_workspace_bytes(1, 10, 4, 8, 4, 256) == -1
     assert fasq.gemm_ex_workspace_bytes(1, 16, 4, 8, 2, 300) == -1
+
+
+def test_launch_list_host_paths(L):
+    """Launch lists: creation, size, misuse and the empty run need no GPU."""
+    h = ctypes.c_void_p()
+    assert L.fasq_launch_list_create(ctypes.byref(h)) == fasq.FASQ_OK and h.value
+    try:
+        assert L.fasq_launch_list_size(h) == 0
+        assert L.fasq_launch_list_end(h) == fasq.FASQ_ERR_INVALID_ARG  # not recording
+        assert "not recording" in fasq.last_error()
+        assert L.fasq_launch_list_run(h, None) == fasq.FASQ_OK  # empty: queues nothing
+        st = L.fasq_launch_list_begin(h)
+        if st == fasq.FASQ_OK:  # a GPU is present: recording started, end it
+            assert L.fasq_launch_list_end(h) == fasq.FASQ_OK
+        else:
+            assert st == fasq.FASQ_ERR_HIP and "device" in fasq.last_error()
+        assert L.fasq_launch_list_size(h) == 0
+    finally:
+        L.fasq_launch_list_destroy(h)
+    assert L.fasq_launch_list_create(None) == fasq.FASQ_ERR_INVALID_ARG
+    assert L.fasq_launch_list_begin(None) == fasq.FASQ_ERR_INVALID_ARG
+    assert L.fasq_launch_list_end(None) == fasq.FASQ_ERR_INVALID_ARG
+    assert L.fasq_launch_list_run(None, None) == fasq.FASQ_ERR_INVALID_ARG
+    assert L.fasq_launch_list_size(None) == -1
+    L.fasq_launch_list_destroy(None)
+    lst = fasq.LaunchList()
+    assert len(lst) == 0 and lst.handle
+    lst.close()
+    assert lst.handle == 0
+    with pytest.raises(ValueError):
+        len(lst)

@@ -2,12 +2,12 @@
 
 Each workload's matrices go out in bench.py's launch groups (q+k+v and
 gate+up as one grouped call, the others alone, a workspace where the call
-takes one), first eagerly and then from a captured HIP graph replayed several
-times.  Every output element must be written (the buffers start as NaN).  The
+takes one), first eagerly, then from a launch list (the timed form) run
+several times and from a captured HIP graph replayed several times.  Every output element must be written (the buffers start as NaN).  The
 single-token effective-4-bit and effective-3-bit layers, lm_head included,
 are compared with the oracle on every output row; the others on sampled rows
 that include the rows at every possible part boundary of a grouped launch.
-Every replay must equal the eager result bit for bit.
+Every run and replay must equal the eager result bit for bit.
 """
 
 import numpy as np
@@ -72,6 +72,21 @@ def test_decode_layer_as_timed(wl_name, M):
         ref = orc.pq_linear(x_of[i], p.idx, p.idx_bits, p.d, p.codebook, rows=rows)
         assert_close(got.astype(np.float64)[:, rows], ref,
                      f"{wl_name} M={M} {name} ({'all' if full else len(rows)} rows)")
+
+    # the same launches recorded into a launch list, as bench.py times them
+    lst = fasq.LaunchList()
+    with lst:
+        ms.launch_all(0, stream)
+    assert len(lst) >= len(ms.groups)
+    for rep in range(3):
+        for y in ys:
+            y.fill_(float("nan"))
+        torch.cuda.synchronize()
+        lst.run(stream)
+        torch.cuda.synchronize()
+        for name, y, e in zip(names, ys, eager):
+            assert np.array_equal(y.cpu().numpy().view(np.uint16), e.view(np.uint16)), f"list run {rep} {name}"
+    lst.close()
 
     # the same launches from a graph (capture_graphs warms up eagerly first)
     graphs = ms.capture_graphs(1)
