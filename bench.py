@@ -627,13 +627,19 @@ def trace_markdown(trace_dir, bench_json, out_path):
     kern = {r["kernel"] for r in tab}
     g = [r for r in trace if short(r["Kernel_Name"]) in kern]
     dur = np.array([(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in g])
-    # the layer's launches come first: the eager warm-up (one layer per copy),
-    # then the warm-up and timed graph replays, lpg layers each
-    nlay = bt["config"]["rotation_copies"] + (bt["warmup"] + bt["steps"] // lpg) * lpg
+    # the layer's launches come first, in this order: the eager warm-up (one
+    # layer per copy), the warm-up list (max(warmup, 1) layers), the timed
+    # list (steps layers), the warm-up graph replays (at least warmup layers,
+    # whole graphs of lpg layers) and the timed graph replays (steps layers)
+    W, K = bt["warmup"], bt["steps"]
+    lw, gw = max(W, 1), max(1, -(-W // lpg)) * lpg
+    seg = {"list": bt["config"]["rotation_copies"] + lw}
+    seg["graph"] = seg["list"] + K + gw
+    nlay = seg["graph"] + K
     if dur.size >= nlay * nl:
         D = dur[:nlay * nl].reshape(nlay, nl)
         lines += ["Per launch of the effective-4-bit layer (M = 1): rocprofv3 median duration over the eager "
-                  "warm-up and the graph replays, against bench.py's HIP events:", "",
+                  "warm-up, the launch lists and the graph replays, against bench.py's HIP events:", "",
                   "| Launch | rows (N) × K | rocprofv3 median µs | bench.py µs (events) |", "|---|---|---:|---:|"]
         for j, m in enumerate(tab):
             lines.append(f"| {m['name']} | {'+'.join(str(n) for n in m['N'])} × {m['K']} | "
@@ -643,31 +649,33 @@ def trace_markdown(trace_dir, bench_json, out_path):
             lines += ["", f"The dominant kernel over its launches in this layer ({', '.join(tab[j]['name'] for j in dj)}): "
                       f"rocprofv3 {np.mean([np.median(D[:, j]) for j in dj]):.3f} µs per launch (mean of the "
                       f"per-launch medians) against bench.py's {rl['us_per_launch']:.3f} µs."]
-        # gaps between consecutive kernels inside the timed graph replays
         starts = np.array([int(r["Start_Timestamp"]) for r in g[:nlay * nl]], dtype=np.float64)
         ends = np.array([int(r["End_Timestamp"]) for r in g[:nlay * nl]], dtype=np.float64)
-        first_timed = (bt["config"]["rotation_copies"] + bt["warmup"] * lpg) * nl
-        gaps = []
-        for k in range(bt["steps"] // lpg):
-            a = first_timed + k * lpg * nl
-            gaps.extend((starts[a + 1:a + lpg * nl] - ends[a:a + lpg * nl - 1]) / 1e3)
-        if gaps:
-            gaps = np.array(gaps)
+
+        def gaps_of(first_layer, layers, per):
+            """Gaps between consecutive kernels of `layers` layers from
+            `first_layer`, within runs of `per` layers (one graph or list)."""
+            out = []
+            for k in range(layers // per):
+                a = (first_layer + k * per) * nl
+                out.extend((starts[a + 1:a + per * nl] - ends[a:a + per * nl - 1]) / 1e3)
+            return np.array(out)
+
+        lg = gaps_of(seg["list"], K, K)
+        a, b = seg["list"] * nl, (seg["list"] + K) * nl
+        lines += ["", f"Gap between consecutive kernels inside the timed launch-list run ({lg.size} gaps): "
+                  f"median {np.median(lg):.2f} µs, mean {lg.mean():.2f} µs, max {lg.max():.2f} µs; the run "
+                  f"spans {(ends[b - 1] - starts[a]) / 1e3 / K:.2f} µs per layer from the first kernel's start "
+                  f"to the last kernel's end.  Kernel tracing intercepts every hipLaunchKernel, which slows the "
+                  f"host's issue of the list's launches below the GPU's pace (bench.py under the profiler: "
+                  f"{bt['us_per_layer']:.2f} µs per layer from the list, {bt['us_per_layer_graph']:.2f} from the "
+                  f"graphs); the graph's launches go out in one call.  The untraced figures are in the bench "
+                  f"record."]
+        gg = gaps_of(seg["graph"], K, lpg)
+        if gg.size:
             lines += ["", f"Gap between the end of one kernel and the start of the next inside the timed graph "
-                      f"replays ({gaps.size} gaps): median {np.median(gaps):.2f} µs, mean {gaps.mean():.2f} µs, "
-                      f"max {gaps.max():.2f} µs."]
-        # and inside the timed launch-list run (after a warm-up list of
-        # max(warmup, 1) layers)
-        a = nlay * nl + max(bt["warmup"], 1) * nl
-        b = a + bt["steps"] * nl
-        if len(g) >= b:
-            st = np.array([int(r["Start_Timestamp"]) for r in g[a:b]], dtype=np.float64)
-            en = np.array([int(r["End_Timestamp"]) for r in g[a:b]], dtype=np.float64)
-            lg = (st[1:] - en[:-1]) / 1e3
-            lines += ["", f"Gap between consecutive kernels inside the timed launch-list run ({lg.size} gaps): "
-                      f"median {np.median(lg):.2f} µs, mean {lg.mean():.2f} µs, max {lg.max():.2f} µs; the run "
-                      f"spans {(en[-1] - st[0]) / 1e3 / bt['steps']:.2f} µs per layer from the first kernel's start "
-                      f"to the last kernel's end."]
+                      f"replays ({gg.size} gaps): median {np.median(gg):.2f} µs, mean {gg.mean():.2f} µs, "
+                      f"max {gg.max():.2f} µs."]
     with open(out_path, "w") as f:
         f.write("\n".join(lines) + "\n")
     log(f"[bench] wrote {out_path}")
@@ -742,42 +750,29 @@ def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None, gro
     ms = MatrixSet(torch, fasq, problems, names, groups, min_copies=max(TIMING_COPIES, lpg))
     log(f"[bench] {wl_name}: {ms.bytes_per_set / 1e6:.1f} MB per layer, {ms.copies} copies, "
         f"{len(ms.groups)} launches, {lpg} layers per graph")
-    graphs = ms.capture_graphs(lpg)
-    for s in range(warmup):
-        graphs[s % ms.copies].replay()
-    torch.cuda.synchronize()
-    # The timed replays continue where the last warm-up graph stopped (it read
-    # copies w .. w + lpg - 1): every copy the timed loop reads was last read
-    # at least copies - 1 layers earlier, far more than the 256 MB MALL holds.
-    start = ((warmup - 1) % ms.copies + lpg) % ms.copies if warmup > 0 else 0
-    # Events on the replay stream beside the wall clock: their difference
-    # shows how much of the wall time is the host's launch of the graph.
+    graphs = ms.capture_graphs(lpg)  # launches every copy once, in order, before capturing
     stream = torch.cuda.current_stream()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    t0 = time.perf_counter()
-    ev0.record(stream)
-    for r in range(steps // lpg):
-        graphs[(start + r * lpg) % ms.copies].replay()
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    gpu_graph = ev0.elapsed_time(ev1) * 1e-3
-    del graphs
-    # The same layers queued from launch lists (fasq_launch_list_*): the
-    # launches recorded once through the same calls, then queued by the
-    # library with one hipLaunchKernel each, no HIP graph.  A warm-up list of
-    # max(warmup, 1) layers, then the timed list of `steps` layers, both on
-    # copies read at least copies - 1 layers earlier.
+    C = ms.copies
+    # Copies are read in order, cyclically, by everything below: each read of
+    # a copy comes C layers (at least 1 GiB) after its previous read, far more
+    # than the 256 MB MALL holds.  `nxt` is the next copy to read.
+    nxt = 0
+
     def record(first, count):
         lst = fasq.LaunchList()
         with lst:
             for k in range(count):
-                ms.launch_all((first + k) % ms.copies, stream.cuda_stream)
+                ms.launch_all((first + k) % C, stream.cuda_stream)
         return lst
 
+    # The timed region: launch lists (fasq_launch_list_*), the launches
+    # recorded once through the same calls, then queued by the library with
+    # one hipLaunchKernel each.  `warmup` layers from a warm-up list, then the
+    # timed list of `steps` layers.  Events on the stream beside the wall
+    # clock show how much of the wall time is the host's start of the run.
     lwarm = max(warmup, 1)
-    lstart = (start + steps) % ms.copies
-    warm_list, timed_list = record(lstart, lwarm), record(lstart + lwarm, steps)
+    warm_list, timed_list = record(nxt, lwarm), record(nxt + lwarm, steps)
+    nxt = (nxt + lwarm + steps) % C
     warm_list.run(stream)
     torch.cuda.synchronize()
     ev4, ev5 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -790,15 +785,34 @@ def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None, gro
     gpu_list = ev4.elapsed_time(ev5) * 1e-3
     warm_list.close()
     timed_list.close()
+    # The same layers from HIP graphs, reported beside it: graph c replays
+    # copies c .. c + lpg - 1; warm-up replays covering at least `warmup`
+    # layers, then steps / lpg timed replays.
+    gwarm = max(1, -(-warmup // lpg))
+    for r in range(gwarm):
+        graphs[(nxt + r * lpg) % C].replay()
+    nxt = (nxt + gwarm * lpg) % C
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for r in range(steps // lpg):
+        graphs[(nxt + r * lpg) % C].replay()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_graph = ev0.elapsed_time(ev1) * 1e-3
+    nxt = (nxt + steps) % C
+    del graphs
     # The same layers launched eagerly, back to back behind a spin kernel
     # (the host's launches run ahead of the GPU): the GPU time without the
     # graph, from events on the stream.  Reported beside the graph figure.
     ev2, ev3 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    eager_layers = min(steps, ms.copies)
+    eager_layers = min(steps, C)
     torch.cuda._sleep(SPACER_CYCLES * 4)
     ev2.record(stream)
     for k in range(eager_layers):
-        ms.launch_all((start + k) % ms.copies, stream.cuda_stream)
+        ms.launch_all((nxt + k) % C, stream.cuda_stream)
     ev3.record(stream)
     torch.cuda.synchronize()
     eager = ev2.elapsed_time(ev3) * 1e-3 / eager_layers
