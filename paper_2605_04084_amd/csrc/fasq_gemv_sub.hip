@@ -208,11 +208,23 @@ __global__ __launch_bounds__(kSubThreads) void k_gemv_sub(SubArgs a) {
   }
 }
 
-// y[m, n] = fp16(sum over segments, in segment order, of ws[ks][m][n])
+// y[m, n] = fp16(sum over segments, in segment order, of ws[ks][m][n]).
+// The partials are read kSumBatch at a time, every load issued before the
+// first add (a load inside the add loop would wait for each one in turn),
+// and added in segment order, so the sum keeps its order and its bits.
+constexpr int kSumBatch = 8;
 __global__ void k_sub_reduce(const float* __restrict__ ws, int64_t MN, int KS, half_t* __restrict__ y) {
   for (int64_t o = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; o < MN; o += (int64_t)gridDim.x * blockDim.x) {
     float s = 0.f;
-    for (int k = 0; k < KS; ++k) s += ws[(int64_t)k * MN + o];
+    for (int k0 = 0; k0 < KS; k0 += kSumBatch) {
+      float v[kSumBatch];
+#pragma unroll
+      for (int j = 0; j < kSumBatch; ++j)
+        if (k0 + j < KS) v[j] = ws[(int64_t)(k0 + j) * MN + o];
+#pragma unroll
+      for (int j = 0; j < kSumBatch; ++j)
+        if (k0 + j < KS) s += v[j];
+    }
     y[o] = static_cast<half_t>(s);
   }
 }
