@@ -66,6 +66,12 @@ struct GemvArgs {
 };
 
 constexpr int kGemvPipe = 8;      // load units per wave in the software pipeline
+// Floats between the partial sums of consecutive (row, token) pairs in the
+// 16-row-tile kernel's LDS buffer, which holds P per pair (one per wave of a
+// row).  An odd stride for P > 1: with a stride of P = 16 floats the 64
+// lanes of a wave that write one MFMA result (16 rows x 4 tokens) hit one
+// or two banks when M is even, and the final sum's reads hit one.
+__host__ __device__ constexpr int gemv_red_stride(int P) { return P > 1 ? P + 1 : 1; }
 constexpr int kGemvSlabPipe = 4;  // the same with x in slabs
 // Index loads each single-token wave keeps in flight.  Two per wave (32 KB
 // per CU at 16 waves) already saturate a CU's share of HBM; more only make
@@ -103,12 +109,13 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
 
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   uint8_t* xl = smem + a.cb_bytes;
-  float* red = reinterpret_cast<float*>(smem + a.cb_bytes + a.x_bytes);  // [RW][M][P]
+  float* red = reinterpret_cast<float*>(smem + a.cb_bytes + a.x_bytes);  // [RW][M][PS], P used of each PS
   const GemvPart& pt = a.part[blockIdx.y];  // the rows this workgroup works on
 
   const int wave = threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
   const int P = a.P;
+  const int PS = gemv_red_stride(P);
   const int Q = (blockDim.x / kWave) / P;
   const int p = wave % P;
   const int q = wave / P;
@@ -301,7 +308,7 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
             for (int k = 0; k < 4; ++k) {
               const int m = 4 * g + k;
               if (m < M) {
-                float* r = &red[(lrow * M + m) * P + p];
+                float* r = &red[(lrow * M + m) * PS + p];
                 *r = sb > 0 ? *r + (acc0[k] + acc1[k]) : acc0[k] + acc1[k];
               }
             }
@@ -314,16 +321,18 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
   }
   __syncthreads();
 
-  // fixed-order sum over the P waves, one fp16 rounding
+  // fixed-order sum over the P waves, one fp16 rounding; consecutive
+  // threads take consecutive (row, token) pairs, whose partials lie an odd
+  // stride apart in LDS
   const int RW = a.TW * 16;
   const int outs = RW * M;
   for (int o = threadIdx.x; o < outs; o += blockDim.x) {
-    const int m = o / RW;
-    const int r = o - m * RW;
+    const int r = o / M;
+    const int m = o - r * M;
     const int64_t n = ((int64_t)blockIdx.x + (int64_t)(r / 16) * gridDim.x) * 16 + (r & 15);
     if (n < pt.N) {
       float sum = 0.f;
-      const float* pr = red + (r * M + m) * P;
+      const float* pr = red + o * PS;
       for (int pp = 0; pp < P; ++pp) sum += pr[pp];
       pt.y[(int64_t)m * pt.ldy + n] = static_cast<half_t>(sum);
     }

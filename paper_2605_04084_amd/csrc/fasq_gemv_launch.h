@@ -194,6 +194,7 @@ hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev,
   if (T == 0) return hipErrorNotSupported;
   const int P = (int)(((CHS + 3) / 4 + T - 1) / T);
   const int Q = 16 / P;
+  const int PS = gemv_red_stride(P);  // floats per (row, token) pair of partials
   // lanes past the slab's (or the row's) last chunk column; slabbed x is
   // always read with the column checks (and never from registers)
   const bool mask = (int64_t)P * T * 4 != CHS || nslab > 1;
@@ -207,7 +208,7 @@ hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev,
   // The replicated table (up to 64 KB) gives way to one copy when it leaves
   // too little room beside x for one row group's partials.
   if (mode == CB_REPL &&
-      cb_lds_bytes(CB_REPL, maxC, d) + x_bytes + (int64_t)Q * 16 * p.M * P * 4 > dev.lds_per_block)
+      cb_lds_bytes(CB_REPL, maxC, d) + x_bytes + (int64_t)Q * 16 * p.M * PS * 4 > dev.lds_per_block)
     mode = CB_LDS;
   // A codebook too large for the LDS budget still goes to LDS when all of it
   // fits beside x and the partials of two row groups (one slice, one pass).
@@ -215,7 +216,7 @@ hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev,
   // gather-from-L2 kernel at M >= 4.
   int sl_shift = 0;
   if (mode == CB_GLOBAL && (maxC * d * 2) % 16 == 0) {
-    const int64_t red_min = 2 * (int64_t)Q * 16 * p.M * P * 4;
+    const int64_t red_min = 2 * (int64_t)Q * 16 * p.M * PS * 4;
     const int64_t room = dev.lds_per_block - x_bytes - (red_min > kSliceReserve ? red_min : kSliceReserve);
     while (sl_shift < 16 && (int64_t(2) << sl_shift) * d * 2 <= room) ++sl_shift;
     if ((int64_t(1) << sl_shift) * d * 2 >= kMinSliceBytes && (int64_t(1) << sl_shift) >= maxC) mode = CB_SLICE;
@@ -228,7 +229,7 @@ hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev,
   if (BITS == 16 && mode == CB_GLOBAL) {
     int64_t minC = maxC;
     for (int i = 0; i < count; ++i) minC = std::min(minC, ps[i].C);
-    const int64_t red_min = 2 * (int64_t)Q * 16 * p.M * P * 4;
+    const int64_t red_min = 2 * (int64_t)Q * 16 * p.M * PS * 4;
     const int64_t room = dev.lds_per_block - x_bytes - std::max<int64_t>(red_min, kSliceReserve);
     const int64_t per_word = 16 / (2 * d);  // entries per 16-byte word
     head = std::min(room / (2 * d), minC) / per_word * per_word;
@@ -254,14 +255,14 @@ hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev,
   if (nwg > (ntiles + Q - 1) / Q) nwg = (ntiles + Q - 1) / Q;
   int64_t tw = (ntiles + nwg - 1) / nwg;
   tw = (tw + Q - 1) / Q * Q;
-  const int64_t tw_max = avail / (16 * p.M * P * 4) / Q * Q;
+  const int64_t tw_max = avail / (16 * p.M * PS * 4) / Q * Q;
   if (tw_max < Q) return hipErrorNotSupported;
   if (tw > tw_max) {
     tw = tw_max;
     nwg = (ntiles + tw - 1) / tw;
   }
   if (nwg > 0x7fffffff || tw * 16 > 0x7fffffff) return hipErrorNotSupported;
-  const int lds = (int)(cb_bytes + x_bytes + tw * 16 * p.M * P * 4);
+  const int lds = (int)(cb_bytes + x_bytes + tw * 16 * p.M * PS * 4);
 
   GemvArgs a = {};
   a.x = static_cast<const half_t*>(p.x);
