@@ -204,8 +204,9 @@ bool gemm_plan(const Problem& p, const DeviceInfo& dev, GemmPlan* out) {
 // tokens on, when the decode kernel would have to stage x in slabs (rows of
 // x too long for LDS) and the GEMM splits K with its codebook in LDS.
 // Measured on the Llama-3-8B down_proj shape (4096 x 14336, d = 2, C = 256):
-// 12 tokens 31.3 us on the decode kernel against 26.1 us on the GEMM, 16
-// tokens 38.0 against 25.9 us; with x whole in LDS or registers, or a
+// 12 tokens 29.3 us on the decode kernel against 25.6 us on the GEMM, 16
+// tokens 35.7 against 26.5 us (8 tokens: 22.0 against 26.6); with x whole in
+// LDS or registers (gate_proj 16 tokens: 15.9 against 25.3 us), or a
 // codebook the GEMM has to gather from global memory (65536 entries), the
 // decode kernel is the faster one.
 bool decode_prefers_gemm(const Problem& p, const DeviceInfo& dev) {
