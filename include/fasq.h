@@ -193,7 +193,12 @@ fasq_status fasq_pq_gemm_lut(const void* x, int64_t M, int64_t K, int64_t N,
  * prefill GEMM split K as fasq_pq_gemm_ex does where the GEMM takes the call:
  * beyond 16 tokens, where no decode kernel applies, and, from 12 tokens on,
  * where the decode kernel would stage x in slabs and the GEMM keeps its
- * codebook in LDS (the measured crossover of Sec. 4.4's batch-size trade-off).
+ * codebook in LDS (the measured crossover of Sec. 4.4's batch-size trade-off);
+ * and it lets the decode kernel for 3 to 16 tokens split K over workgroups
+ * where the rows of x outweigh a workgroup's share of the ids (tall K, few
+ * rows: 2 to 8 segments, at most 4 MiB of fp32 partials, added in segment
+ * order by a second kernel; deterministic, though not the bits of the
+ * unsplit call).
  */
 fasq_status fasq_pq_gemv_ex(const void* x, int64_t M, int64_t K, int64_t N,
                             const void* idx, int idx_bits, int d,

@@ -138,7 +138,13 @@ fasq_status run(const Problem& p, Regime regime, hipStream_t stream, void* works
     // a decode call with a workspace goes to the GEMM where that is faster
     const bool to_gemm = regime == Regime::kGemv && workspace != nullptr && decode_prefers_gemm(p, dev) &&
                          workspace_bytes >= gemm_workspace_bytes(p, dev);
-    if (regime == Regime::kGemv && !to_gemm) e = launch_gemv(p, dev, stream);
+    if (regime == Regime::kGemv && !to_gemm) {
+      // the workspace also lets the 16-row-tile decode kernel split K
+      Problem q = p;
+      q.ws = workspace;
+      q.ws_bytes = workspace_bytes;
+      e = launch_gemv(q, dev, stream);
+    }
     if (e == hipErrorNotSupported) e = launch_gemm_mfma(p, dev, stream, workspace, workspace_bytes);
   }
   if (e == hipErrorNotSupported) e = launch_generic(p, stream);
@@ -312,11 +318,14 @@ int64_t fasq_pq_gemv_ex_workspace_bytes(int64_t M, int64_t K, int64_t N, int idx
   if (fasq::device_info(&dev) != hipSuccess) return -1;
   if (cb_stride != 0) return fasq::gemv_sub_workspace_bytes(p, dev);
   // one shared codebook: a workspace serves the GEMM when the decode kernels
-  // hand it the call, or when the GEMM with its K split is the faster one
-  if (std::strncmp(fasq_pq_plan(0, M, K, N, idx_bits, d, C), "k_gemm_mfma", 11) != 0 &&
-      !(fasq::decode_prefers_gemm(p, dev) && !fasq::force_generic()))
-    return 0;
-  return fasq::gemm_workspace_bytes(p, dev);
+  // hand it the call, or when the GEMM with its K split is the faster one,
+  // and the 16-row-tile decode kernel when it splits K
+  if (fasq::force_generic()) return 0;
+  const char* plan = fasq_pq_plan(0, M, K, N, idx_bits, d, C);
+  if (std::strncmp(plan, "k_gemm_mfma", 11) == 0 || fasq::decode_prefers_gemm(p, dev))
+    return fasq::gemm_workspace_bytes(p, dev);
+  if (std::strncmp(plan, "k_gemv<", 7) == 0) return fasq::gemv_split_workspace_bytes(p);
+  return 0;
 }
 
 fasq_status fasq_pq_gemv_ex(const void* x, int64_t M, int64_t K, int64_t N, const void* idx, int idx_bits, int d,

@@ -216,6 +216,11 @@ bool decode_prefers_gemm(const Problem& p, const DeviceInfo& dev) {
   return pl.ksplit > 1 && (pl.mode == CB_REPL || pl.mode == CB_HALF || pl.mode == CB_LDS);
 }
 
+int64_t gemv_split_workspace_bytes(const Problem& p) {
+  const GemvSplit sp = gemv_split_plan(p);
+  return sp.nseg > 1 ? (int64_t)sp.nseg * p.M * p.N * 4 : 0;
+}
+
 int64_t gemm_workspace_bytes(const Problem& p, const DeviceInfo& dev) {
   GemmPlan pl;
   if (!gemm_plan(p, dev, &pl) || pl.ksplit == 1) return 0;

@@ -44,6 +44,7 @@ struct GemvPart {
   int64_t ldy;         // elements between the outputs of consecutive tokens
   int C;
   int nsl;             // codebook slices; k_gemv takes one (the whole codebook)
+  int64_t ws_row;      // K split: the partials of the part's first row are at ws + ws_row
 };
 
 constexpr int kGemvMaxParts = 8;  // parts one k_gemv launch can take
@@ -62,6 +63,12 @@ struct GemvArgs {
   int x_bytes;   // LDS bytes of x (partials follow)
   int sl_shift;  // CB_SLICE: log2 of the entries of the one LDS slice (at least C)
   int head;      // CB_SPLIT: entries staged in LDS (the rest are read from global memory)
+  // K split over workgroups (gridDim.z segments of seg_slabs slabs each):
+  // segment z writes its fp32 partial of (token m, row n) to
+  // ws[(z * M + m) * ld_ws + part.ws_row + n]; one segment writes y itself.
+  int seg_slabs;
+  float* ws;
+  int64_t ld_ws;
   GemvPart part[kGemvMaxParts];
 };
 
@@ -143,7 +150,10 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
   const uint32_t lane_off0 = (uint32_t)(nl * a.R);
   const uint32_t tile_stride = (uint32_t)(16 * a.R);
   uint32_t buf[L][DW];
-  int c0 = 0, chs = CH;  // the slab: chunk columns [c0, c0 + chs)
+  // the slabs of this workgroup's K segment: [sb0, sb1)
+  const int sb0 = SLAB ? (int)blockIdx.z * a.seg_slabs : 0;
+  const int sb1 = SLAB ? (sb0 + a.seg_slabs < a.nslab ? sb0 + a.seg_slabs : a.nslab) : 1;
+  int c0 = sb0 * a.CHS, chs = CH;  // the slab: chunk columns [c0, c0 + chs)
   // byte offset of the lane's chunk in column t of the slab within its row,
   // or ~0 for columns past the slab (set per slab)
   uint32_t col_off[T];
@@ -199,8 +209,7 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
   };
 
 
-  const int nslab = SLAB ? a.nslab : 1;
-  chs = CH < a.CHS ? CH : a.CHS;
+  chs = CH - c0 < a.CHS ? CH - c0 : a.CHS;
   set_cols();
   {
     // codebook and the first slab of x (or x in registers)
@@ -244,8 +253,8 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
     __syncthreads();
   }
 
-  for (int sb = 0; sb < nslab; ++sb) {
-    if (sb > 0) {
+  for (int sb = sb0; sb < sb1; ++sb) {
+    if (sb > sb0) {
       // the next slab: every wave is done with the previous slab's x; its
       // first index loads go out, then x is staged in batches of
       // kXSlabBatch words per thread
@@ -309,7 +318,7 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
               const int m = 4 * g + k;
               if (m < M) {
                 float* r = &red[(lrow * M + m) * PS + p];
-                *r = sb > 0 ? *r + (acc0[k] + acc1[k]) : acc0[k] + acc1[k];
+                *r = sb > sb0 ? *r + (acc0[k] + acc1[k]) : acc0[k] + acc1[k];
               }
             }
             acc0 = float4_t{0.f, 0.f, 0.f, 0.f};
@@ -334,7 +343,8 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
       float sum = 0.f;
       const float* pr = red + o * PS;
       for (int pp = 0; pp < P; ++pp) sum += pr[pp];
-      pt.y[(int64_t)m * pt.ldy + n] = static_cast<half_t>(sum);
+      if (SLAB && gridDim.z > 1) a.ws[((int64_t)blockIdx.z * M + m) * a.ld_ws + pt.ws_row + n] = sum;
+      else pt.y[(int64_t)m * pt.ldy + n] = static_cast<half_t>(sum);
     }
   }
 }

@@ -139,6 +139,63 @@ inline bool gemv_x_in_regs(int64_t CH, int G, int d) {
   return P0 * T * 4 == CH && T * (G * d / 8) <= 8;
 }
 
+// K split of the 16-row-tile kernel over workgroups, for one matrix whose
+// M rows of x take more than kXSegBytes and do not go to registers, when the
+// caller gives a workspace: K is cut into 2, 4 or 8 segments (gridDim.z) of
+// whole chunk columns, each workgroup stages only its segment of x (whole)
+// for kXSegBytes or less of x per segment, and a second kernel adds the
+// segments' fp32 partials in segment order.  Each workgroup then stages a
+// fraction of x for the same ids, where without the split the x staging of a
+// workgroup outweighed its share of the index stream (tall K, few rows per
+// workgroup).  The partials take at most kGemvSplitMaxWs bytes.
+constexpr int64_t kXSegBytes = 64 * 1024;
+constexpr int kGemvMaxSegs = 8;
+constexpr int64_t kGemvSplitMaxWs = int64_t(4) << 20;
+
+struct GemvSplit {
+  int nseg = 1;      // K segments (1: no split)
+  int64_t chs = 0;   // chunk columns per segment
+};
+
+inline GemvSplit gemv_split_plan(const Problem& p) {
+  GemvSplit sp;
+  const int G = p.idx_bits == 8 ? 16 : 8;
+  if (p.cb_stride != 0 || p.M < 2 || p.M > 16 || p.S % G) return sp;
+  const int64_t CH = p.S / G;
+  if (gemv_x_in_regs(CH, G, p.d)) return sp;
+  const int64_t XCB = (int64_t)G * p.d * 2;
+  const int64_t x_total = p.M * CH * XCB;
+  if (x_total <= kXSegBytes) return sp;
+  int ks = 2;
+  while (ks < kGemvMaxSegs && x_total / ks > kXSegBytes) ks *= 2;
+  const int64_t chs = ((CH + ks - 1) / ks + 3) / 4 * 4;
+  const int nseg = (int)((CH + chs - 1) / chs);
+  const int T = gemv_pick_t(chs);
+  if (nseg < 2 || T == 0 || T > 4 || p.M * (chs * XCB + 16) > kXWholeBytes) return sp;
+  if ((int64_t)nseg * p.M * p.N * 4 > kGemvSplitMaxWs) return sp;
+  sp.nseg = nseg;
+  sp.chs = chs;
+  return sp;
+}
+
+namespace {
+// y[o] = fp16(sum over the K segments, in segment order, of ws[seg][o]);
+// every partial is loaded before the first add.
+__global__ void k_gemv_seg_sum(const float* __restrict__ ws, int64_t MN, int nseg, half_t* __restrict__ y) {
+  for (int64_t o = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; o < MN; o += (int64_t)gridDim.x * blockDim.x) {
+    float v[kGemvMaxSegs];
+#pragma unroll
+    for (int k = 0; k < kGemvMaxSegs; ++k)
+      if (k < nseg) v[k] = ws[(int64_t)k * MN + o];
+    float s = 0.f;
+#pragma unroll
+    for (int k = 0; k < kGemvMaxSegs; ++k)
+      if (k < nseg) s += v[k];
+    y[o] = static_cast<half_t>(s);
+  }
+}
+}  // namespace
+
 inline bool gemv_x_slabbed(const Problem& p) {
   const int G = p.idx_bits == 8 ? 16 : 8;
   if (p.S % G) return false;
@@ -182,7 +239,17 @@ hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev,
   // x in registers (whole rows, no masked columns) needs no LDS
   const bool x_in_regs = gemv_x_in_regs(CH, G, d);
   int64_t CHS = CH;  // chunk columns per x slab
-  if (!x_in_regs && p.M * (CH * XCB + 16) > kXWholeBytes) {
+  // K split over workgroups with a caller workspace (one matrix): each
+  // segment is one slab
+  int nseg = 1;
+  if (count == 1 && p.ws != nullptr && !(reinterpret_cast<uintptr_t>(p.ws) & 3)) {
+    const GemvSplit sp = gemv_split_plan(p);
+    if (sp.nseg > 1 && p.ws_bytes >= (int64_t)sp.nseg * p.M * p.N * 4) {
+      nseg = sp.nseg;
+      CHS = sp.chs;
+    }
+  }
+  if (nseg == 1 && !x_in_regs && p.M * (CH * XCB + 16) > kXWholeBytes) {
     // at most 64 chunk columns of each K group per slab (T <= 4)
     const int64_t cmax = std::min<int64_t>(((kXSlabBytes / p.M - 16) / XCB) / 4 * 4, 256);
     if (cmax < 4) return hipErrorNotSupported;
@@ -251,7 +318,7 @@ hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev,
   const int nparts = choose_part_cuts(tiles_of, count, dev.num_cus, kGemvMaxParts, cuts);
   int64_t ntiles = 0;  // tiles of the largest part
   for (int i = 0; i < count; ++i) ntiles = std::max(ntiles, (tiles_of[i] + cuts[i] - 1) / cuts[i]);
-  int64_t nwg = std::max<int64_t>(dev.num_cus / nparts, 1);
+  int64_t nwg = std::max<int64_t>(dev.num_cus / (nparts * nseg), 1);
   if (nwg > (ntiles + Q - 1) / Q) nwg = (ntiles + Q - 1) / Q;
   int64_t tw = (ntiles + nwg - 1) / nwg;
   tw = (tw + Q - 1) / Q * Q;
@@ -279,6 +346,9 @@ hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev,
   a.x_bytes = (int)x_bytes;
   a.sl_shift = sl_shift;
   a.head = (int)head;
+  a.seg_slabs = nseg > 1 ? 1 : nslab;
+  a.ws = nseg > 1 ? static_cast<float*>(p.ws) : nullptr;
+  a.ld_ws = p.N;
   int k = 0;
   for (int i = 0; i < count; ++i) {
     const int64_t base = tiles_of[i] / cuts[i], extra = tiles_of[i] % cuts[i];
@@ -293,16 +363,23 @@ hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev,
       pt.ldy = ps[i].N;
       pt.C = (int)ps[i].C;
       pt.nsl = 1;
+      pt.ws_row = row;
       row += rows;
     }
   }
-  const dim3 grid((unsigned)nwg, (unsigned)nparts);
+  const dim3 grid((unsigned)nwg, (unsigned)nparts, (unsigned)nseg);
+  hipError_t e;
   switch (d) {
-    case 1: return launch_gemv_mode<BITS, MR, 1>(a, mode, T, mask, threads, grid, lds, stream);
-    case 2: return launch_gemv_mode<BITS, MR, 2>(a, mode, T, mask, threads, grid, lds, stream);
-    case 4: return launch_gemv_mode<BITS, MR, 4>(a, mode, T, mask, threads, grid, lds, stream);
-    default: return launch_gemv_mode<BITS, MR, 8>(a, mode, T, mask, threads, grid, lds, stream);
+    case 1: e = launch_gemv_mode<BITS, MR, 1>(a, mode, T, mask, threads, grid, lds, stream); break;
+    case 2: e = launch_gemv_mode<BITS, MR, 2>(a, mode, T, mask, threads, grid, lds, stream); break;
+    case 4: e = launch_gemv_mode<BITS, MR, 4>(a, mode, T, mask, threads, grid, lds, stream); break;
+    default: e = launch_gemv_mode<BITS, MR, 8>(a, mode, T, mask, threads, grid, lds, stream); break;
   }
+  if (e != hipSuccess || nseg == 1 || plan().active) return e;
+  const int64_t mn = p.M * p.N;
+  const int64_t rblocks = (mn + 255) / 256;
+  return launch_kernel(k_gemv_seg_sum, dim3((unsigned)(rblocks < 65536 ? rblocks : 65536)), dim3(256), 0, stream,
+                       static_cast<const float*>(p.ws), mn, nseg, static_cast<half_t*>(p.y));
 }
 
 }  // namespace fasq

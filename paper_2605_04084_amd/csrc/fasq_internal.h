@@ -27,6 +27,10 @@ struct Problem {
   int64_t S;  // sub-vectors per row, K / d
   int64_t R;  // bytes per packed index row
   int64_t cb_stride = 0;  // 0: one shared codebook; C * d: codebook s of subspace s at codebook + s * C * d
+  // caller scratch the 16-row-tile decode kernel may split K with (fp32
+  // partials; nullptr: no split)
+  void* ws = nullptr;
+  int64_t ws_bytes = 0;
 };
 
 // Properties of the current device, read once per device and cached.
@@ -69,6 +73,9 @@ bool gemv_x_slabbed(const Problem& p);
 // with its K split (the measured crossover); see fasq_gemm.hip.
 constexpr int kGemmFromTokens = 12;
 bool decode_prefers_gemm(const Problem& p, const DeviceInfo& dev);
+// Workspace bytes with which the 16-row-tile decode kernel splits K over
+// workgroups for p (one matrix; 0 when it would not split).
+int64_t gemv_split_workspace_bytes(const Problem& p);
 
 // The paper's lookup-table GEMM (Alg. 3), kept for comparison with the MFMA
 // GEMM.  hipErrorNotSupported when its tables do not fit in LDS.

@@ -807,8 +807,36 @@ def test_decode_with_workspace_takes_the_gemm_past_the_crossover(case):
 
 
 def test_decode_with_workspace_keeps_the_decode_kernel_elsewhere():
-    # x whole in registers (q_proj rows at 16 tokens), and a codebook the GEMM
-    # would gather from global memory (Qwen3-8B down_proj rows at 16 tokens)
+    # x whole in registers (q_proj rows at 16 tokens): no workspace
     assert fasq.gemv_ex_workspace_bytes(16, 4096, 4096, 8, 2, 256, 0) == 0
-    assert fasq.gemv_ex_workspace_bytes(16, 12288, 4096, 16, 4, 65536, 0) == 0
-    assert fasq.gemv_ex_workspace_bytes(8, 14336, 4096, 8, 2, 256, 0) == 0   # below 12 tokens
+    # a codebook the GEMM would gather from global memory (Qwen3-8B down_proj
+    # rows at 16 tokens), and below 12 tokens (down_proj rows at 8): the decode
+    # kernel, which splits K with the workspace (8 and 4 segments)
+    for (M, K, N, bits, d, C), nseg in (((16, 12288, 4096, 16, 4, 65536), 8), ((8, 14336, 4096, 8, 2, 256), 4)):
+        assert fasq.plan("gemv", M, K, N, bits, d, C).startswith("k_gemv<")
+        assert fasq.gemv_ex_workspace_bytes(M, K, N, bits, d, C, 0) == nseg * M * N * 4
+
+
+@pytest.mark.parametrize("case", [(3, 14336, 333, 2, 256, 8), (4, 14336, 1000, 2, 256, 8),
+                                  (8, 14336, 4096, 2, 256, 8), (5, 14336, 130, 4, 4096, 12),
+                                  (16, 12288, 700, 4, 65536, 16), (4, 12288, 4096, 4, 65536, 16)])
+def test_decode_k_split_with_workspace(case):
+    """Where x outweighs a workgroup's share of the ids, fasq_pq_gemv_ex's
+    workspace lets the 16-row-tile decode kernel split K over workgroups.
+    Every output is written, matches the oracle, and repeats bit for bit;
+    fasq_pq_gemv (no workspace) keeps the unsplit kernel."""
+    M, K, N, d, C, bits = case
+    print(f"[case] decode K split {case}", flush=True)
+    need = fasq.gemv_ex_workspace_bytes(M, K, N, bits, d, C, 0)
+    assert need > 0 and need % (M * N * 4) == 0 and 2 <= need // (M * N * 4) <= 8, need
+    rng = np.random.default_rng(97 + sum(case))
+    p = pi.draw_problem(rng, M, K, N, d, C, bits)
+    ws = torch.full((need,), 0xFF, dtype=torch.uint8, device="cuda:0")  # NaN partials before the call
+    xd, idd, cbd = to_dev(p.x), to_dev(p.idx), to_dev(p.codebook)
+    y1 = to_np(fasq.pq_gemv_ex(xd, idd, bits, d, cbd, workspace=ws))
+    y2 = to_np(fasq.pq_gemv_ex(xd, idd, bits, d, cbd, workspace=ws))
+    assert np.isfinite(y1).all()
+    assert np.array_equal(y1.view(np.uint16), y2.view(np.uint16))
+    ref = orc.pq_linear(p.x, p.idx, bits, d, p.codebook)
+    assert_close(y1.astype(np.float64), ref, f"gemv_ex decode K split {case}")
+    assert_close(run("gemv", p), ref, f"gemv without the split {case}")

@@ -173,6 +173,26 @@ def test_gemm_k_split(case, kind):
 
 
 @pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("case", [(4, 14336, 300, 2, 256, 8), (8, 14336, 140, 4, 4096, 12),
+                                  (16, 12288, 100, 4, 65536, 16)])
+def test_gemv_k_split(case, kind):
+    """fasq_pq_gemv_ex with one shared codebook where the 16-row-tile decode
+    kernel splits K over workgroups (each stages its segment of x; fp32
+    partials in the workspace, then the fixed-order sum)."""
+    M, K, N, d, C, bits = case
+    label = f"gemv_ex decode K split {case} {kind}"
+    print(f"[case] {label}", flush=True)
+    assert fasq.plan("gemv", M, K, N, bits, d, C).startswith("k_gemv<"), label
+    need = fasq.gemv_ex_workspace_bytes(M, K, N, bits, d, C, 0)
+    assert need > 0 and need % (M * N * 4) == 0 and need // (M * N * 4) >= 2, (label, need)
+    x, cb, ids = draw(kind, M, K, N, d, C, seed=sum(case) + 5)
+    idx = pi.pack_indices(ids, bits)
+    ws = torch.zeros(need, dtype=torch.uint8, device="cuda:0")
+    y = to_np(fasq.pq_gemv_ex(to_dev(x), to_dev(idx), bits, d, to_dev(cb), workspace=ws))
+    check_exact(y, orc.pq_linear(x, idx, bits, d, cb), kind, label)
+
+
+@pytest.mark.parametrize("kind", KINDS)
 @pytest.mark.parametrize("case", [(1, 4096, 300, 2, 256, 8), (1, 768, 70, 4, 1024, 12),
                                   (4, 1024, 300, 2, 256, 8), (16, 768, 70, 4, 1024, 12)])
 def test_per_subspace_books(case, kind):
