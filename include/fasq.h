@@ -217,7 +217,8 @@ int64_t fasq_pq_gemv_ex_workspace_bytes(int64_t M, int64_t K, int64_t N, int idx
  * HIP graph capture, tight serving loops, harnesses that forbid allocation).
  * Same operation, arguments (minus the workspace), layouts and results as
  * fasq_pq_gemv_ex: the scratch that call would take from a caller workspace
- * (the per-subspace K split, or the K split of the GEMM fallback) comes from
+ * (the per-subspace K split, the decode kernel's K split, or the K split of
+ * the GEMM fallback) comes from
  * a static device array the library holds on every GPU it runs on, of
  * fasq_noalloc_scratch_bytes() = FASQ_NOALLOC_SCRATCH_BYTES bytes, kept until
  * the process ends.  The call allocates nothing: no hipMalloc, no allocating

@@ -75,6 +75,8 @@ CASES = [
      (8, 2048, 1000, 2, 256, 8), (3, 1024, 300, 2, 256, 8)),
     ("shared codebook, GEMM fallback with K split", False,
      (20, 2048, 300, 4, 256, 8), (17, 1024, 100, 4, 256, 8)),
+    ("shared codebook, decode kernel splitting K", False,
+     (8, 14336, 700, 2, 256, 8), (4, 14336, 300, 2, 256, 8)),
     ("shared codebook, decode kernel (no scratch)", False,
      (1, 4096, 1024, 2, 256, 8), (1, 512, 64, 2, 256, 8)),
 ]
