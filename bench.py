@@ -769,15 +769,17 @@ def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None, gro
     # recorded once through the same calls, then queued by the library with
     # one hipLaunchKernel each.  `warmup` layers from a warm-up list, then the
     # timed list of `steps` layers.  Events on the stream beside the wall
-    # clock show how much of the wall time is the host's start of the run.
+    # clock show how much of the wall time is the host's start of the run;
+    # the first is recorded just before the clock starts (it queues no work
+    # and its host call is not part of a step).
     lwarm = max(warmup, 1)
     warm_list, timed_list = record(nxt, lwarm), record(nxt + lwarm, steps)
     nxt = (nxt + lwarm + steps) % C
     warm_list.run(stream)
     torch.cuda.synchronize()
     ev4, ev5 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    t0 = time.perf_counter()
     ev4.record(stream)
+    t0 = time.perf_counter()
     timed_list.run(stream)
     ev5.record(stream)
     torch.cuda.synchronize()
@@ -794,8 +796,8 @@ def decode_layer(torch, fasq, pi, wl_name, steps, warmup, M=1, include=None, gro
     nxt = (nxt + gwarm * lpg) % C
     torch.cuda.synchronize()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    t0 = time.perf_counter()
     ev0.record(stream)
+    t0 = time.perf_counter()
     for r in range(steps // lpg):
         graphs[(nxt + r * lpg) % C].replay()
     ev1.record(stream)

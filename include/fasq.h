@@ -332,7 +332,10 @@ int64_t fasq_pq_encode_workspace_bytes(int64_t N, int64_t K, int d, int64_t C);
  *   fasq_launch_list_size     launches recorded, -1 for a NULL list.
  *   fasq_launch_list_destroy  free the list (and stop recording into it on the
  *                             calling thread); NULL is ignored.  Launches
- *                             already queued are not affected.
+ *                             already queued are not affected.  No other
+ *                             thread may record into the list, or run it,
+ *                             while it is destroyed, and no thread may
+ *                             record into a list that another thread runs.
  */
 typedef struct fasq_launch_list fasq_launch_list;
 fasq_status fasq_launch_list_create(fasq_launch_list** list);
