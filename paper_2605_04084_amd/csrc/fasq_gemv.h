@@ -69,6 +69,11 @@ struct GemvArgs {
   int seg_slabs;
   float* ws;
   int64_t ld_ws;
+  // 1 (K split, one slab per segment, many tokens): the partials of each
+  // round of tiles (tile j of every row group) are summed and written as soon
+  // as the round is done, so LDS holds one round's partials instead of every
+  // tile's
+  int round_sum;
   GemvPart part[kGemvMaxParts];
 };
 
@@ -253,6 +258,28 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
     __syncthreads();
   }
 
+  const bool rounds = SLAB && a.round_sum != 0;
+  // fixed-order sum over the P waves of the partials of the workgroup's
+  // local rows [r0, r0 + nr) (LDS rows from lr0), one fp16 rounding, or one
+  // fp32 partial of this K segment; consecutive threads take consecutive
+  // (row, token) pairs, whose partials lie an odd stride apart in LDS
+  auto sum_rows = [&](int r0, int lr0, int nr) {
+    const int outs = nr * M;
+    for (int o = threadIdx.x; o < outs; o += blockDim.x) {
+      const int rr = o / M;
+      const int m = o - rr * M;
+      const int r = r0 + rr;
+      const int64_t n = ((int64_t)blockIdx.x + (int64_t)(r / 16) * gridDim.x) * 16 + (r & 15);
+      if (n < pt.N) {
+        float sum = 0.f;
+        const float* pr = red + ((lr0 + rr) * M + m) * PS;
+        for (int pp = 0; pp < P; ++pp) sum += pr[pp];
+        if (SLAB && gridDim.z > 1) a.ws[((int64_t)blockIdx.z * M + m) * a.ld_ws + pt.ws_row + n] = sum;
+        else pt.y[(int64_t)m * pt.ldy + n] = static_cast<half_t>(sum);
+      }
+    }
+  };
+
   for (int sb = sb0; sb < sb1; ++sb) {
     if (sb > sb0) {
       // the next slab: every wave is done with the previous slab's x; its
@@ -312,7 +339,7 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
           if (t == T - 1) {
             // lane l holds rows m = 4g .. 4g + 3 of column nl of the 16 x 16
             // tile; the slabs of a row are summed in slab order by this lane
-            const int lrow = ((u / T) * Q + q) * 16 + nl;
+            const int lrow = ((rounds ? 0 : u / T) * Q + q) * 16 + nl;
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
               const int m = 4 * g + k;
@@ -325,28 +352,20 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
             acc1 = float4_t{0.f, 0.f, 0.f, 0.f};
           }
         }
+        // a round of tiles done (the condition is the same in every wave:
+        // all waves have the same units): sum it while the next round's
+        // loads are in flight
+        if (rounds && t == T - 1 && u < nunits) {
+          __syncthreads();
+          sum_rows((u / T) * Q * 16, 0, Q * 16);
+          __syncthreads();
+        }
       }
     }
   }
+  if (rounds) return;
   __syncthreads();
-
-  // fixed-order sum over the P waves, one fp16 rounding; consecutive
-  // threads take consecutive (row, token) pairs, whose partials lie an odd
-  // stride apart in LDS
-  const int RW = a.TW * 16;
-  const int outs = RW * M;
-  for (int o = threadIdx.x; o < outs; o += blockDim.x) {
-    const int r = o / M;
-    const int m = o - r * M;
-    const int64_t n = ((int64_t)blockIdx.x + (int64_t)(r / 16) * gridDim.x) * 16 + (r & 15);
-    if (n < pt.N) {
-      float sum = 0.f;
-      const float* pr = red + o * PS;
-      for (int pp = 0; pp < P; ++pp) sum += pr[pp];
-      if (SLAB && gridDim.z > 1) a.ws[((int64_t)blockIdx.z * M + m) * a.ld_ws + pt.ws_row + n] = sum;
-      else pt.y[(int64_t)m * pt.ldy + n] = static_cast<half_t>(sum);
-    }
-  }
+  sum_rows(0, 0, a.TW * 16);
 }
 
 }  // namespace fasq

@@ -151,6 +151,15 @@ inline bool gemv_x_in_regs(int64_t CH, int G, int d) {
 constexpr int64_t kXSegBytes = 64 * 1024;
 constexpr int kGemvMaxSegs = 8;
 constexpr int64_t kGemvSplitMaxWs = int64_t(4) << 20;
+// From this many tokens on, a split launch sums each round of tiles as soon
+// as it is done (two barriers per round) and keeps one workgroup per CU;
+// below it, the partials of all the workgroup's tiles wait in LDS and the
+// LDS they take caps the tiles per workgroup.  Measured (same box,
+// alternating builds): down_proj 4096 x 14336 at 4 / 8 / 11 tokens 15.1 /
+// 15.8 / 24.5 us without the rounds against 16.2 / 18.4 / 23.1 us with
+// them; Qwen3-8B down_proj (4096 x 12288, 65536-entry codebook) at 4 / 16
+// tokens 51.0 / 64.7 against 52.1 / 58.2 us.
+constexpr int kRoundSumFromTokens = 11;
 
 struct GemvSplit {
   int nseg = 1;      // K segments (1: no split)
@@ -322,14 +331,17 @@ hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev,
   if (nwg > (ntiles + Q - 1) / Q) nwg = (ntiles + Q - 1) / Q;
   int64_t tw = (ntiles + nwg - 1) / nwg;
   tw = (tw + Q - 1) / Q * Q;
-  const int64_t tw_max = avail / (16 * p.M * PS * 4) / Q * Q;
+  // summing by rounds, LDS holds one round of Q tiles' partials at a time
+  const bool rounds = nseg > 1 && p.M >= kRoundSumFromTokens;
+  const int64_t tw_max = rounds ? (avail >= Q * 16 * p.M * PS * 4 ? tw : 0)
+                                : avail / (16 * p.M * PS * 4) / Q * Q;
   if (tw_max < Q) return hipErrorNotSupported;
   if (tw > tw_max) {
     tw = tw_max;
     nwg = (ntiles + tw - 1) / tw;
   }
   if (nwg > 0x7fffffff || tw * 16 > 0x7fffffff) return hipErrorNotSupported;
-  const int lds = (int)(cb_bytes + x_bytes + tw * 16 * p.M * PS * 4);
+  const int lds = (int)(cb_bytes + x_bytes + (rounds ? Q : tw) * 16 * p.M * PS * 4);
 
   GemvArgs a = {};
   a.x = static_cast<const half_t*>(p.x);
@@ -349,6 +361,7 @@ hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev,
   a.seg_slabs = nseg > 1 ? 1 : nslab;
   a.ws = nseg > 1 ? static_cast<float*>(p.ws) : nullptr;
   a.ld_ws = p.N;
+  a.round_sum = rounds ? 1 : 0;
   int k = 0;
   for (int i = 0; i < count; ++i) {
     const int64_t base = tiles_of[i] / cuts[i], extra = tiles_of[i] % cuts[i];

@@ -820,7 +820,8 @@ def test_decode_with_workspace_keeps_the_decode_kernel_elsewhere():
 @pytest.mark.parametrize("case", [(3, 14336, 333, 2, 256, 8), (4, 14336, 1000, 2, 256, 8),
                                   (8, 14336, 4096, 2, 256, 8), (5, 14336, 130, 4, 4096, 12),
                                   (16, 12288, 700, 4, 65536, 16), (4, 12288, 4096, 4, 65536, 16),
-                                  (4, 12288, 500, 4, 8192, 16), (7, 8192, 257, 1, 256, 8)])
+                                  (4, 12288, 500, 4, 8192, 16), (7, 8192, 257, 1, 256, 8),
+                                  (11, 14336, 500, 2, 256, 8), (12, 12288, 333, 4, 65536, 16)])
 def test_decode_k_split_with_workspace(case):
     """Where x outweighs a workgroup's share of the ids, fasq_pq_gemv_ex's
     workspace lets the 16-row-tile decode kernel split K over workgroups.

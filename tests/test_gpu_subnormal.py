@@ -174,7 +174,7 @@ def test_gemm_k_split(case, kind):
 
 @pytest.mark.parametrize("kind", KINDS)
 @pytest.mark.parametrize("case", [(4, 14336, 300, 2, 256, 8), (8, 14336, 140, 4, 4096, 12),
-                                  (16, 12288, 100, 4, 65536, 16)])
+                                  (11, 14336, 200, 2, 256, 8), (16, 12288, 100, 4, 65536, 16)])
 def test_gemv_k_split(case, kind):
     """fasq_pq_gemv_ex with one shared codebook where the 16-row-tile decode
     kernel splits K over workgroups (each stages its segment of x; fp32
