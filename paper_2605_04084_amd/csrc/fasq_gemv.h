@@ -69,10 +69,10 @@ struct GemvArgs {
   int seg_slabs;
   float* ws;
   int64_t ld_ws;
-  // 1 (K split, one slab per segment, many tokens): the partials of each
-  // round of tiles (tile j of every row group) are summed and written as soon
-  // as the round is done, so LDS holds one round's partials instead of every
-  // tile's
+  // 1 (K split with one slab per segment and many tokens, or a codebook head
+  // in LDS): the partials of each round of tiles (tile j of every row group)
+  // are summed and written as soon as the round is done, so LDS holds one
+  // round's partials instead of every tile's
   int round_sum;
   GemvPart part[kGemvMaxParts];
 };
@@ -258,7 +258,7 @@ __global__ __launch_bounds__(1024) void k_gemv(GemvArgs a) {
     __syncthreads();
   }
 
-  const bool rounds = SLAB && a.round_sum != 0;
+  const bool rounds = (SLAB || MODE == CB_SPLIT) && a.round_sum != 0;
   // fixed-order sum over the P waves of the partials of the workgroup's
   // local rows [r0, r0 + nr) (LDS rows from lr0), one fp16 rounding, or one
   // fp32 partial of this K segment; consecutive threads take consecutive

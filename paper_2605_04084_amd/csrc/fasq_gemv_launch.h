@@ -160,6 +160,13 @@ constexpr int64_t kGemvSplitMaxWs = int64_t(4) << 20;
 // them; Qwen3-8B down_proj (4096 x 12288, 65536-entry codebook) at 4 / 16
 // tokens 51.0 / 64.7 against 52.1 / 58.2 us.
 constexpr int kRoundSumFromTokens = 11;
+// The same rounds for a codebook whose head is in LDS and the rest read from
+// global memory (CB_SPLIT), from this many tokens on: the head takes most of
+// LDS, so with the partials of all its tiles a workgroup could hold one or
+// two tiles, and every CU restaged the head for each of several workgroups.
+// Qwen3-8B layer (kernel sum) at 4 / 16 tokens: 193.9 / 211.5 against
+// 190.4 / 205.9 us with the rounds (same box, alternating builds).
+constexpr int kRoundHeadFromTokens = 4;
 
 struct GemvSplit {
   int nseg = 1;      // K segments (1: no split)
@@ -332,7 +339,7 @@ hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev,
   int64_t tw = (ntiles + nwg - 1) / nwg;
   tw = (tw + Q - 1) / Q * Q;
   // summing by rounds, LDS holds one round of Q tiles' partials at a time
-  const bool rounds = nseg > 1 && p.M >= kRoundSumFromTokens;
+  const bool rounds = (nseg > 1 && p.M >= kRoundSumFromTokens) || (mode == CB_SPLIT && p.M >= kRoundHeadFromTokens);
   const int64_t tw_max = rounds ? (avail >= Q * 16 * p.M * PS * 4 ? tw : 0)
                                 : avail / (16 * p.M * PS * 4) / Q * Q;
   if (tw_max < Q) return hipErrorNotSupported;
