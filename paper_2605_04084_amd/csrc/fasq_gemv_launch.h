@@ -312,7 +312,9 @@ hipError_t launch_gemv_bits(const Problem* ps, int count, const DeviceInfo& dev,
   if (BITS == 16 && mode == CB_GLOBAL) {
     int64_t minC = maxC;
     for (int i = 0; i < count; ++i) minC = std::min(minC, ps[i].C);
-    const int64_t red_min = 2 * (int64_t)Q * 16 * p.M * PS * 4;
+    // the partials of one round of tiles beside the head when the launch
+    // sums by rounds (below), else of two
+    const int64_t red_min = (p.M >= kRoundHeadFromTokens ? 1 : 2) * (int64_t)Q * 16 * p.M * PS * 4;
     const int64_t room = dev.lds_per_block - x_bytes - std::max<int64_t>(red_min, kSliceReserve);
     const int64_t per_word = 16 / (2 * d);  // entries per 16-byte word
     head = std::min(room / (2 * d), minC) / per_word * per_word;
