@@ -507,7 +507,11 @@ __device__ __forceinline__ void gemv_rows_body(const GemvM1Args& a) {
   // ---- prologue (see k_gemv): codebook and x first, then the index stream.
   // CB_SLICE repeats everything from the codebook staging to the end of the
   // row loop once per slice; x is staged once.
-  constexpr int XWT = 2;
+  // x words each thread loads before the staging barrier: two per token
+  // cover the longest rows here (K = 14336 on 14 waves).  Words past them are
+  // loaded after the early index loads, one more round trip before the
+  // barrier.
+  constexpr int XWT = 2 * MT;
   const int xw_total = (int)(a.K / 8) * a.M;  // 16-byte words of x
   const int xw_slots = (int)(a.K / 8) * MT;   // LDS words of x (token slots past M hold zeros)
   const uint32_t xtok = (uint32_t)a.K * 2;    // LDS bytes between tokens
