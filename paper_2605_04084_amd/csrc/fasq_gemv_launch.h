@@ -14,6 +14,7 @@ constexpr int kSliceReserve = 8 * 1024;        // LDS kept for row partials besi
 constexpr int kMinSliceBytes = 32 * 1024;      // smaller slices: gather from global memory instead
 constexpr int kReplMinIdsPerEntry = 16;        // replicate the codebook only above this many ids per workgroup and entry
 constexpr int64_t kMtWideXMinRows = 64;        // two tokens: rows per CU from which x takes twice the registers
+constexpr int64_t kM1TwoWgReplMinRows = 64;    // one token, replicated table: rows per CU from which two workgroups share a CU
 static_assert(kMaxBatchLaunch <= kM1MaxParts && kMaxBatchLaunch <= kGemvMaxParts,
               "a grouped launch needs a part per matrix at least");
 
@@ -537,13 +538,26 @@ hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& d
     for (int i = 0; i < count; ++i)
       if ((ps[i].C * d * 2) % 16 != 0) return hipErrorNotSupported;
   const int cb_bytes = mode == CB_SLICE ? (int)((int64_t(1) << sl_shift) * d * 2) : (int)cb_lds_bytes(mode, maxC, d);
-  const int64_t avail = dev.lds_per_block - cb_bytes - x_bytes;
+  // Workgroup slots per CU: two workgroups of at most 8 waves when a wave
+  // owns whole rows (P = 1) and two workgroups' LDS fits side by side, unless
+  // few rows per CU meet the replicated table (two stagings of it per CU would
+  // then cost more than the second workgroup hides); else one of up to 16.
+  // Measured on the Llama-3-8B layers against one workgroup per CU: gate+up
+  // 12.07 against 12.37 us at 4 bits, q+k+v 6.43 against 6.67 and gate+up
+  // 11.95 against 12.17 at 3 bits; slower on the 4-bit q+k+v and o_proj
+  // (6.10 against 5.55 and 5.05 against 4.68, 24 and 16 rows per CU) and on
+  // the 3-bit down_proj (P = 7: 9.50 against 8.75).
+  const int wgcu = P == 1 && 2 * (cb_bytes + x_bytes) < dev.lds_per_block &&
+                           (mode != CB_REPL || rows_per_cu >= kM1TwoWgReplMinRows)
+                       ? 2
+                       : 1;
+  const int64_t avail = dev.lds_per_block / wgcu - cb_bytes - x_bytes;
 
-  // Q row groups per workgroup: enough workgroups to cover every CU for
-  // small N, up to 16 waves per workgroup.
-  const int64_t ncu = dev.num_cus;
+  // Q row groups per workgroup: enough workgroups to cover every slot for
+  // small N, up to 16 waves per CU.
+  const int64_t ncu = (int64_t)dev.num_cus * wgcu;
   int64_t Q = (total_rows + ncu - 1) / ncu;
-  if (Q > 16 / P) Q = 16 / P;
+  if (Q > 16 / wgcu / P) Q = 16 / wgcu / P;
   if (Q < 1) Q = 1;
 
   // Parts: matrix i is cut into best[i] ranges of near-equal row counts, and
