@@ -512,9 +512,24 @@ __device__ __forceinline__ void gemv_rows_body(const GemvM1Args& a) {
   // loaded after the early index loads, one more round trip before the
   // barrier.
   constexpr int XWT = 2 * MT;
-  const int xw_total = (int)(a.K / 8) * a.M;  // 16-byte words of x
-  const int xw_slots = (int)(a.K / 8) * MT;   // LDS words of x (token slots past M hold zeros)
+  const int xw_tok = (int)(a.K / 8);         // 16-byte words of x per token
+  const int xw_total = xw_tok * a.M;          // 16-byte words of x
+  const int xw_slots = xw_tok * MT;           // LDS words of x (token slots past M hold zeros)
   const uint32_t xtok = (uint32_t)a.K * 2;    // LDS bytes between tokens
+  // x in LDS: word s of chunk c (SPC words per chunk) sits at word
+  // c * SPC + (s ^ xsw(c)).  The 16 lanes of one LDS cycle read word s of 16
+  // consecutive chunks; without the swizzle, chunks of 4 or more words put
+  // 4 or more of those lanes on the same banks.
+  auto xsw = [](int c) { return (c * SPC / 16) & (SPC - 1); };
+  auto xpos = [&](int w) {  // LDS word of x word w
+    int r = w, m = 0;
+    while (r >= xw_tok) { r -= xw_tok; ++m; }
+    const int c = r / SPC;
+    return m * xw_tok + c * SPC + ((r - c * SPC) ^ xsw(c));
+  };
+  auto xword = [&](int m, int c, int s) {  // LDS address of word s of chunk c of token m
+    return xl + m * xtok + (uint32_t)(c * SPC + (s ^ xsw(c))) * 16;
+  };
   const uint32_t lane_off = repl_lane_off<D>(lane);
   half8_t xreg[kXInRegs ? MT * T * SPC : 1];
   // lane l holds D[4g + i][j]; the diagonal element D[j][j] sits in lane
@@ -569,10 +584,10 @@ __device__ __forceinline__ void gemv_rows_body(const GemvM1Args& a) {
 #pragma unroll
       for (int k = 0; k < XWT; ++k) {
         const int w = threadIdx.x + k * blockDim.x;
-        if (w < xw_slots) reinterpret_cast<u32x4*>(xl)[w] = w < xw_total ? xst[k] : u32x4{0u, 0u, 0u, 0u};
+        if (w < xw_slots) reinterpret_cast<u32x4*>(xl)[xpos(w)] = w < xw_total ? xst[k] : u32x4{0u, 0u, 0u, 0u};
       }
       for (int w = threadIdx.x + XWT * blockDim.x; w < xw_slots; w += blockDim.x)
-        reinterpret_cast<u32x4*>(xl)[w] = w < xw_total ? reinterpret_cast<const u32x4*>(a.x)[w] : u32x4{0u, 0u, 0u, 0u};
+        reinterpret_cast<u32x4*>(xl)[xpos(w)] = w < xw_total ? reinterpret_cast<const u32x4*>(a.x)[w] : u32x4{0u, 0u, 0u, 0u};
     }
     __syncthreads();
 
@@ -585,7 +600,7 @@ __device__ __forceinline__ void gemv_rows_body(const GemvM1Args& a) {
             const bool ok = !MASK || ccol_raw(t) < CH;
 #pragma unroll
             for (int s = 0; s < SPC; ++s) {
-              const half8_t v = *reinterpret_cast<const half8_t*>(xl + m * xtok + ccol(t) * (G * D * 2) + s * 16);
+              const half8_t v = *reinterpret_cast<const half8_t*>(xword(m, ccol(t), s));
               xreg[(m * T + t) * SPC + s] = ok ? v : half8_t{};
             }
           }
@@ -613,7 +628,7 @@ __device__ __forceinline__ void gemv_rows_body(const GemvM1Args& a) {
         for (int m = 0; m < MT; ++m) {
           half8_t bop;
           if constexpr (kXInRegs) bop = xreg[(m * T + t) * SPC + s];
-          else bop = *reinterpret_cast<const half8_t*>(xl + m * xtok + ccol(t) * (G * D * 2) + s * 16);
+          else bop = *reinterpret_cast<const half8_t*>(xword(m, ccol(t), s));
           if (MASK && !cval) bop = half8_t{};
           if constexpr (kDecodeDot) {
             // eight K values: four packed fp16 products-and-adds into fp32
