@@ -514,21 +514,20 @@ __device__ __forceinline__ void gemv_rows_body(const GemvM1Args& a) {
   constexpr int XWT = 2 * MT;
   const int xw_tok = (int)(a.K / 8);         // 16-byte words of x per token
   const int xw_total = xw_tok * a.M;          // 16-byte words of x
-  const int xw_slots = xw_tok * MT;           // LDS words of x (token slots past M hold zeros)
-  const uint32_t xtok = (uint32_t)a.K * 2;    // LDS bytes between tokens
-  // x in LDS: word s of chunk c (SPC words per chunk) sits at word
-  // c * SPC + (s ^ xsw(c)).  The 16 lanes of one LDS cycle read word s of 16
-  // consecutive chunks; without the swizzle, chunks of 4 or more words put
-  // 4 or more of those lanes on the same banks.
-  auto xsw = [](int c) { return (c * SPC / 16) & (SPC - 1); };
+  const int xw_slots = xw_tok * MT;           // words of x staged (token slots past M hold zeros)
+  // x in LDS: one unused word after every 16, so word r of a token sits at
+  // LDS word r + r / 16.  The 16 lanes of one LDS cycle read word s of 16
+  // consecutive chunks (SPC words each); without the padding, chunks of 4 or
+  // more words put 4 or more of those lanes on the same banks.
+  const int xw_tokp = xw_tok + (xw_tok + 15) / 16;  // LDS words per token
   auto xpos = [&](int w) {  // LDS word of x word w
     int r = w, m = 0;
     while (r >= xw_tok) { r -= xw_tok; ++m; }
-    const int c = r / SPC;
-    return m * xw_tok + c * SPC + ((r - c * SPC) ^ xsw(c));
+    return m * xw_tokp + r + (r >> 4);
   };
   auto xword = [&](int m, int c, int s) {  // LDS address of word s of chunk c of token m
-    return xl + m * xtok + (uint32_t)(c * SPC + (s ^ xsw(c))) * 16;
+    const int r = c * SPC;
+    return xl + (m * xw_tokp + r + (r >> 4)) * 16 + s * 16;
   };
   const uint32_t lane_off = repl_lane_off<D>(lane);
   half8_t xreg[kXInRegs ? MT * T * SPC : 1];

@@ -10,7 +10,7 @@
 namespace fasq {
 
 constexpr int kLdsCodebookBudget = 64 * 1024;  // bytes of LDS a codebook may take
-constexpr int kSliceReserve = 8 * 1024;        // LDS kept for row partials beside a codebook slice
+constexpr int kSliceReserve = 4 * 1024;        // LDS kept for row partials beside a codebook slice
 constexpr int kMinSliceBytes = 32 * 1024;      // smaller slices: gather from global memory instead
 constexpr int kReplMinIdsPerEntry = 16;        // replicate the codebook only above this many ids per workgroup and entry
 constexpr int64_t kMtWideXMinRows = 64;        // two tokens: rows per CU from which x takes twice the registers
@@ -526,7 +526,8 @@ hipError_t launch_gemv_m1_bits(const Problem* ps, int count, const DeviceInfo& d
   // workgroup with few ids to gather is faster with one copy.
   if (mode == CB_REPL && (total_rows + dev.num_cus - 1) / dev.num_cus * p.S < kReplMinIdsPerEntry * maxC)
     mode = CB_LDS;
-  const int64_t x_bytes = (MT * p.K * 2 + 15) / 16 * 16;
+  const int64_t xw = p.K / 8;                                  // 16-byte words of x per token
+  const int64_t x_bytes = MT * (xw + (xw + 15) / 16) * 16;     // one unused word after every 16
   int sl_shift = 0;
   if (mode == CB_GLOBAL && (maxC * d * 2) % 16 == 0) {
     const int64_t room = dev.lds_per_block - x_bytes - kSliceReserve;
