@@ -74,6 +74,11 @@ __global__ __launch_bounds__(kSubThreads) void k_gemv_sub(SubArgs a) {
   constexpr int RPL = kWave / NCH;             // rows per wave-wide load
   constexpr int XW = D == 1 ? 1 : D / 2;       // dwords of x per id (D == 1: the low half)
   constexpr int XSB = G * D * 2;               // bytes of one chunk's x slice (one token)
+  // several tokens: x words per token, and LDS words per token with one
+  // unused word after every 16, so that the 16 lanes of one LDS read cycle,
+  // one chunk apart, hit distinct banks
+  constexpr int WPS = NCH * XSB / 16;
+  constexpr int WPSP = WPS + (WPS + 15) / 16;
   static_assert(kWave % NCH == 0 && NCH <= kSubMaxNch, "NCH must divide the wave");
   static_assert(!XL || (D <= 4 && XSB % 16 == 0), "the multi-token kernel takes d <= 4");
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
@@ -124,7 +129,6 @@ __global__ __launch_bounds__(kSubThreads) void k_gemv_sub(SubArgs a) {
   // several tokens: the segment's slice of every row of x (NCH chunks of G
   // ids, zeros past the row) after the books, 16-byte words
   if constexpr (XL) {
-    constexpr int WPS = NCH * XSB / 16;  // words per token
     const int words = (int)a.M * WPS;
     const int64_t seg0 = (int64_t)ks * NCH * G * D;  // first x element of the segment
     for (int w = threadIdx.x; w < words; w += blockDim.x) {
@@ -132,7 +136,7 @@ __global__ __launch_bounds__(kSubThreads) void k_gemv_sub(SubArgs a) {
       const int64_t ch_w = (int64_t)ks * NCH + (k * 16) / XSB;  // chunk of the word
       u32x4 v = u32x4{0u, 0u, 0u, 0u};
       if (ch_w < a.CH) v = *reinterpret_cast<const u32x4*>(a.x + (int64_t)m * a.K + seg0 + (int64_t)k * 8);
-      *reinterpret_cast<u32x4*>(smem + a.x_off + (uint32_t)w * 16) = v;
+      *reinterpret_cast<u32x4*>(smem + a.x_off + (uint32_t)(m * WPSP + k + (k >> 4)) * 16) = v;
     }
   }
   // one token: x of the lane's chunk, G * D halves, in registers
@@ -163,12 +167,13 @@ __global__ __launch_bounds__(kSubThreads) void k_gemv_sub(SubArgs a) {
         for (int q = 0; q < XW; ++q) cw[i][q] = 0u;
         if (cval) read_codeword_lds<D>(((book0 + i) * (uint32_t)a.C + stream_id<BITS>(w, i)) * (2 * D), cw[i]);
       }
-      const uint32_t xs0 = (uint32_t)a.x_off + (uint32_t)c * XSB;
+      const uint32_t cw0 = (uint32_t)c * (XSB / 16);  // first word of the lane's chunk
+      const uint32_t xs0 = (uint32_t)a.x_off + (cw0 + (cw0 >> 4)) * 16;
       for (int m = 0; m < (int)a.M; ++m) {
         uint32_t xs[G * D / 2 > 0 ? G * D / 2 : 1];
 #pragma unroll
         for (int q = 0; q < XSB / 16; ++q) {
-          const u32x4 v = *lds_at<u32x4>(xs0 + (uint32_t)m * (NCH * XSB) + (uint32_t)q * 16);
+          const u32x4 v = *lds_at<u32x4>(xs0 + (uint32_t)m * (WPSP * 16) + (uint32_t)q * 16);
           xs[4 * q] = v[0]; xs[4 * q + 1] = v[1]; xs[4 * q + 2] = v[2]; xs[4 * q + 3] = v[3];
         }
         float acc = 0.f;
@@ -236,6 +241,13 @@ struct SubPlan {
   int64_t rb = 0, rows = 0;
 };
 
+// LDS bytes of the staged x slices of M tokens over nch chunks: one unused
+// 16-byte word after every 16 (see the kernel).
+inline int64_t sub_x_bytes(int64_t M, int nch, int G, int d) {
+  const int64_t wps = (int64_t)nch * G * d * 2 / 16;  // words per token
+  return M * (wps + (wps + 15) / 16) * 16;
+}
+
 bool sub_plan(const Problem& p, const DeviceInfo& dev, SubPlan* out) {
   if (p.M < 1 || p.M > kSubMaxTokens || p.cb_stride != p.C * p.d) return false;
   const int d = p.d;
@@ -250,10 +262,10 @@ bool sub_plan(const Problem& p, const DeviceInfo& dev, SubPlan* out) {
     return false;
   if ((p.N + kWave) * p.R >= (int64_t(1) << 32)) return false;  // loads read up to one load past N
   const int64_t per_chunk = (int64_t)G * p.C * d * 2;  // book bytes per chunk of ids
-  const int64_t x_chunk = p.M > 1 ? p.M * G * d * 2 : 0;  // staged x bytes per chunk (several tokens)
+  auto x_bytes = [&](int n) { return p.M > 1 ? sub_x_bytes(p.M, n, G, d) : 0; };  // staged x (several tokens)
   int nch = kSubMaxNch;
-  while (nch > 1 && (nch * per_chunk > kSubBookBytes || nch * (per_chunk + x_chunk) > dev.lds_per_block)) nch /= 2;
-  if (per_chunk > kSubBookBytes || per_chunk + x_chunk > dev.lds_per_block) return false;
+  while (nch > 1 && (nch * per_chunk > kSubBookBytes || nch * per_chunk + x_bytes(nch) > dev.lds_per_block)) nch /= 2;
+  if (per_chunk > kSubBookBytes || per_chunk + x_bytes(1) > dev.lds_per_block) return false;
   const int64_t CH = p.S / G;
   const int64_t ks = (CH + nch - 1) / nch;
   // row blocks: about one workgroup per CU in all, each with whole loads
@@ -337,7 +349,7 @@ hipError_t launch_gemv_sub(const Problem& p, void* workspace, int64_t workspace_
   a.KS = sp.ks;
   a.rows_per_block = sp.rows;
   a.ws = static_cast<float*>(workspace);
-  const int lds = books + (p.M > 1 ? (int)(p.M * sp.nch * G * p.d * 2) : 0);
+  const int lds = books + (p.M > 1 ? (int)sub_x_bytes(p.M, sp.nch, G, p.d) : 0);
   const int blocks = (int)(sp.rb * sp.ks);
   hipError_t e;
   switch (p.idx_bits) {
